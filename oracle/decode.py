@@ -1,0 +1,55 @@
+"""One decode step of trie-based beam search, in the order of Alg 2 (oracle only).
+
+Per step s (s = 1, 2, ...):
+
+1. from step 2 on, the K/V rows of the current leaves (produced by their forward
+   pass) are written into their nodes;
+2. every live leaf attends over its ancestor path (Section 3.3);
+3. row log-softmax and the global top-b over the n_live x V candidates
+   (``argsort_b`` of Alg 2);
+4. the b chosen continuations are appended (``update_trie``), then the trie is
+   garbage-collected (Section 3.5) - here at every step, i.e. interval g = 1.
+
+Two ways to choose what is appended:
+
+* ``driven``: the top-b selection of step 3 (real beam search);
+* ``scripted``: caller-given (parent rank, token) pairs, scored with the same
+  float32 formula; step 3 still runs and is reported.  This reproduces a fixed
+  trie shape independent of the (synthetic) logits.
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import numpy as np
+
+from .attention import path_attention
+from .beam import pair_scores, select
+from .trie import Trie
+
+
+def decode_step(trie: Trie, step: int, q: Optional[np.ndarray], k_new, v_new, logits: np.ndarray,
+                scale: float, script=None) -> dict:
+    """q / k_new / v_new: [L'][b][..][d] (rows >= n_live unused) or None to skip attention.
+
+    logits: [b][V] (rows >= n_live unused).  script: (parent_rank [b], token [b]) or None.
+    """
+    n_live = trie.n_live
+    if step > 1 and k_new is not None:
+        trie.write_leaf_kv(k_new[:, :n_live], v_new[:, :n_live])
+    out = {}
+    if q is not None:
+        out["o"] = path_attention(trie, q[:, :n_live], scale)
+    sel = select(logits[:n_live], trie.scores, trie.b)
+    out.update(sel)
+    if script is None:
+        par, tok, sc = sel["sel_parent"], sel["sel_token"], sel["sel_score"]
+    else:
+        par, tok = np.asarray(script[0]), np.asarray(script[1])
+        sc, lp = pair_scores(logits[:n_live], sel["lse"], trie.scores, par, tok)
+        out["pair_score"] = sc
+        out["pair_logprob"] = lp
+    trie.append(par, tok, sc)
+    trie.garbage_collect()
+    out["state"] = trie.state()
+    return out

@@ -1,0 +1,125 @@
+"""Planted mistakes in the oracle (CPU only): each must make at least one pin fail.
+
+Every mutant is a plausible slip in code of this kind - a dropped scale, a wrong
+GQA head mapping, an off-by-one window, reversed tie order, a float32 log-sum-exp,
+a missing prune, a wrong mask remap, a wrong parent, a swapped query row, a
+missing window eviction, a wrong row in the pair score.  The pins run on a
+monkeypatched copy of the oracle for the duration of one test.
+"""
+import numpy as np
+import pytest
+
+import pins
+import oracle.attention as oatt
+import oracle.beam as obeam
+import oracle.trie as otrie
+
+
+def _fails(fn, *a, **k):
+    with pytest.raises(AssertionError):
+        fn(*a, **k)
+
+
+def test_mutant_missing_scale(monkeypatch):
+    orig = oatt.softmax_attention
+    monkeypatch.setattr(oatt, "softmax_attention", lambda q, k, v, scale: orig(q, k, v, 1.0))
+    _fails(pins.pin_dense_mask, pins.small_workload(b=3, V=20, steps=3), 0)
+
+
+def test_mutant_gqa_head_mapping(monkeypatch):
+    def bad(trie, q, scale):
+        n_layers, n_live, n_q_heads, d = q.shape
+        out = np.zeros((n_layers, n_live, n_q_heads, d))
+        for i, leaf in enumerate(trie.leaves[:n_live]):
+            path = trie.visible_path(leaf)
+            for li in range(n_layers):
+                kp = np.stack([n.k[li] for n in path]).astype(np.float64)
+                vp = np.stack([n.v[li] for n in path]).astype(np.float64)
+                for h in range(n_q_heads):
+                    g = h % kp.shape[1]
+                    out[li, i, h] = oatt.softmax_attention(q[li, i, h].astype(np.float64),
+                                                           kp[:, g], vp[:, g], scale)
+        return out
+    monkeypatch.setattr(oatt, "path_attention", bad)
+    _fails(pins.pin_dense_mask, pins.small_workload(b=3, V=20, steps=3, Hq=4, Hkv=2), 0)
+
+
+def test_mutant_window_off_by_one(monkeypatch):
+    def bad(self, leaf):
+        return [n for n in self.path(leaf) if self.window == 0 or leaf.depth - n.depth <= self.window]
+    monkeypatch.setattr(otrie.Trie, "visible_path", bad)
+    _fails(pins.pin_window_one, pins.small_workload(b=3, V=30), 1)
+
+
+def test_mutant_reversed_ties(monkeypatch):
+    def bad(s, b):
+        flat = s.ravel()
+        idx = np.arange(flat.size)
+        return np.lexsort((-idx, -flat))[:b]
+    monkeypatch.setattr(obeam, "top_b", bad)
+    _fails(pins.pin_logsoftmax_properties, 2)
+
+
+def test_mutant_float32_lse(monkeypatch):
+    def bad(logits):
+        x = np.asarray(logits, dtype=np.float32)
+        m = x.max(axis=1)
+        return (m + np.log(np.exp(x - m[:, None]).sum(axis=1, dtype=np.float32))).astype(np.float32)
+    monkeypatch.setattr(obeam, "row_lse32", bad)
+    _fails(pins.pin_lse_vs_scipy, 3)
+
+
+def test_mutant_no_prune(monkeypatch):
+    monkeypatch.setattr(otrie.Trie, "garbage_collect", lambda self: None)
+    _fails(pins.pin_batch_equivalence, pins.small_workload(b=3, V=20, steps=6), 4)
+
+
+def test_mutant_mask_remap(monkeypatch):
+    orig = otrie.Trie.append
+
+    def bad(self, parent_rank, token, score):
+        orig(self, parent_rank, token, score)
+        for n in self.order[:-self.b]:  # overwrite with a remap that ignores the parents
+            self.masks[id(n)] = self.masks[id(n)] | 1
+    monkeypatch.setattr(otrie.Trie, "append", bad)
+    _fails(pins.pin_batch_equivalence, pins.small_workload(b=3, V=20, steps=6), 5)
+
+
+def test_mutant_wrong_parent(monkeypatch):
+    orig = otrie.Trie.append
+
+    def bad(self, parent_rank, token, score):
+        orig(self, [j % self.n_live for j in range(self.b)], token, score)
+    monkeypatch.setattr(otrie.Trie, "append", bad)
+    _fails(pins.pin_batch_equivalence, pins.small_workload(b=3, V=20, steps=6), 6)
+
+
+def test_mutant_swapped_query_rows(monkeypatch):
+    orig = oatt.path_attention
+    monkeypatch.setattr(oatt, "path_attention", lambda trie, q, scale: orig(trie, q[:, ::-1], scale))
+    import oracle.decode as odec
+    monkeypatch.setattr(odec, "path_attention", oatt.path_attention)
+    _fails(pins.pin_batch_equivalence, pins.small_workload(b=3, V=20, steps=6), 7)
+
+
+def test_mutant_no_window_eviction(monkeypatch):
+    orig = otrie.Trie.garbage_collect
+
+    def bad(self):
+        w = self.window
+        self.window = 0
+        orig(self)
+        self.window = w
+    monkeypatch.setattr(otrie.Trie, "garbage_collect", bad)
+    _fails(pins.pin_batch_equivalence, pins.small_workload(b=3, V=20, steps=6, W=3), 8)
+
+
+def test_mutant_pair_score_row(monkeypatch):
+    def bad(logits, lse32, scores, parent, token):
+        parent = np.asarray(parent)
+        token = np.asarray(token)
+        x = np.asarray(logits, np.float32)[parent, token]
+        lp = (x - lse32[0]).astype(np.float32)
+        return (np.asarray(scores, np.float32)[parent] + lp).astype(np.float32), lp
+    monkeypatch.setattr(obeam, "pair_scores", bad)
+    _fails(pins.pin_pair_scores, 9)

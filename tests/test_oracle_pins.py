@@ -1,0 +1,78 @@
+"""The CPU oracle against brute force, library routines, closed forms and the paper's counts."""
+import numpy as np
+import pytest
+
+import pins
+import synth
+import oracle.trie as otrie
+import oracle.invariants as oinv
+
+
+@pytest.mark.parametrize("b,V,W,alpha,seed", [
+    (1, 20, 0, 1.0, 0), (2, 10, 0, 1.0, 1), (3, 20, 0, 1.0, 2), (4, 30, 0, 0.0, 3),
+    (6, 50, 0, 1.0, 4), (3, 20, 1, 1.0, 5), (3, 20, 3, 1.0, 6), (5, 12, 3, 0.0, 7),
+])
+def test_trie_equals_batch_beam_search_driven(b, V, W, alpha, seed):
+    w = pins.small_workload(b=b, V=V, W=W, steps=12, alpha=alpha)
+    pins.pin_batch_equivalence(w, seed)
+
+
+@pytest.mark.parametrize("b,W,alpha,seed", [(3, 0, 1.0, 10), (4, 0, 0.0, 11), (4, 3, 1.0, 12),
+                                            (6, 0, 1.0, 13)])
+def test_trie_equals_batch_beam_search_scripted(b, W, alpha, seed):
+    w = pins.small_workload(b=b, V=40, W=W, steps=12, alpha=alpha)
+    pins.pin_batch_equivalence(w, seed, scripted=True)
+
+
+@pytest.mark.parametrize("W,seed", [(0, 20), (3, 21)])
+def test_path_attention_equals_alg3_masked_dense_sdpa(W, seed):
+    pins.pin_dense_mask(pins.small_workload(b=4, V=30, W=W, steps=6), seed)
+
+
+def test_attention_closed_forms():
+    pins.pin_closed_forms(pins.small_workload(b=4, V=30), 30)
+    pins.pin_closed_forms(pins.small_workload(b=4, V=30, W=3), 31)
+
+
+def test_window_one_is_own_row():
+    pins.pin_window_one(pins.small_workload(b=3, V=30), 32)
+
+
+def test_wide_window_is_dense():
+    pins.pin_window_wide(pins.small_workload(b=3, V=30), 33)
+
+
+def test_single_chain_is_causal_greedy():
+    pins.pin_chain_is_causal(pins.small_workload(V=30), 34)
+
+
+def test_lse_matches_scipy_logsumexp():
+    pins.pin_lse_vs_scipy(40)
+
+
+def test_topb_matches_full_enumeration():
+    pins.pin_topb_enumeration(41)
+
+
+def test_pair_scores_match_enumeration():
+    pins.pin_pair_scores(43)
+
+
+def test_logsoftmax_properties_and_ties():
+    pins.pin_logsoftmax_properties(42)
+
+
+def test_fig1_token_counts():
+    pins.pin_fig1_counts()
+
+
+def test_node_count_over_a_long_scripted_run():
+    """N = P + s*b - pruned - evicted over 64 scripted steps of a flat-parent workload."""
+    w = pins.small_workload(b=8, V=64, P=16, steps=64, alpha=0.0, L=1, Hq=1, Hkv=1, d=4)
+    trie = otrie.Trie(np.arange(16), None, None, w.beam_width)
+    for s in range(1, w.steps + 1):
+        par, tok = synth.step_script(w, s, 3)
+        trie.append(par[0], tok[0], np.zeros(w.beam_width, np.float32))
+        trie.garbage_collect()
+        oinv.check(trie)
+    assert trie.pruned > 0
