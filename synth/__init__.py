@@ -187,6 +187,8 @@ def step_script(w: Workload, step: int, seed: int = 0):
     is drawn again.
     """
     n_live = 1 if step == 1 else w.beam_width
+    if n_live * w.vocab < w.beam_width:
+        raise ValueError("fewer distinct (parent, token) pairs than the beam width")
     par = np.empty((w.n_tries, w.beam_width), dtype=np.int32)
     tok = np.empty((w.n_tries, w.beam_width), dtype=np.int32)
     wts = (np.arange(n_live, dtype=np.float64) + 1.0) ** (-w.alpha)

@@ -28,7 +28,7 @@ def test_bf16_rounding_is_nearest_even():
 
 
 def test_script_draws_distinct_pairs_and_respects_live_leaves():
-    w = synth.WORKLOADS["stress"].replace(vocab=3, n_tries=4)
+    w = synth.WORKLOADS["stress"].replace(vocab=20, n_tries=4)
     for step in (1, 2, 7):
         par, tok = synth.step_script(w, step, seed=1)
         n_live = 1 if step == 1 else w.beam_width
