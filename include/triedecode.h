@@ -1,0 +1,178 @@
+/*
+ * triedecode.h - C ABI of the MI355X (gfx950) hot path of trie-based beam search.
+ *
+ * "Efficient Beam Search for LLMs Using Trie-Based Decoding" (arXiv 2502.00085).
+ * One decode step of the method (Alg 2) is three calls, issued in this order on one
+ * HIP stream:
+ *
+ *   trie_attn_decode      every live beam attends over its own root-to-leaf path of
+ *                         the shared, trie-structured KV cache (Section 3.3, Alg 3)
+ *   beam_logsoftmax_topk  row log-softmax and the global top-b over the b x V
+ *                         continuations (the argsort_b of Alg 1 / Alg 2)
+ *   trie_append_prune     append the b chosen children (update_trie / update_mask of
+ *                         Alg 2), then garbage-collect: mark, prune, compact
+ *                         (Section 3.5)
+ *
+ * Memory.  The caller owns every tensor (K/V pools, queries, outputs, logits and
+ * selections) as device memory; PyTorch tensors are the intended source.  The library
+ * owns only the trie metadata and a fixed workspace, both allocated in td_create.  The
+ * three hot calls allocate nothing, never synchronise the host, and are ordered by the
+ * stream they are given.  One context is driven by one stream at a time.
+ *
+ * Layouts (row-major, innermost index last; "cap" = desc.capacity):
+ *   K/V pool   [T][L][Hkv][cap][d]  one node's row of one (layer, KV head) = d elements
+ *   q, out     [nl][T][b][Hq][d]    nl = layers of the call; rows of beams >= n_live
+ *                                   are not read (q) and are written as zeros (out)
+ *   k_new/v_new[nl][T][b][Hkv][d]   K/V of the current leaves (their forward pass)
+ *   logits     [T][b][V] fp32       rows >= n_live are not read
+ *   selections [T][b]               rank order (best first)
+ * Element type of pools, q, out, k_new, v_new: desc.dtype (fp32 or bf16).
+ *
+ * Slots.  Node metadata and K/V rows live at physical slots base .. base+n_nodes-1 of a
+ * trie (base advances when a sliding window evicts the oldest nodes, so evicted rows are
+ * never moved).  Survivors keep their relative order (the paper's index_select
+ * compaction), so node ids and depths never decrease along the slots, and the live
+ * leaves are always the last n_live slots, in rank order.
+ *
+ * Errors.  Argument checks run on the host before any HIP call and return TD_EINVAL
+ * with nothing changed.  A failed HIP launch returns TD_EHIP.  Conditions only the
+ * device can see (parent rank >= n_live, token outside [0, V), duplicate (parent,
+ * token) pairs, slot capacity exceeded) set a sticky device status and leave that
+ * trie unchanged; td_get_status() reads and clears it.  Messages of host-side failures
+ * are available from td_error_string().
+ */
+#ifndef TRIEDECODE_H
+#define TRIEDECODE_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct td_ctx td_ctx;
+
+typedef enum {
+  TD_OK = 0,
+  TD_EINVAL = -1,       /* bad argument or inconsistent call sequence              */
+  TD_ECAPACITY = -2,    /* a trie would exceed desc.capacity node slots            */
+  TD_EHIP = -3,         /* HIP runtime error                                       */
+  TD_ESTATE = -4,       /* call out of order (e.g. append before all layers ran)   */
+  TD_EUNSUPPORTED = -5  /* shape the kernels do not implement (see td_desc)        */
+} td_status;
+
+typedef enum { TD_F32 = 0, TD_BF16 = 1 } td_dtype;
+
+/* Attention kernel choice: AUTO = bf16 -> matrix-core (MFMA) kernel, fp32 -> vector-ALU
+ * kernel.  VALU / MFMA force one (MFMA requires bf16). */
+typedef enum { TD_ATTN_AUTO = 0, TD_ATTN_VALU = 1, TD_ATTN_MFMA = 2 } td_attn_impl;
+
+typedef struct {
+  int32_t n_tries;      /* T >= 1: independent requests decoded together                 */
+  int32_t beam_width;   /* b in [1, 64] (one bit per beam in a 64-bit ancestor mask)      */
+  int32_t capacity;     /* node slots per trie (>= every prompt length + b)              */
+  int32_t vocab;        /* V >= b, V * b < 2^31                                           */
+  int32_t n_layers;     /* L >= 1                                                         */
+  int32_t n_q_heads;    /* Hq, a multiple of Hkv                                          */
+  int32_t n_kv_heads;   /* Hkv >= 1                                                       */
+  int32_t head_dim;     /* d in {64, 96, 128}                                             */
+  int32_t window;       /* sliding window W (0 = dense): key visible iff D - depth < W    */
+  int32_t dtype;        /* td_dtype of pools, q, out, k_new, v_new                        */
+  int32_t attn_impl;    /* td_attn_impl                                                   */
+  void* k_pool;         /* caller-owned device [T][L][Hkv][capacity][d]; valid until      */
+  void* v_pool;         /*   td_destroy                                                   */
+} td_desc;
+
+/* Host view of one trie, in logical slot order (slot i = physical slot base + i).
+ * Arrays are caller-allocated host memory with room for capacity (node arrays) and
+ * beam_width (leaf arrays) entries. */
+typedef struct {
+  int32_t n_nodes;      /* N: stored (live) nodes                                         */
+  int32_t n_live;       /* live leaves (1 after the prompt, b afterwards)                 */
+  int32_t base;         /* physical slot of logical slot 0 (read only)                    */
+  int32_t n_shared;     /* leading slots on every live beam's path (read only)            */
+  int32_t next_id;      /* id of the next appended node (prompt P, then P + s*b)          */
+  int32_t kv_pending;   /* 1: the leaves' K/V rows are not yet in the pools; the next     */
+                        /*    trie_attn_decode call(s) must pass k_new/v_new              */
+  int32_t* node_id;     /* [N] prompt token j -> j; step s rank j -> P + (s-1)*b + j     */
+  int32_t* parent_slot; /* [N] logical slot of the parent, -1 for a root                 */
+  int32_t* token;       /* [N]                                                            */
+  int32_t* depth;       /* [N] position in the equivalent per-beam sequence (Section 3.4) */
+  uint64_t* mask;       /* [N] bit i set <=> slot lies on live leaf i's path (Alg 3)      */
+  int32_t* leaf_slot;   /* [n_live] logical slots of the live leaves, rank order          */
+  float* leaf_score;    /* [n_live] cumulative log-probability of each live leaf          */
+} td_state;
+
+/* Create a context: validates desc, allocates trie metadata and workspace on the
+ * current device (synchronous).  Tries start empty; call td_init_prompt or
+ * td_load_state before decoding. */
+td_status td_create(const td_desc* desc, td_ctx** out);
+td_status td_destroy(td_ctx* ctx);
+
+/* Initialise every trie from its prompt (Alg 2: initialize_trie): prompt token j of
+ * trie t becomes node j at slot j with depth j, parent j-1 and mask bit 0; the prompt
+ * tail is the single live leaf with score 0.  h_prompt_len: host [T], each in
+ * [1, capacity - b].  d_tokens: device int32, token j of trie t at d_tokens[t*stride+j].
+ * The caller writes the prompt's K/V rows (its prefill) into pool slots 0..P_t-1. */
+td_status td_init_prompt(td_ctx* ctx, const int32_t* h_prompt_len, const int32_t* d_tokens,
+                         int32_t tokens_stride, hipStream_t stream);
+
+/* Section 3.3: for layers [layer_begin, layer_begin+n_layers), every trie t, live leaf i
+ * and query head h:  out = softmax(scale * q . K_P^T) V_P  over the nodes P on leaf i's
+ * root-to-leaf path (Alg 3 mask) with D - depth < W when a window is set; query head h
+ * reads KV head h / (Hq/Hkv).  When the leaves' K/V are pending (after an append), the
+ * call first stores k_new/v_new into the leaves' pool rows and the leaves attend to
+ * them; otherwise d_k_new/d_v_new must be NULL.  fp32 accumulation; out rows of beams
+ * >= n_live are zeroed.  scale is normally 1/sqrt(d). */
+td_status trie_attn_decode(td_ctx* ctx, int32_t layer_begin, int32_t n_layers, const void* d_q,
+                           const void* d_k_new, const void* d_v_new, void* d_out, float scale,
+                           hipStream_t stream);
+
+/* Alg 1 / Alg 2 top-b with cumulative log-probability scores.  For every trie, row r <
+ * n_live:  lse_r = fp32 rounding of the fp64 log-sum-exp of the row;  per candidate
+ * (r, v):  lp = fl32(x - lse_r),  s = fl32(leaf_score_r + lp)  (IEEE round to nearest
+ * even).  The b best candidates by (s descending, flat index r*V+v ascending) are written
+ * in that order: sel_parent = r (leaf rank), sel_token = v, sel_score = s,
+ * sel_logprob = lp, each [T][b].  d_lse ([T][b], may be NULL) receives lse_r.
+ * Optional scoring of caller-chosen pairs (d_pair_parent/d_pair_token [T][b], both
+ * NULL or both set): d_pair_score receives s of each pair by the same formula.
+ * Reads n_live and leaf scores from the context on the device. */
+td_status beam_logsoftmax_topk(td_ctx* ctx, const float* d_logits, int32_t* d_sel_parent,
+                               int32_t* d_sel_token, float* d_sel_score, float* d_sel_logprob,
+                               float* d_lse, const int32_t* d_pair_parent,
+                               const int32_t* d_pair_token, float* d_pair_score,
+                               hipStream_t stream);
+
+/* Alg 2 update_trie + update_mask, then Section 3.5 garbage collection (every call).
+ * New node j (j < b) is a child of live leaf sel_parent[j] with token sel_token[j],
+ * score sel_score[j], depth D+1 and id next_id+j; every stored node's mask is remapped
+ * (new bit j = old bit sel_parent[j]).  A node dies when its new mask is 0 (no live leaf
+ * reaches it) or, with a window, when depth <= D+1-W.  Survivors are compacted stably
+ * (parent slots remapped, -1 if the parent died) and the K/V rows of moved survivors are
+ * copied to their new slots in every layer and KV head.  The new leaves become the last
+ * b slots in rank j order; their K/V rows are pending until the next trie_attn_decode.
+ * Inputs [T][b] device.  Invalid selections / capacity overflow: sticky device status,
+ * trie unchanged. */
+td_status trie_append_prune(td_ctx* ctx, const int32_t* d_sel_parent, const int32_t* d_sel_token,
+                            const float* d_sel_score, hipStream_t stream);
+
+/* Copy trie t to the host (synchronises the device). */
+td_status td_read_state(td_ctx* ctx, int32_t trie, td_state* host_out);
+/* Replace trie t by a host state (synchronous).  Slots are placed at base 0.  The state
+ * must be one the method can produce: depth non-decreasing along slots, parents before
+ * children with depth + 1, leaves = last n_live slots in rank order with one-hot masks,
+ * the all-beam (shared) slots a prefix.  The pools must hold the K/V rows of every slot
+ * (except the leaves' when kv_pending = 1). */
+td_status td_load_state(td_ctx* ctx, int32_t trie, const td_state* host_in);
+/* Read and clear the sticky device status (synchronises the device). */
+td_status td_get_status(td_ctx* ctx);
+/* Last host-side error message of ctx ("" if none); valid until the next call on ctx. */
+const char* td_error_string(const td_ctx* ctx);
+/* Symbolic name of a td_status value. */
+const char* td_status_name(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TRIEDECODE_H */

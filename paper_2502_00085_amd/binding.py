@@ -1,0 +1,272 @@
+"""ctypes binding of libtriedecode.so: the C ABI's calls under the same names.
+
+Argument marshalling only: torch tensors are checked for device, dtype, contiguity and
+element count (so that no kernel is launched on a buffer smaller than it reads or
+writes), then passed as raw device pointers together with the current HIP stream.
+All computation happens in the library's kernels.  There is no fallback: if the
+library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtriedecode.so")
+
+TD_OK, TD_EINVAL, TD_ECAPACITY, TD_EHIP, TD_ESTATE, TD_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+TD_F32, TD_BF16 = 0, 1
+TD_ATTN_AUTO, TD_ATTN_VALU, TD_ATTN_MFMA = 0, 1, 2
+
+
+class TdDesc(ctypes.Structure):
+    _fields_ = [("n_tries", ctypes.c_int32), ("beam_width", ctypes.c_int32),
+                ("capacity", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("n_layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("window", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("attn_impl", ctypes.c_int32),
+                ("k_pool", ctypes.c_void_p), ("v_pool", ctypes.c_void_p)]
+
+
+class TdState(ctypes.Structure):
+    _fields_ = [("n_nodes", ctypes.c_int32), ("n_live", ctypes.c_int32), ("base", ctypes.c_int32),
+                ("n_shared", ctypes.c_int32), ("next_id", ctypes.c_int32),
+                ("kv_pending", ctypes.c_int32),
+                ("node_id", ctypes.POINTER(ctypes.c_int32)),
+                ("parent_slot", ctypes.POINTER(ctypes.c_int32)),
+                ("token", ctypes.POINTER(ctypes.c_int32)),
+                ("depth", ctypes.POINTER(ctypes.c_int32)),
+                ("mask", ctypes.POINTER(ctypes.c_uint64)),
+                ("leaf_slot", ctypes.POINTER(ctypes.c_int32)),
+                ("leaf_score", ctypes.POINTER(ctypes.c_float))]
+
+
+class TdError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{status_name(status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with python -m paper_2502_00085_amd.build")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
+        L.td_create.argtypes = [ctypes.POINTER(TdDesc), ctypes.POINTER(vp)]
+        L.td_destroy.argtypes = [vp]
+        L.td_init_prompt.argtypes = [vp, ctypes.POINTER(i32), vp, i32, vp]
+        L.trie_attn_decode.argtypes = [vp, i32, i32, vp, vp, vp, vp, f32, vp]
+        L.beam_logsoftmax_topk.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.trie_append_prune.argtypes = [vp, vp, vp, vp, vp]
+        L.td_read_state.argtypes = [vp, i32, ctypes.POINTER(TdState)]
+        L.td_load_state.argtypes = [vp, i32, ctypes.POINTER(TdState)]
+        L.td_get_status.argtypes = [vp]
+        L.td_error_string.argtypes = [vp]
+        L.td_error_string.restype = ctypes.c_char_p
+        L.td_status_name.argtypes = [i32]
+        L.td_status_name.restype = ctypes.c_char_p
+        for name in ("td_create", "td_destroy", "td_init_prompt", "trie_attn_decode",
+                     "beam_logsoftmax_topk", "trie_append_prune", "td_read_state", "td_load_state",
+                     "td_get_status"):
+            getattr(L, name).restype = ctypes.c_int32
+        _lib = L
+    return _lib
+
+
+def status_name(s: int) -> str:
+    return lib().td_status_name(int(s)).decode()
+
+
+def _check(ctx, st: int):
+    if st != TD_OK:
+        msg = lib().td_error_string(ctx).decode() if ctx is not None or st != TD_OK else ""
+        raise TdError(st, msg)
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _ptr(t, dtype=None, numel=None, name="tensor"):
+    if t is None:
+        return None
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous device tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} must have {numel} elements, got {t.numel()}")
+    return t.data_ptr()
+
+
+# ---------------------------------------------------------------------------------------------
+# the C ABI, one function per entry point
+# ---------------------------------------------------------------------------------------------
+def td_create(desc: TdDesc):
+    ctx = ctypes.c_void_p()
+    st = lib().td_create(ctypes.byref(desc), ctypes.byref(ctx))
+    if st != TD_OK:
+        raise TdError(st, lib().td_error_string(None).decode())
+    return ctx
+
+
+def td_destroy(ctx):
+    _check(None, lib().td_destroy(ctx))
+
+
+def td_init_prompt(ctx, prompt_len: Sequence[int], tokens, stream=None):
+    import torch
+    plen = np.ascontiguousarray(np.asarray(prompt_len, dtype=np.int32))
+    if tokens.dim() != 2 or tokens.shape[0] != plen.size:
+        raise ValueError("tokens must be [T][stride]")
+    _ptr(tokens, torch.int32, name="tokens")
+    _check(ctx, lib().td_init_prompt(ctx, plen.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                     tokens.data_ptr(), int(tokens.shape[1]), _stream(stream)))
+
+
+class Dims:
+    """Shape bookkeeping of one context (for the binding's element-count checks)."""
+
+    def __init__(self, desc: TdDesc):
+        self.T, self.b, self.cap, self.V = desc.n_tries, desc.beam_width, desc.capacity, desc.vocab
+        self.L, self.Hq, self.Hkv, self.D = desc.n_layers, desc.n_q_heads, desc.n_kv_heads, desc.head_dim
+        self.dtype = desc.dtype
+
+
+def trie_attn_decode(ctx, dims: Dims, layer_begin: int, n_layers: int, q, k_new, v_new, out,
+                     scale: float, stream=None):
+    import torch
+    tdt = torch.float32 if dims.dtype == TD_F32 else torch.bfloat16
+    nq = n_layers * dims.T * dims.b * dims.Hq * dims.D
+    nk = n_layers * dims.T * dims.b * dims.Hkv * dims.D
+    _check(ctx, lib().trie_attn_decode(
+        ctx, int(layer_begin), int(n_layers), _ptr(q, tdt, nq, "q"), _ptr(k_new, tdt, nk, "k_new"),
+        _ptr(v_new, tdt, nk, "v_new"), _ptr(out, tdt, nq, "out"), float(scale), _stream(stream)))
+
+
+def beam_logsoftmax_topk(ctx, dims: Dims, logits, sel_parent, sel_token, sel_score, sel_logprob,
+                         lse=None, pair_parent=None, pair_token=None, pair_score=None, stream=None):
+    import torch
+    tb = dims.T * dims.b
+    _check(ctx, lib().beam_logsoftmax_topk(
+        ctx, _ptr(logits, torch.float32, tb * dims.V, "logits"),
+        _ptr(sel_parent, torch.int32, tb, "sel_parent"), _ptr(sel_token, torch.int32, tb, "sel_token"),
+        _ptr(sel_score, torch.float32, tb, "sel_score"),
+        _ptr(sel_logprob, torch.float32, tb, "sel_logprob"), _ptr(lse, torch.float32, tb, "lse"),
+        _ptr(pair_parent, torch.int32, tb, "pair_parent"), _ptr(pair_token, torch.int32, tb, "pair_token"),
+        _ptr(pair_score, torch.float32, tb, "pair_score"), _stream(stream)))
+
+
+def trie_append_prune(ctx, dims: Dims, sel_parent, sel_token, sel_score, stream=None):
+    import torch
+    tb = dims.T * dims.b
+    _check(ctx, lib().trie_append_prune(
+        ctx, _ptr(sel_parent, torch.int32, tb, "sel_parent"), _ptr(sel_token, torch.int32, tb, "sel_token"),
+        _ptr(sel_score, torch.float32, tb, "sel_score"), _stream(stream)))
+
+
+def td_read_state(ctx, dims: Dims, trie: int) -> dict:
+    cap, b = dims.cap, dims.b
+    arrs = {k: np.zeros(cap, np.int32) for k in ("node_id", "parent_slot", "token", "depth")}
+    arrs["mask"] = np.zeros(cap, np.uint64)
+    arrs["leaf_slot"] = np.zeros(b, np.int32)
+    arrs["leaf_score"] = np.zeros(b, np.float32)
+    st = TdState()
+    for k, a in arrs.items():
+        setattr(st, k, a.ctypes.data_as(ctypes.POINTER(np.ctypeslib.as_ctypes_type(a.dtype))))
+    _check(ctx, lib().td_read_state(ctx, int(trie), ctypes.byref(st)))
+    n, nl = st.n_nodes, st.n_live
+    out = {k: arrs[k][:n].copy() for k in ("node_id", "parent_slot", "token", "depth", "mask")}
+    out["leaf_slot"] = arrs["leaf_slot"][:nl].copy()
+    out["leaf_score"] = arrs["leaf_score"][:nl].copy()
+    out.update(n_nodes=n, n_live=nl, base=st.base, n_shared=st.n_shared, next_id=st.next_id,
+               kv_pending=st.kv_pending)
+    return out
+
+
+def td_load_state(ctx, dims: Dims, trie: int, state: dict):
+    keep = {}
+    st = TdState()
+    st.n_nodes, st.n_live = int(state["n_nodes"]), int(state["n_live"])
+    st.next_id, st.kv_pending = int(state["next_id"]), int(state.get("kv_pending", 0))
+    for k, dt in (("node_id", np.int32), ("parent_slot", np.int32), ("token", np.int32),
+                  ("depth", np.int32), ("mask", np.uint64), ("leaf_slot", np.int32),
+                  ("leaf_score", np.float32)):
+        a = np.ascontiguousarray(np.asarray(state[k], dtype=dt))
+        keep[k] = a
+        setattr(st, k, a.ctypes.data_as(ctypes.POINTER(np.ctypeslib.as_ctypes_type(a.dtype))))
+    _check(ctx, lib().td_load_state(ctx, int(trie), ctypes.byref(st)))
+
+
+def td_get_status(ctx) -> int:
+    return int(lib().td_get_status(ctx))
+
+
+def td_error_string(ctx) -> str:
+    return lib().td_error_string(ctx).decode()
+
+
+# ---------------------------------------------------------------------------------------------
+# convenience wrapper: owns the pools (torch tensors) and one context
+# ---------------------------------------------------------------------------------------------
+class TrieDecoder:
+    """One context plus its caller-owned K/V pools, allocated as torch tensors on the device."""
+
+    def __init__(self, n_tries, beam_width, capacity, vocab, n_layers, n_q_heads, n_kv_heads,
+                 head_dim, window=0, dtype="bf16", attn_impl=TD_ATTN_AUTO, device="cuda"):
+        import torch
+        self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+        shape = (n_tries, n_layers, n_kv_heads, capacity, head_dim)
+        self.k_pool = torch.zeros(shape, dtype=self.tdtype, device=device)
+        self.v_pool = torch.zeros(shape, dtype=self.tdtype, device=device)
+        self.desc = TdDesc(n_tries, beam_width, capacity, vocab, n_layers, n_q_heads, n_kv_heads,
+                           head_dim, window, TD_BF16 if dtype == "bf16" else TD_F32, attn_impl,
+                           self.k_pool.data_ptr(), self.v_pool.data_ptr())
+        self.dims = Dims(self.desc)
+        self.ctx = td_create(self.desc)
+
+    def close(self):
+        if self.ctx is not None:
+            td_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def init_prompt(self, prompt_len, tokens, stream=None):
+        td_init_prompt(self.ctx, prompt_len, tokens, stream)
+
+    def attn_decode(self, layer_begin, n_layers, q, k_new, v_new, out, scale, stream=None):
+        trie_attn_decode(self.ctx, self.dims, layer_begin, n_layers, q, k_new, v_new, out, scale, stream)
+
+    def logsoftmax_topk(self, logits, sel_parent, sel_token, sel_score, sel_logprob, lse=None,
+                        pair_parent=None, pair_token=None, pair_score=None, stream=None):
+        beam_logsoftmax_topk(self.ctx, self.dims, logits, sel_parent, sel_token, sel_score, sel_logprob,
+                             lse, pair_parent, pair_token, pair_score, stream)
+
+    def append_prune(self, sel_parent, sel_token, sel_score, stream=None):
+        trie_append_prune(self.ctx, self.dims, sel_parent, sel_token, sel_score, stream)
+
+    def read_state(self, trie=0):
+        return td_read_state(self.ctx, self.dims, trie)
+
+    def load_state(self, trie, state):
+        td_load_state(self.ctx, self.dims, trie, state)
+
+    def status(self):
+        return td_get_status(self.ctx)

@@ -1,0 +1,68 @@
+// Pieces shared by the two trie-attention kernels (vector-ALU and matrix-core).
+#pragma once
+
+#include "td_internal.h"
+
+namespace td {
+
+// Work unit of one attention WG: (trie, layer of the call, KV head, row block, split).
+struct AttnUnit {
+  int t, li, g, rb, split;
+};
+
+__device__ inline AttnUnit attn_unit(const DevState& s, const AttnArgs& a) {
+  int x = blockIdx.x;
+  AttnUnit u;
+  u.split = x % a.splits;
+  x /= a.splits;
+  u.rb = x % a.row_blocks;
+  x /= a.row_blocks;
+  u.g = x % s.Hkv;
+  x /= s.Hkv;
+  u.li = x % a.n_layers;
+  u.t = x / a.n_layers;
+  return u;
+}
+
+// First logical slot inside the sliding window of a query at depth D (depth is
+// non-decreasing along the slots): the smallest n with D - depth[n] < W.
+__device__ inline int window_lo(const DevState& s, int t, int base, int N, int D) {
+  if (s.W <= 0) return 0;
+  const int32_t* dep = s.depth + (size_t)t * s.cap + base;
+  int lo = 0, hi = N;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (D - dep[mid] >= s.W) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+// Pool row of (trie t, absolute layer l, KV head g, physical slot p), in elements.
+__device__ inline size_t pool_row(const DevState& s, int t, int l, int g, int p) {
+  return ((((size_t)t * s.L + l) * s.Hkv + g) * s.cap + p) * s.D;
+}
+
+// Stores the pending leaves' K/V rows of one (trie, layer, KV head) into the pools
+// (16-byte chunks, whole block).
+template <typename T>
+__device__ inline void store_leaf_kv(const DevState& s, const AttnArgs& a, const AttnUnit& u,
+                                     int base, int N, int n_live) {
+  const int chunks = s.D * (int)sizeof(T) / 16;
+  const int lab = a.layer_begin + u.li;
+  const T* kn = static_cast<const T*>(a.k_new);
+  const T* vn = static_cast<const T*>(a.v_new);
+  T* kp = static_cast<T*>(s.k_pool);
+  T* vp = static_cast<T*>(s.v_pool);
+  for (int c = threadIdx.x; c < 2 * n_live * chunks; c += blockDim.x) {
+    const int which = c / (n_live * chunks);
+    const int j = (c / chunks) % n_live;
+    const int k = c % chunks;
+    const size_t src = ((((size_t)u.li * s.T + u.t) * s.b + j) * s.Hkv + u.g) * s.D;
+    const size_t dst = pool_row(s, u.t, lab, u.g, base + N - n_live + j);
+    const uint4* from = reinterpret_cast<const uint4*>((which ? vn : kn) + src) + k;
+    uint4* to = reinterpret_cast<uint4*>((which ? vp : kp) + dst) + k;
+    *to = *from;
+  }
+}
+
+}  // namespace td

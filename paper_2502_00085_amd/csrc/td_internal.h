@@ -1,0 +1,89 @@
+// Internal definitions shared by the host ABI (ctx.cpp) and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "triedecode.h"
+
+namespace td {
+
+// Per-trie header kept in device memory (one per trie).
+struct TrieHdr {
+  int32_t n_nodes;     // stored nodes N
+  int32_t base;        // physical slot of logical slot 0
+  int32_t n_live;      // live leaves (last n_live logical slots, rank order)
+  int32_t n_shared;    // leading logical slots that lie on every live leaf's path
+  int32_t leaf_depth;  // depth D of every live leaf
+  int32_t next_id;     // id given to the next appended node of rank 0
+  int32_t pad0, pad1;
+};
+
+// Device-side pointers of one context.  Node arrays are [T][cap], indexed by physical slot.
+struct DevState {
+  int T, b, cap, V, L, Hq, Hkv, D, W, dtype;
+  void* k_pool;
+  void* v_pool;
+  TrieHdr* hdr;          // [T]
+  int32_t* node_id;      // [T][cap]
+  int32_t* parent;       // [T][cap] physical slot of the parent or -1
+  int32_t* token;        // [T][cap]
+  int32_t* depth;        // [T][cap]
+  uint64_t* mask;        // [T][cap]
+  float* leaf_score;     // [T][b]
+  int32_t* status;       // sticky device status (first error wins)
+  // workspace
+  double* lse_part;      // [T][b][lse_chunks][2]  (chunk max, chunk sum of exp)
+  uint64_t* topk_keys;   // [T][sel_chunks][b]
+  int32_t* topk_count;   // [T] arrival counters of the select kernel (self-resetting)
+  int32_t* newpos;       // [T][cap] new logical position of each old logical slot, -1 dead
+  int2* moves;           // [T][cap] (src phys, dst phys) rows to move, ascending src
+  int32_t* n_moves;      // [T]
+  float* attn_part;      // split-combine partials
+  int32_t* attn_count;   // [pairs] arrival counters of split WGs (self-resetting)
+  int lse_chunks, sel_chunks, attn_part_floats, attn_pairs_max;
+};
+
+// selection / log-softmax geometry
+constexpr int kLseChunk = 4096;      // logits per WG in the log-sum-exp pass
+constexpr int kSelThreads = 256;
+constexpr int kSelPerThread = 32;
+constexpr int kSelChunk = kSelThreads * kSelPerThread;  // candidates per WG in the select pass
+constexpr int kMaxBeam = 64;
+
+// status codes written by kernels (same values as td_status)
+constexpr int kDevEinval = TD_EINVAL;
+constexpr int kDevEcapacity = TD_ECAPACITY;
+
+struct AttnArgs {
+  const void* q;
+  const void* k_new;
+  const void* v_new;
+  void* out;
+  int layer_begin, n_layers;
+  float scale_log2;      // scale * log2(e)
+  int kv_pending;
+  int splits;            // WGs per (trie, layer, kv head, row block) along the node axis
+  int row_blocks;        // ceil(b * G / rows_per_block)
+};
+
+hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const int32_t* d_tokens,
+                              int stride, hipStream_t st);
+hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st);
+hipError_t launch_attn_valu(const DevState& s, const AttnArgs& a, hipStream_t st);
+int attn_mfma_rows_per_block();
+int attn_valu_rows_per_block();
+int attn_choose_splits(const DevState& s, int n_layers, int row_blocks);
+hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_t* sel_parent,
+                                  int32_t* sel_token, float* sel_score, float* sel_logprob,
+                                  float* lse, const int32_t* pair_parent, const int32_t* pair_token,
+                                  float* pair_score, hipStream_t st);
+hipError_t launch_append_prune(const DevState& s, const int32_t* sel_parent,
+                               const int32_t* sel_token, const float* sel_score, hipStream_t st);
+
+// ---------------------------------------------------------------------------------------
+// small device helpers
+// ---------------------------------------------------------------------------------------
+__device__ inline void set_status(int32_t* status, int code) { atomicCAS(status, 0, code); }
+
+}  // namespace td

@@ -1,0 +1,274 @@
+// Row log-softmax and the global top-b of beam search (gfx950).
+//
+// Alg 1 / Alg 2 keep the b best continuations; a beam's score is its cumulative
+// log-probability.  Arithmetic (identical to the CPU oracle, bit for bit):
+//   lse_r = fl32( m_r + log(sum_v exp(x_rv - m_r)) )   accumulated in fp64
+//   lp    = fl32(x - lse_r),   s = fl32(score_r + lp)   (round to nearest even)
+// Candidates are ranked by the 64-bit key  (ord(s) << 32) | (2^32 - 1 - (r*V + v)),
+// where ord() maps floats to order-preserving unsigned integers: a larger key is a
+// better candidate and equal scores go to the lower flat index.  Keys are unique.
+//
+// Kernels:
+//   k_lse_partials  grid (lse_chunks, b, T): max and fp64 sum of exp of a 4096-logit chunk
+//   k_select        grid (sel_chunks, T): lse of the rows it touches (from the partials),
+//                   keys of 8192 candidates, the WG's top-b; the last WG of a trie to
+//                   finish merges all WGs' top-b lists into the final selection.
+// Top-b of a set split into groups (threads or WGs) whose maxima are known: the b-th
+// largest group maximum is a lower bound of the b-th largest key, so only keys at or
+// above it (at most b groups' worth) are ranked, each by counting larger candidates.
+#include "td_internal.h"
+
+namespace td {
+
+namespace {
+
+__device__ inline uint32_t float_ord(float f) {
+  if (f == 0.0f) f = 0.0f;  // -0 and +0 compare equal: give them one key
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ inline float wave_max_f(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ inline double wave_sum_d(double v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+constexpr int kLseThreads = 256;
+constexpr int kLsePer = kLseChunk / kLseThreads;
+
+__global__ __launch_bounds__(kLseThreads) void k_lse_partials(DevState s, const float* logits) {
+  const int c = blockIdx.x, r = blockIdx.y, t = blockIdx.z;
+  if (r >= s.hdr[t].n_live) return;
+  const float* row = logits + ((size_t)t * s.b + r) * s.V;
+  const int v0 = c * kLseChunk;
+  float x[kLsePer];
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < kLsePer; ++i) {
+    const int v = v0 + i * kLseThreads + threadIdx.x;
+    x[i] = v < s.V ? row[v] : -INFINITY;
+    m = fmaxf(m, x[i]);
+  }
+  __shared__ float wm[kLseThreads / 64];
+  __shared__ double ws[kLseThreads / 64];
+  m = wave_max_f(m);
+  if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
+  __syncthreads();
+  m = wm[0];
+  for (int w = 1; w < kLseThreads / 64; ++w) m = fmaxf(m, wm[w]);
+  double acc = 0.0;
+  const double md = (double)m;
+#pragma unroll
+  for (int i = 0; i < kLsePer; ++i) {
+    const int v = v0 + i * kLseThreads + threadIdx.x;
+    if (v < s.V) acc += exp((double)x[i] - md);
+  }
+  acc = wave_sum_d(acc);
+  if ((threadIdx.x & 63) == 0) ws[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double tot = 0.0;
+    for (int w = 0; w < kLseThreads / 64; ++w) tot += ws[w];
+    double* p = s.lse_part + (((size_t)t * s.b + r) * s.lse_chunks + c) * 2;
+    p[0] = md;
+    p[1] = tot;
+  }
+}
+
+// fp64 log-sum-exp of row r from its chunk partials (fixed order: bit-reproducible)
+__device__ inline float row_lse32(const DevState& s, int t, int r) {
+  const double* p = s.lse_part + ((size_t)t * s.b + r) * s.lse_chunks * 2;
+  const int nch = (s.V + kLseChunk - 1) / kLseChunk;
+  double M = p[0];
+  for (int c = 1; c < nch; ++c) M = fmax(M, p[2 * c]);
+  double S = 0.0;
+  for (int c = 0; c < nch; ++c) S += p[2 * c + 1] * exp(p[2 * c] - M);
+  return (float)(M + log(S));
+}
+
+__device__ inline float cand_score(float x, float lse, float score, float* lp_out) {
+  const float lp = __fsub_rn(x, lse);
+  *lp_out = lp;
+  return __fadd_rn(score, lp);
+}
+
+__device__ inline uint64_t make_key(float s, uint32_t flat) {
+  return ((uint64_t)float_ord(s) << 32) | (uint64_t)(0xffffffffu - flat);
+}
+
+constexpr int kCandMax = 4096;
+
+// Rank candidates cand[0..n) by counting larger keys; writes the b best in order to out.
+__device__ inline void rank_topb(const uint64_t* cand, int n, int b, uint64_t* out) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const uint64_t k = cand[i];
+    int rank = 0;
+    for (int j = 0; j < n; ++j) rank += cand[j] > k;
+    if (rank < b) out[rank] = k;
+  }
+}
+
+// b-th largest value among gmax[0..n) (n >= 1): the smallest of the values whose count of
+// strictly larger values is < b.  Zero entries (empty groups) are allowed.
+__device__ inline uint64_t bth_largest(const uint64_t* gmax, int n, int b, uint64_t* red) {
+  uint64_t mine = ~0ull;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const uint64_t k = gmax[i];
+    int rank = 0;
+    for (int j = 0; j < n; ++j) rank += gmax[j] > k;
+    if (rank < b) mine = min(mine, k);
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t other = __shfl_xor(mine, o);
+    mine = min(mine, other);
+  }
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mine;
+  __syncthreads();
+  uint64_t r = red[0];
+  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) r = min(r, red[w]);
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float* logits,
+                                                        int32_t* sel_parent, int32_t* sel_token,
+                                                        float* sel_score, float* sel_logprob,
+                                                        float* lse_out, const int32_t* pair_parent,
+                                                        const int32_t* pair_token,
+                                                        float* pair_score) {
+  const int c = blockIdx.x, t = blockIdx.y;
+  const int b = s.b, V = s.V;
+  const int n_live = s.hdr[t].n_live;
+  const int total = n_live * V;
+  const int n_active = (total + kSelChunk - 1) / kSelChunk;
+  if (c >= n_active) return;
+
+  __shared__ uint64_t gmax[kSelThreads];
+  __shared__ uint64_t cand[kCandMax];
+  __shared__ uint64_t red[kSelThreads / 64];
+  __shared__ uint64_t best[kMaxBeam];
+  __shared__ float row_lse[kMaxBeam];
+  __shared__ int ncand, ticket;
+
+  const int f0 = c * kSelChunk;
+  const int f1 = min(total, f0 + kSelChunk);
+  const int r_lo = f0 / V, r_hi = (f1 - 1) / V;
+  for (int r = r_lo + (int)threadIdx.x; r <= r_hi; r += kSelThreads) row_lse[r - r_lo] = row_lse32(s, t, r);
+  if (threadIdx.x == 0) ncand = 0;
+  __syncthreads();
+
+  // keys of this WG's candidates (contiguous per thread-iteration for coalescing)
+  uint64_t key[kSelPerThread];
+  uint64_t kmax = 0;
+  const float* lrow = logits + (size_t)t * s.b * V;
+  const float* scores = s.leaf_score + (size_t)t * b;
+#pragma unroll
+  for (int i = 0; i < kSelPerThread; ++i) {
+    const int f = f0 + i * kSelThreads + threadIdx.x;
+    uint64_t k = 0;
+    if (f < f1) {
+      const int r = f / V;
+      float lp;
+      const float sc = cand_score(lrow[f], row_lse[r - r_lo], scores[r], &lp);
+      k = make_key(sc, (uint32_t)f);
+    }
+    key[i] = k;
+    kmax = max(kmax, k);
+  }
+  gmax[threadIdx.x] = kmax;
+  __syncthreads();
+  const uint64_t thr = bth_largest(gmax, kSelThreads, b, red);
+#pragma unroll
+  for (int i = 0; i < kSelPerThread; ++i) {
+    if (key[i] != 0 && key[i] >= thr) {
+      const int slot = atomicAdd(&ncand, 1);
+      cand[slot] = key[i];  // at most b threads hold keys >= thr: <= 32 b <= kCandMax
+    }
+  }
+  for (int j = threadIdx.x; j < b; j += kSelThreads) best[j] = 0;
+  __syncthreads();
+  rank_topb(cand, ncand, b, best);
+  __syncthreads();
+  uint64_t* my = s.topk_keys + ((size_t)t * s.sel_chunks + c) * b;
+  for (int j = threadIdx.x; j < b; j += kSelThreads) my[j] = best[j];
+
+  // arrival: the last WG of trie t merges
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) ticket = atomicAdd(&s.topk_count[t], 1);
+  __syncthreads();
+  if (ticket != n_active - 1) return;
+  __threadfence();
+  if (threadIdx.x == 0) {
+    s.topk_count[t] = 0;
+    ncand = 0;
+  }
+  const uint64_t* all = s.topk_keys + (size_t)t * s.sel_chunks * b;
+  // group maxima = first (largest) key of every WG list; at most kSelThreads per pass
+  uint64_t* gm = cand;  // reuse: group maxima of up to kCandMax WGs
+  for (int i = threadIdx.x; i < n_active; i += kSelThreads) gm[i] = all[(size_t)i * b];
+  __syncthreads();
+  const uint64_t thr2 = bth_largest(gm, n_active, b, red);
+  __syncthreads();
+  uint64_t* cand2 = cand;  // overwrite after the threshold is known
+  for (int i = threadIdx.x; i < n_active * b; i += kSelThreads) {
+    const uint64_t k = all[i];
+    if (k != 0 && k >= thr2) {
+      const int slot = atomicAdd(&ncand, 1);
+      cand2[slot] = k;  // <= b WGs hold keys >= thr2: <= b*b <= kCandMax
+    }
+  }
+  for (int j = threadIdx.x; j < b; j += kSelThreads) best[j] = 0;
+  __syncthreads();
+  rank_topb(cand2, ncand, b, best);
+  for (int r = threadIdx.x; r < n_live; r += kSelThreads) row_lse[r] = row_lse32(s, t, r);
+  __syncthreads();
+  for (int j = threadIdx.x; j < b; j += kSelThreads) {
+    const uint64_t k = best[j];
+    const uint32_t f = 0xffffffffu - (uint32_t)(k & 0xffffffffu);
+    const int r = (int)(f / (uint32_t)V), v = (int)(f % (uint32_t)V);
+    float lp;
+    const float sc = cand_score(lrow[f], row_lse[r], scores[r], &lp);
+    sel_parent[(size_t)t * b + j] = r;
+    sel_token[(size_t)t * b + j] = v;
+    sel_score[(size_t)t * b + j] = sc;
+    sel_logprob[(size_t)t * b + j] = lp;
+  }
+  if (lse_out != nullptr) {
+    for (int r = threadIdx.x; r < b; r += kSelThreads)
+      lse_out[(size_t)t * b + r] = r < n_live ? row_lse[r] : 0.0f;
+  }
+  if (pair_parent != nullptr) {
+    for (int j = threadIdx.x; j < b; j += kSelThreads) {
+      const int p = pair_parent[(size_t)t * b + j], v = pair_token[(size_t)t * b + j];
+      float sc = __uint_as_float(0x7fc00000u);  // NaN for an out-of-range pair
+      if (p >= 0 && p < n_live && v >= 0 && v < V) {
+        float lp;
+        sc = cand_score(lrow[(size_t)p * V + v], row_lse[p], scores[p], &lp);
+      }
+      pair_score[(size_t)t * b + j] = sc;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_t* sel_parent,
+                                  int32_t* sel_token, float* sel_score, float* sel_logprob,
+                                  float* lse, const int32_t* pair_parent, const int32_t* pair_token,
+                                  float* pair_score, hipStream_t st) {
+  const int nch = (s.V + kLseChunk - 1) / kLseChunk;
+  hipLaunchKernelGGL(k_lse_partials, dim3(nch, s.b, s.T), dim3(kLseThreads), 0, st, s, logits);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_select, dim3(s.sel_chunks, s.T), dim3(kSelThreads), 0, st, s, logits,
+                     sel_parent, sel_token, sel_score, sel_logprob, lse, pair_parent, pair_token,
+                     pair_score);
+  return hipGetLastError();
+}
+
+}  // namespace td

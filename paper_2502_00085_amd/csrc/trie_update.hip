@@ -1,0 +1,297 @@
+// Trie initialisation, append + mask update, garbage collection and KV compaction (gfx950).
+//
+// Alg 2 (update_trie, update_mask) and Section 3.5 (mark, prune, compact) of the paper,
+// restated for a device-resident trie:
+//   * a node's ancestor mask holds one bit per live leaf (bit i <=> on leaf i's path);
+//     after the top-b, new bit j of every node is old bit sel_parent[j];
+//   * marking from the leaves is the same as "new mask != 0"; with a sliding window a
+//     node whose depth is <= D_new - W is evicted as well;
+//   * survivors keep their order (stable compaction).  Two facts keep the work small:
+//     the slots on every beam's path (the shared prefix) are a leading run whose masks
+//     only depend on n_live, and depth never decreases along the slots, so window
+//     eviction removes a leading run and is done by advancing `base` instead of moving
+//     rows.  Only the slots after the shared prefix are remapped, scanned and moved.
+#include "td_internal.h"
+
+namespace td {
+
+namespace {
+
+__global__ __launch_bounds__(256) void k_init_prompt(DevState s, const int32_t* plen,
+                                                     const int32_t* tokens, int stride) {
+  const int t = blockIdx.x;
+  const int P = plen[t];
+  const size_t off = (size_t)t * s.cap;
+  for (int n = threadIdx.x; n < P; n += blockDim.x) {
+    s.node_id[off + n] = n;
+    s.parent[off + n] = n - 1;
+    s.token[off + n] = tokens[(size_t)t * stride + n];
+    s.depth[off + n] = n;
+    s.mask[off + n] = 1ull;
+  }
+  for (int j = threadIdx.x; j < s.b; j += blockDim.x) s.leaf_score[(size_t)t * s.b + j] = 0.0f;
+  if (threadIdx.x == 0) {
+    TrieHdr h;
+    h.n_nodes = P;
+    h.base = 0;
+    h.n_live = 1;
+    h.n_shared = P;
+    h.leaf_depth = P - 1;
+    h.next_id = P;
+    h.pad0 = h.pad1 = 0;
+    s.hdr[t] = h;
+  }
+}
+
+constexpr int kAppThreads = 1024;
+constexpr int kAppWaves = kAppThreads / 64;
+
+// Exclusive prefix count of `flag` over the block; returns this thread's rank, writes the
+// block total to *total.  Uses wave ballots (64-bit) and a 16-entry LDS carry.
+__device__ inline int block_rank(bool flag, int* wave_cnt, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t bal = __ballot(flag);
+  const int in_wave = __popcll(bal & ((1ull << lane) - 1ull));
+  if (lane == 0) wave_cnt[wave] = __popcll(bal);
+  __syncthreads();
+  int before = 0, tot = 0;
+  for (int w = 0; w < kAppWaves; ++w) {
+    const int c = wave_cnt[w];
+    before += (w < wave) ? c : 0;
+    tot += c;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + in_wave;
+}
+
+__device__ inline uint64_t remap_mask(uint64_t m, const int* sp, int b) {
+  uint64_t r = 0;
+  for (int j = 0; j < b; ++j) r |= ((m >> sp[j]) & 1ull) << j;
+  return r;
+}
+
+__global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const int32_t* sel_parent,
+                                                              const int32_t* sel_token,
+                                                              const float* sel_score) {
+  const int t = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int b = s.b;
+  const size_t off = (size_t)t * s.cap;
+  __shared__ int sp[kMaxBeam], stok[kMaxBeam];
+  __shared__ float ssc[kMaxBeam];
+  __shared__ int err, sh_e, wave_cnt[kAppWaves], wave_cnt2[kAppWaves];
+  __shared__ int full_cnt;
+
+  const TrieHdr h = s.hdr[t];
+  const int N = h.n_nodes, base = h.base, n_live = h.n_live;
+  if (tid == 0) {
+    err = 0;
+    full_cnt = 0;
+  }
+  __syncthreads();
+  if (tid < b) {
+    const int p = sel_parent[(size_t)t * b + tid];
+    const int v = sel_token[(size_t)t * b + tid];
+    sp[tid] = p;
+    stok[tid] = v;
+    ssc[tid] = sel_score[(size_t)t * b + tid];
+    if (p < 0 || p >= n_live || v < 0 || v >= s.V) atomicOr(&err, 1);
+  }
+  __syncthreads();
+  for (int idx = tid; idx < b * b; idx += kAppThreads) {
+    const int i = idx / b, j = idx % b;
+    if (i < j && sp[i] == sp[j] && stok[i] == stok[j]) atomicOr(&err, 1);
+  }
+  __syncthreads();
+  if (err) {
+    if (tid == 0) {
+      set_status(s.status, kDevEinval);
+      s.n_moves[t] = 0;
+    }
+    return;
+  }
+
+  const int d_new = h.leaf_depth + 1;
+  // window eviction: the leading run of slots with depth <= d_new - W (depth is sorted)
+  if (tid == 0) {
+    int e = 0;
+    if (s.W > 0) {
+      const int thr = d_new - s.W;
+      int lo = 0, hi = N;  // first logical slot with depth > thr
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (s.depth[off + base + mid] <= thr) lo = mid + 1; else hi = mid;
+      }
+      e = lo;
+    }
+    sh_e = e;
+  }
+  __syncthreads();
+  const int e = sh_e;
+  const int r0 = max(e, h.n_shared);
+  const int base_new = base + e;
+  const uint64_t full_b = (b == 64) ? ~0ull : ((1ull << b) - 1ull);
+
+  // pass 1: new masks of the slots after the shared prefix, survivors' new positions
+  int alive_run = 0;
+  for (int c0 = r0; c0 < N; c0 += kAppThreads) {
+    const int n = c0 + tid;
+    bool alive = false;
+    uint64_t nm = 0;
+    if (n < N) {
+      nm = remap_mask(s.mask[off + base + n], sp, b);
+      alive = nm != 0ull;
+      if (alive && nm == full_b) atomicAdd(&full_cnt, 1);
+    }
+    int tot;
+    const int rank = block_rank(alive, wave_cnt, &tot);
+    if (n < N) s.newpos[off + n] = alive ? (r0 - e) + alive_run + rank : -1;
+    alive_run += tot;
+  }
+  const int n_new = (r0 - e) + alive_run + b;
+  if (base_new + n_new > s.cap) {
+    if (tid == 0) {
+      set_status(s.status, kDevEcapacity);
+      s.n_moves[t] = 0;
+    }
+    return;
+  }
+  __syncthreads();
+
+  // pass 2: rewrite the survivors after the shared prefix at their new slots (in place:
+  // destinations never exceed sources and chunks go in ascending order), collect moves
+  int mv_run = 0;
+  for (int c0 = r0; c0 < N; c0 += kAppThreads) {
+    const int n = c0 + tid;
+    int np = -1, id = 0, tk = 0, dp = 0, par = -1;
+    uint64_t nm = 0;
+    if (n < N) {
+      np = s.newpos[off + n];
+      if (np >= 0) {
+        id = s.node_id[off + base + n];
+        tk = s.token[off + base + n];
+        dp = s.depth[off + base + n];
+        nm = remap_mask(s.mask[off + base + n], sp, b);
+        const int pp = s.parent[off + base + n];
+        if (pp >= 0) {
+          const int lp = pp - base;
+          if (lp < e) par = -1;
+          else if (lp < r0) par = pp;
+          else {
+            const int q = s.newpos[off + lp];
+            par = q >= 0 ? base_new + q : -1;
+          }
+        }
+      }
+    }
+    const bool moved = np >= 0 && (np + e != n);
+    int mtot;
+    const int mrank = block_rank(moved, wave_cnt2, &mtot);
+    if (moved) s.moves[off + mv_run + mrank] = make_int2(base + n, base_new + np);
+    __syncthreads();  // every read of this chunk precedes its writes
+    if (np >= 0) {
+      const size_t dst = off + base_new + np;
+      s.node_id[dst] = id;
+      s.token[dst] = tk;
+      s.depth[dst] = dp;
+      s.parent[dst] = par;
+      s.mask[dst] = nm;
+    }
+    __syncthreads();
+    mv_run += mtot;
+  }
+
+  // the shared run [e, r0): masks become full(b); its first survivor loses an evicted parent
+  if (n_live != b) {
+    for (int n = e + tid; n < r0; n += kAppThreads) s.mask[off + base + n] = full_b;
+  }
+  if (tid == 0 && e > 0 && e < r0) s.parent[off + base + e] = -1;
+
+  // new leaves: rank j at logical (r0 - e) + alive_run + j
+  if (tid < b) {
+    const int lp = N - n_live + sp[tid];  // old logical slot of the parent leaf
+    int par;
+    if (lp < e) par = -1;
+    else if (lp < r0) par = base + lp;
+    else {
+      const int q = s.newpos[off + lp];
+      par = q >= 0 ? base_new + q : -1;
+    }
+    const size_t dst = off + base_new + (r0 - e) + alive_run + tid;
+    s.node_id[dst] = h.next_id + tid;
+    s.token[dst] = stok[tid];
+    s.depth[dst] = d_new;
+    s.parent[dst] = par;
+    s.mask[dst] = 1ull << tid;
+    s.leaf_score[(size_t)t * b + tid] = ssc[tid];
+  }
+  __syncthreads();
+  if (tid == 0) {
+    TrieHdr nh;
+    nh.n_nodes = n_new;
+    nh.base = base_new;
+    nh.n_live = b;
+    nh.n_shared = (r0 - e) + full_cnt + (b == 1 ? 1 : 0);
+    nh.leaf_depth = d_new;
+    nh.next_id = h.next_id + b;
+    nh.pad0 = nh.pad1 = 0;
+    s.hdr[t] = nh;
+    s.n_moves[t] = mv_run;
+  }
+}
+
+// The paper's index_select compaction of the KV cache, restricted to rows that move.
+// One WG per (trie, layer, KV head, K|V); moves are staged through LDS in ascending-source
+// batches so that in-place copies never overwrite an unread source.
+constexpr int kMoveThreads = 256;
+constexpr int kMoveLdsBytes = 64 * 1024;
+
+__global__ __launch_bounds__(kMoveThreads) void k_move_rows(DevState s) {
+  const int which = blockIdx.x & 1;
+  const int pair = blockIdx.x >> 1;           // (t * L + l) * Hkv + g
+  const int t = pair / (s.L * s.Hkv);
+  const int nm = s.n_moves[t];
+  if (nm == 0) return;
+  extern __shared__ uint4 stage[];
+  const int esz = s.dtype == TD_F32 ? 4 : 2;
+  const int row_chunks = s.D * esz / 16;      // 16-byte chunks per row
+  const int rows_per_batch = kMoveLdsBytes / (row_chunks * 16);
+  uint4* pool = reinterpret_cast<uint4*>(which ? s.v_pool : s.k_pool) +
+                (size_t)pair * s.cap * row_chunks;
+  const int2* mv = s.moves + (size_t)t * s.cap;
+  for (int i0 = 0; i0 < nm; i0 += rows_per_batch) {
+    const int cnt = min(rows_per_batch, nm - i0);
+    for (int c = threadIdx.x; c < cnt * row_chunks; c += kMoveThreads) {
+      const int r = c / row_chunks, k = c % row_chunks;
+      stage[c] = pool[(size_t)mv[i0 + r].x * row_chunks + k];
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < cnt * row_chunks; c += kMoveThreads) {
+      const int r = c / row_chunks, k = c % row_chunks;
+      pool[(size_t)mv[i0 + r].y * row_chunks + k] = stage[c];
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const int32_t* d_tokens,
+                              int stride, hipStream_t st) {
+  hipLaunchKernelGGL(k_init_prompt, dim3(s.T), dim3(256), 0, st, s, d_plen, d_tokens, stride);
+  return hipGetLastError();
+}
+
+hipError_t launch_append_prune(const DevState& s, const int32_t* sel_parent,
+                               const int32_t* sel_token, const float* sel_score, hipStream_t st) {
+  hipLaunchKernelGGL(k_append_prune, dim3(s.T), dim3(kAppThreads), 0, st, s, sel_parent, sel_token,
+                     sel_score);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_move_rows, dim3(s.T * s.L * s.Hkv * 2), dim3(kMoveThreads), kMoveLdsBytes, st,
+                     s);
+  return hipGetLastError();
+}
+
+}  // namespace td

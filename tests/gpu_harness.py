@@ -1,0 +1,165 @@
+"""Drives the HIP path and the CPU oracle on the same seeded inputs and compares them.
+
+The GPU side calls only the C ABI (through the ctypes binding); the oracle side only
+``oracle/``.  Both read the arrays made by ``synth``.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+import oracle.decode as odec
+import oracle.trie as otrie
+import synth
+
+ATTN_ABS_TOL = 2e-2        # bf16 in / fp32 accumulate / bf16 out
+ATTN_REL_TOL = 1e-2        # of max |o_ref| (bf16 path)
+ATTN_F32_TOL = 1e-4        # fp32 path
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(w, a):
+    import torch
+    a = np.ascontiguousarray(a)
+    if w.dtype == "f32":
+        return torch.from_numpy(a).cuda()
+    return torch.from_numpy(a).view(torch.bfloat16).cuda()
+
+
+def from_dev(t) -> np.ndarray:
+    import torch
+    return t.detach().to(torch.float32).cpu().numpy()
+
+
+class Run:
+    """One decode run of workload ``w`` on the GPU with a CPU oracle beside it."""
+
+    def __init__(self, w, seed=0, layers=None, attn_impl=0, capacity=None, mode="scripted",
+                 oracle=True):
+        import torch
+        import paper_2502_00085_amd.binding as B
+        self.w, self.seed, self.mode = w, seed, mode
+        self.layers = list(range(w.n_layers)) if layers is None else list(layers)
+        self.cap = capacity or w.capacity
+        self.scale = 1.0 / float(np.sqrt(w.head_dim))
+        self.dec = B.TrieDecoder(w.n_tries, w.beam_width, self.cap, w.vocab, w.n_layers, w.n_q_heads,
+                                 w.n_kv_heads, w.head_dim, w.window, w.dtype, attn_impl)
+        self.plens = synth.prompt_lengths(w, seed)
+        tokens = np.zeros((w.n_tries, int(self.plens.max())), np.int32)
+        self.tries = []
+        for t in range(w.n_tries):
+            P = int(self.plens[t])
+            tok, pk, pv = synth.prompt(w, t, P, seed)
+            tokens[t, :P] = tok
+            self.dec.k_pool[t, :, :, :P] = to_dev(w, pk)
+            self.dec.v_pool[t, :, :, :P] = to_dev(w, pv)
+            if oracle:
+                self.tries.append(otrie.Trie(tok, synth.as_f32(w, pk[self.layers]),
+                                             synth.as_f32(w, pv[self.layers]), w.beam_width, w.window))
+        self.dec.init_prompt(self.plens.tolist(), torch.from_numpy(tokens).cuda())
+        self.pending = False
+        self.step_no = 0
+
+    def inputs(self, s):
+        w = self.w
+        q, kn, vn = synth.step_qkv(w, s, self.seed)
+        logits = synth.step_logits(w, s, self.seed)
+        par, tok = synth.step_script(w, s, self.seed) if self.mode == "scripted" else (None, None)
+        return q, kn, vn, logits, par, tok
+
+    def gpu_step(self, s, q, kn, vn, logits, par, tok):
+        import torch
+        w, dec = self.w, self.dec
+        T, b = w.n_tries, w.beam_width
+        qd = to_dev(w, q)
+        out = torch.full_like(qd, 7.0)  # garbage: every row must be written
+        knd = to_dev(w, kn) if self.pending else None
+        vnd = to_dev(w, vn) if self.pending else None
+        dec.attn_decode(0, w.n_layers, qd, knd, vnd, out, self.scale)
+        ld = torch.from_numpy(np.ascontiguousarray(logits)).cuda()
+        i32 = dict(dtype=torch.int32, device="cuda")
+        f32 = dict(dtype=torch.float32, device="cuda")
+        sp, st = torch.empty((T, b), **i32), torch.empty((T, b), **i32)
+        ss, sl, lse = torch.empty((T, b), **f32), torch.empty((T, b), **f32), torch.empty((T, b), **f32)
+        if self.mode == "scripted":
+            pp, pt = torch.from_numpy(par).cuda(), torch.from_numpy(tok).cuda()
+            ps = torch.empty((T, b), **f32)
+            dec.logsoftmax_topk(ld, sp, st, ss, sl, lse, pp, pt, ps)
+            dec.append_prune(pp, pt, ps)
+        else:
+            ps = None
+            dec.logsoftmax_topk(ld, sp, st, ss, sl, lse)
+            dec.append_prune(sp, st, ss)
+        torch.cuda.synchronize()
+        self.pending = True
+        res = {"o": from_dev(out), "sel_parent": sp.cpu().numpy(), "sel_token": st.cpu().numpy(),
+               "sel_score": ss.cpu().numpy(), "sel_logprob": sl.cpu().numpy(), "lse": lse.cpu().numpy()}
+        if ps is not None:
+            res["pair_score"] = ps.cpu().numpy()
+        res["state"] = [dec.read_state(t) for t in range(T)]
+        return res
+
+    def step(self, check=True, check_attn=True):
+        """Run one step on both sides; return the list of mismatch messages (empty = parity)."""
+        self.step_no += 1
+        s = self.step_no
+        w = self.w
+        q, kn, vn, logits, par, tok = self.inputs(s)
+        n_live = [tr.n_live for tr in self.tries] if self.tries else None
+        g = self.gpu_step(s, q, kn, vn, logits, par, tok)
+        if not check or not self.tries:
+            return [], g
+        errs = []
+        qf, knf, vnf = (synth.as_f32(w, a[self.layers]) for a in (q, kn, vn))
+        for t, tr in enumerate(self.tries):
+            nl = n_live[t]
+            script = (par[t], tok[t]) if self.mode == "scripted" else None
+            ref = odec.decode_step(tr, s, qf[:, t] if check_attn else None, knf[:, t], vnf[:, t],
+                                   logits[t], self.scale, script)
+            errs += compare(w, s, t, nl, self.layers, g, ref, check_attn)
+        return errs, g
+
+
+def compare(w, s, t, nl, layers, g, ref, check_attn=True):
+    errs = []
+    tag = f"step {s} trie {t}"
+    if check_attn:
+        og = g["o"][layers, t]                     # [L'][b][Hq][d]
+        orf = ref["o"]                             # [L'][nl][Hq][d]
+        err = float(np.max(np.abs(og[:, :nl] - orf)))
+        mx = float(np.max(np.abs(orf)))
+        if w.dtype == "f32":
+            if not err <= ATTN_F32_TOL:
+                errs.append(f"{tag}: attention max err {err:.3e} > {ATTN_F32_TOL}")
+        elif not (err <= ATTN_ABS_TOL and err <= ATTN_REL_TOL * mx + 1e-6):
+            errs.append(f"{tag}: attention max err {err:.3e} (max |o_ref| {mx:.3e})")
+        if nl < w.beam_width and np.any(og[:, nl:] != 0):
+            errs.append(f"{tag}: output rows of beams >= n_live are not zero")
+    for k in ("sel_parent", "sel_token"):
+        if not np.array_equal(g[k][t], ref[k]):
+            errs.append(f"{tag}: {k} {g[k][t].tolist()} != {ref[k].tolist()}")
+    for k in ("sel_score", "sel_logprob"):
+        if not np.array_equal(g[k][t].view(np.uint32), ref[k].view(np.uint32)):
+            errs.append(f"{tag}: {k} bits differ {g[k][t].tolist()} vs {ref[k].tolist()}")
+    if not np.array_equal(g["lse"][t][:nl].view(np.uint32), ref["lse"].view(np.uint32)):
+        errs.append(f"{tag}: lse bits differ {g['lse'][t][:nl]} vs {ref['lse']}")
+    if "pair_score" in ref and not np.array_equal(g["pair_score"][t].view(np.uint32),
+                                                  ref["pair_score"].view(np.uint32)):
+        errs.append(f"{tag}: pair_score bits differ")
+    gs, rs = g["state"][t], ref["state"]
+    for k in ("n_nodes", "n_live"):
+        if gs[k] != rs[k]:
+            errs.append(f"{tag}: {k} {gs[k]} != {rs[k]}")
+    if gs["n_nodes"] == rs["n_nodes"]:
+        for k in ("node_id", "parent_slot", "token", "depth", "mask", "leaf_slot"):
+            if not np.array_equal(gs[k], rs[k]):
+                bad = np.nonzero(np.asarray(gs[k]) != np.asarray(rs[k]))[0][:5]
+                errs.append(f"{tag}: state {k} differs at slots {bad.tolist()}")
+        if not np.array_equal(gs["leaf_score"].view(np.uint32), rs["leaf_score"].view(np.uint32)):
+            errs.append(f"{tag}: leaf_score bits differ")
+    return errs

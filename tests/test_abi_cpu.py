@@ -1,0 +1,90 @@
+"""C-ABI library: loads, exports every declared entry point, and rejects bad arguments on the
+host before touching the GPU (CPU only)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2502_00085_amd.binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "triedecode.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:td_status|const char\*)\s+(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_three_hot_calls():
+    names = declared_functions()
+    for n in ("trie_attn_decode", "beam_logsoftmax_topk", "trie_append_prune", "td_create",
+              "td_destroy", "td_init_prompt", "td_read_state", "td_load_state", "td_get_status",
+              "td_error_string", "td_status_name"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = B.lib()
+    for n in declared_functions():
+        assert hasattr(L, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True, text=True).stdout
+    exported = {ln.split()[-1] for ln in out.splitlines() if ln.strip()}
+    missing = [n for n in declared_functions() if n not in exported]
+    assert not missing, missing
+
+
+def _desc(**kw):
+    d = dict(n_tries=1, beam_width=8, capacity=4096, vocab=1000, n_layers=2, n_q_heads=8,
+             n_kv_heads=2, head_dim=128, window=0, dtype=B.TD_BF16, attn_impl=0, k_pool=0x10000,
+             v_pool=0x20000)
+    d.update(kw)
+    return B.TdDesc(**d)
+
+
+@pytest.mark.parametrize("kw,frag", [
+    (dict(n_tries=0), "n_tries"), (dict(beam_width=0), "beam_width"), (dict(beam_width=65), "beam_width"),
+    (dict(vocab=4), "vocab"), (dict(n_q_heads=6, n_kv_heads=4), "n_q_heads"),
+    (dict(head_dim=80), "head_dim"), (dict(capacity=8), "capacity"), (dict(window=-1), "window"),
+    (dict(dtype=7), "dtype"), (dict(k_pool=0), "k_pool"), (dict(v_pool=0x20004), "aligned"),
+    (dict(attn_impl=2, dtype=B.TD_F32), "bf16"), (dict(vocab=2 ** 28, beam_width=16), "vocab"),
+])
+def test_create_rejects_bad_descriptors(kw, frag):
+    L = B.lib()
+    ctx = ctypes.c_void_p()
+    st = L.td_create(ctypes.byref(_desc(**kw)), ctypes.byref(ctx))
+    assert st in (B.TD_EINVAL, B.TD_EUNSUPPORTED)
+    assert ctx.value is None
+    assert frag in L.td_error_string(None).decode()
+
+
+def test_null_context_is_rejected_by_every_call():
+    L = B.lib()
+    assert L.td_destroy(None) == B.TD_EINVAL
+    assert L.trie_attn_decode(None, 0, 1, None, None, None, None, 1.0, None) == B.TD_EINVAL
+    assert L.beam_logsoftmax_topk(None, *([None] * 10)) == B.TD_EINVAL
+    assert L.trie_append_prune(None, None, None, None, None) == B.TD_EINVAL
+    assert L.td_get_status(None) == B.TD_EINVAL
+    assert L.td_read_state(None, 0, None) == B.TD_EINVAL
+    assert L.td_load_state(None, 0, None) == B.TD_EINVAL
+    assert L.td_status_name(B.TD_ECAPACITY) == b"TD_ECAPACITY"
+
+
+def test_valid_descriptor_without_a_gpu_reports_a_hip_error():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    L = B.lib()
+    ctx = ctypes.c_void_p()
+    st = L.td_create(ctypes.byref(_desc()), ctypes.byref(ctx))
+    assert st == B.TD_EHIP and ctx.value is None
+
+
+def test_binding_refuses_to_run_without_the_library(monkeypatch):
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "LIB_PATH", "/nonexistent/libtriedecode.so")
+    with pytest.raises(RuntimeError, match="missing"):
+        B.lib()
