@@ -272,6 +272,9 @@ td_status td_read_state(td_ctx* c, int32_t trie, td_state* o) {
   td::TrieHdr h;
   if (e == hipSuccess) e = hipMemcpy(&h, s.hdr + trie, sizeof h, hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(c, e, "td_read_state");
+  if (h.n_nodes < 0 || h.base < 0 || h.base + h.n_nodes > s.cap || h.n_live < 0 || h.n_live > s.b)
+    return fail(c, TD_ESTATE, "trie %d header is inconsistent (n_nodes %d, base %d, n_live %d)", trie,
+                h.n_nodes, h.base, h.n_live);
   const size_t off = (size_t)trie * s.cap + h.base;
   const size_t n = (size_t)h.n_nodes;
   if (n > 0) {

@@ -112,9 +112,11 @@ __device__ inline void rank_topb(const uint64_t* cand, int n, int b, uint64_t* o
   }
 }
 
-// b-th largest value among gmax[0..n) (n >= 1): the smallest of the values whose count of
-// strictly larger values is < b.  Zero entries (empty groups) are allowed.
+// Lower bound of the b-th largest key from the group maxima gmax[0..n): the b-th largest
+// maximum when there are at least b groups (each of the b largest groups holds a key at or
+// above it), else 0 (every key is a candidate).  Zero entries (empty groups) are allowed.
 __device__ inline uint64_t bth_largest(const uint64_t* gmax, int n, int b, uint64_t* red) {
+  if (n < b) return 0;
   uint64_t mine = ~0ull;
   for (int i = threadIdx.x; i < n; i += blockDim.x) {
     const uint64_t k = gmax[i];
@@ -186,12 +188,12 @@ __global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float*
   for (int i = 0; i < kSelPerThread; ++i) {
     if (key[i] != 0 && key[i] >= thr) {
       const int slot = atomicAdd(&ncand, 1);
-      cand[slot] = key[i];  // at most b threads hold keys >= thr: <= 32 b <= kCandMax
+      if (slot < kCandMax) cand[slot] = key[i];  // <= b threads hold keys >= thr: <= 32 b
     }
   }
   for (int j = threadIdx.x; j < b; j += kSelThreads) best[j] = 0;
   __syncthreads();
-  rank_topb(cand, ncand, b, best);
+  rank_topb(cand, min(ncand, kCandMax), b, best);
   __syncthreads();
   uint64_t* my = s.topk_keys + ((size_t)t * s.sel_chunks + c) * b;
   for (int j = threadIdx.x; j < b; j += kSelThreads) my[j] = best[j];
@@ -219,17 +221,22 @@ __global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float*
     const uint64_t k = all[i];
     if (k != 0 && k >= thr2) {
       const int slot = atomicAdd(&ncand, 1);
-      cand2[slot] = k;  // <= b WGs hold keys >= thr2: <= b*b <= kCandMax
+      // <= b WGs hold keys >= thr2 (or < b WGs exist): at most b*b <= kCandMax keys
+      if (slot < kCandMax) cand2[slot] = k;
     }
   }
   for (int j = threadIdx.x; j < b; j += kSelThreads) best[j] = 0;
   __syncthreads();
-  rank_topb(cand2, ncand, b, best);
+  rank_topb(cand2, min(ncand, kCandMax), b, best);
   for (int r = threadIdx.x; r < n_live; r += kSelThreads) row_lse[r] = row_lse32(s, t, r);
   __syncthreads();
   for (int j = threadIdx.x; j < b; j += kSelThreads) {
     const uint64_t k = best[j];
-    const uint32_t f = 0xffffffffu - (uint32_t)(k & 0xffffffffu);
+    uint32_t f = 0xffffffffu - (uint32_t)(k & 0xffffffffu);
+    if (k == 0 || f >= (uint32_t)total) {  // unreachable: there are >= b candidates
+      set_status(s.status, kDevEinval);
+      f = 0;
+    }
     const int r = (int)(f / (uint32_t)V), v = (int)(f % (uint32_t)V);
     float lp;
     const float sc = cand_score(lrow[f], row_lse[r], scores[r], &lp);

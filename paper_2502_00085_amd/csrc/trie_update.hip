@@ -176,7 +176,7 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
         const int pp = s.parent[off + base + n];
         if (pp >= 0) {
           const int lp = pp - base;
-          if (lp < e) par = -1;
+          if (lp < e || lp >= n) par = -1;  // evicted (a parent always precedes its child)
           else if (lp < r0) par = pp;
           else {
             const int q = s.newpos[off + lp];
