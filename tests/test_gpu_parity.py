@@ -106,6 +106,11 @@ def test_invalid_selection_leaves_trie_unchanged():
     w = small(beam_width=4, steps=3)
     r = Run(w, 11)
     r.step()
+    # the next step's attention stores the pending leaf K/V; then append invalid selections
+    q, kn, vn, _, _, _ = r.inputs(2)
+    from gpu_harness import to_dev
+    qd = to_dev(w, q)
+    r.dec.attn_decode(0, w.n_layers, qd, to_dev(w, kn), to_dev(w, vn), torch.empty_like(qd), r.scale)
     before = r.dec.read_state(0)
     i32 = dict(dtype=torch.int32, device="cuda")
     bad_parent = torch.tensor([[0, 1, 9, 0]], **i32)       # rank 9 >= n_live
