@@ -165,7 +165,11 @@ td_status td_read_state(td_ctx* ctx, int32_t trie, td_state* host_out);
  * the all-beam (shared) slots a prefix.  The pools must hold the K/V rows of every slot
  * (except the leaves' when kv_pending = 1). */
 td_status td_load_state(td_ctx* ctx, int32_t trie, const td_state* host_in);
-/* Read and clear the sticky device status (synchronises the device). */
+/* Read and clear the sticky device status (synchronises the device).  When the status
+ * comes from a rejected trie_append_prune of a one-trie context, the context is returned
+ * to its state before that call (the leaves' K/V count as stored again), so decoding can
+ * resume; with several tries the other tries have advanced, and the rejected trie must be
+ * restored with td_load_state. */
 td_status td_get_status(td_ctx* ctx);
 /* Last host-side error message of ctx ("" if none); valid until the next call on ctx. */
 const char* td_error_string(const td_ctx* ctx);

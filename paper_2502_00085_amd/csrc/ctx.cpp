@@ -136,7 +136,7 @@ td_status td_create(const td_desc* d, td_ctx** out) {
       (e = alloc(c, &s.token, tc)) != hipSuccess || (e = alloc(c, &s.depth, tc)) != hipSuccess ||
       (e = alloc(c, &s.mask, tc)) != hipSuccess ||
       (e = alloc(c, &s.leaf_score, (size_t)s.T * s.b)) != hipSuccess ||
-      (e = alloc(c, &s.status, 1)) != hipSuccess ||
+      (e = alloc(c, &s.status, 2)) != hipSuccess ||
       (e = alloc(c, &s.lse_part, (size_t)s.T * s.b * s.lse_chunks * 2)) != hipSuccess ||
       (e = alloc(c, &s.topk_keys, (size_t)s.T * s.sel_chunks * s.b)) != hipSuccess ||
       (e = alloc(c, &s.topk_count, (size_t)s.T)) != hipSuccess ||
@@ -362,12 +362,18 @@ td_status td_load_state(td_ctx* c, int32_t trie, const td_state* in) {
 
 td_status td_get_status(td_ctx* c) {
   if (!c) return TD_EINVAL;
-  int32_t v = 0;
+  int32_t v[2] = {0, 0};
   hipError_t e = hipDeviceSynchronize();
-  if (e == hipSuccess) e = hipMemcpy(&v, c->dev.status, 4, hipMemcpyDeviceToHost);
-  if (e == hipSuccess) e = hipMemset(c->dev.status, 0, 4);
+  if (e == hipSuccess) e = hipMemcpy(v, c->dev.status, sizeof v, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemset(c->dev.status, 0, sizeof v);
   if (e != hipSuccess) return hip_fail(c, e, "td_get_status");
-  return static_cast<td_status>(v);
+  if (v[1] && c->dev.T == 1) {
+    // a rejected append left the trie as it was: the leaves' K/V are stored, not pending
+    // (with several tries the others advanced; such a context needs td_load_state)
+    c->pending = false;
+    c->layer_written.assign(c->dev.L, 0);
+  }
+  return static_cast<td_status>(v[0]);
 }
 
 }  // extern "C"

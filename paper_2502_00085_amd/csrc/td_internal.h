@@ -31,7 +31,8 @@ struct DevState {
   int32_t* depth;        // [T][cap]
   uint64_t* mask;        // [T][cap]
   float* leaf_score;     // [T][b]
-  int32_t* status;       // sticky device status (first error wins)
+  int32_t* status;       // [0] sticky device status (first error wins), [1] 1 if an append
+                         // was rejected (the trie kept its previous state)
   // workspace
   double* lse_part;      // [T][b][lse_chunks][2]  (chunk max, chunk sum of exp)
   uint64_t* topk_keys;   // [T][sel_chunks][b]

@@ -107,6 +107,7 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
   if (err) {
     if (tid == 0) {
       set_status(s.status, kDevEinval);
+      s.status[1] = 1;
       s.n_moves[t] = 0;
     }
     return;
@@ -153,6 +154,7 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
   if (base_new + n_new > s.cap) {
     if (tid == 0) {
       set_status(s.status, kDevEcapacity);
+      s.status[1] = 1;
       s.n_moves[t] = 0;
     }
     return;
