@@ -151,51 +151,51 @@ def gpu_bench(args, w, K):
         bench.step(i, stream)
     torch.cuda.synchronize()
 
-    # events around every attention launch (recorded as graph nodes in graph mode)
-    evs = None
-    mode = "eager" if args.eager else "graph"
-    graph = None
+    # attention kernel duration: HIP events around every launch of an eager pass over the
+    # same K steps (events cannot be recorded inside a graph on this platform)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(K)]
+    bench.init()
+    t0 = time.perf_counter()
+    for i in range(K):
+        bench.step(i, stream, evs[i])
+    torch.cuda.synchronize()
+    eager_s = time.perf_counter() - t0
+    attn_ms = np.array([a.elapsed_time(b) for a, b in evs])
+
+    mode, graph = ("eager", None) if args.eager else ("graph", None)
     if mode == "graph":
         try:
             bench.init()
-            evs = [(torch.cuda.Event(enable_timing=True, external=True),
-                    torch.cuda.Event(enable_timing=True, external=True)) for _ in range(K)]
             graph = torch.cuda.CUDAGraph()
             cs = torch.cuda.Stream()
             with torch.cuda.graph(graph, stream=cs):
                 s = torch.cuda.current_stream().cuda_stream
                 for i in range(K):
-                    bench.step(i, s, evs[i])
+                    bench.step(i, s)
+            bench.init()
+            graph.replay()  # warm replay
+            torch.cuda.synchronize()
         except Exception as e:  # graph capture unavailable: fall back to eager launches
             log(f"[bench] graph capture failed ({e}); timing eager launches")
             mode, graph = "eager", None
-    if mode == "graph":
-        bench.init()
-        graph.replay()  # warm replay
-        torch.cuda.synchronize()
-        bench.init()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
+    # the timed region: exactly K decode steps
+    bench.init()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    if graph is not None:
         graph.replay()
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
     else:
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(K)]
-        bench.init()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
         for i in range(K):
-            bench.step(i, stream, evs[i])
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
-    attn_ms = np.array([a.elapsed_time(b) for a, b in evs])
+            bench.step(i, stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
     status = bench.dec.status()
     if status != 0:
         raise RuntimeError(f"device status {status} after the timed run")
     nodes = bench.nodes_per_step(K)
     bench.dec.close()
-    return dict(mode=mode, seconds=t1 - t0, attn_ms=attn_ms, nodes=nodes)
+    return dict(mode=mode, seconds=t1 - t0, eager_seconds=eager_s, attn_ms=attn_ms, nodes=nodes)
 
 
 def cpu_baseline(w, seed, budget_s):
@@ -270,6 +270,7 @@ def main():
                      "attn_us_mean": round(float(attn_s.mean() * 1e6), 2),
                      "unique_kv_bytes_per_launch": int(kv_bytes.mean())},
         "hbm_gbps_unique_kv_whole_step": round(float(kv_bytes.mean() / (ms_per_step / 1e3) / 1e9), 1),
+        "eager_ms_per_step": round(r["eager_seconds"] * 1e3 / K, 5),
         "nodes_per_step_mean": round(float(r["nodes"].sum(axis=1).mean()), 1),
     }
     if not args.no_cpu_baseline and not args.profile_only:

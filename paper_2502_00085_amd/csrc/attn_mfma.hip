@@ -235,33 +235,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
       }
     }
   }
-  if (a.splits == 1) return;
 
-  __shared__ int ticket;
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) ticket = atomicAdd(&s.attn_count[unit], 1);
-  __syncthreads();
-  if (ticket != a.splits - 1) return;
-  __threadfence();
-  if (threadIdx.x == 0) s.attn_count[unit] = 0;
-  for (int idx = threadIdx.x; idx < kRows * D; idx += NW * 64) {
-    const int i = idx / D, c = idx % D;
-    const int rr = u.rb * kRows + i;
-    if (rr >= s.b * G) continue;
-    float Mi = kNegBig;
-    for (int sp = 0; sp < a.splits; ++sp) Mi = fmaxf(Mi, part[((size_t)sp * kRows + i) * (D + 2) + D]);
-    float L = 0.0f, O = 0.0f;
-    for (int sp = 0; sp < a.splits; ++sp) {
-      const float* pp = part + ((size_t)sp * kRows + i) * (D + 2);
-      const float ff = exp2f(pp[D] - Mi);
-      L += pp[D + 1] * ff;
-      O += pp[c] * ff;
-    }
-    const int bm = rr / G;
-    const float val = (bm < n_live && L > 0.0f) ? O / L : 0.0f;
-    outp[((((size_t)u.li * s.T + u.t) * s.b + bm) * s.Hq + u.g * G + rr % G) * D + c] = (__bf16)val;
-  }
 }
 
 constexpr int kNW = 8;

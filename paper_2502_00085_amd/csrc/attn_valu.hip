@@ -185,33 +185,7 @@ __global__ __launch_bounds__(kValuThreads) void k_attn_valu(DevState s, AttnArgs
       }
     }
   }
-  if (a.splits == 1) return;
 
-  __shared__ int ticket;
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) ticket = atomicAdd(&s.attn_count[unit], 1);
-  __syncthreads();
-  if (ticket != a.splits - 1) return;
-  __threadfence();
-  if (threadIdx.x == 0) s.attn_count[unit] = 0;
-  for (int idx = threadIdx.x; idx < R * DD; idx += kValuThreads) {
-    const int i = idx / DD, c = idx % DD;
-    const int r = u.rb * R + i;
-    if (r >= s.b * G) continue;
-    float M = kNegBig;
-    for (int sp = 0; sp < a.splits; ++sp) M = fmaxf(M, part[((size_t)sp * R + i) * (DD + 2) + DD]);
-    float L = 0.0f, O = 0.0f;
-    for (int sp = 0; sp < a.splits; ++sp) {
-      const float* pp = part + ((size_t)sp * R + i) * (DD + 2);
-      const float f = exp2f(pp[DD] - M);
-      L += pp[DD + 1] * f;
-      O += pp[c] * f;
-    }
-    const int bm = r / G, hl = r % G;
-    const float val = (bm < n_live && L > 0.0f) ? O / L : 0.0f;
-    outp[((((size_t)u.li * s.T + u.t) * s.b + bm) * s.Hq + u.g * G + hl) * DD + c] = from_f<T>(val);
-  }
 }
 
 template <typename T>

@@ -2,6 +2,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -16,6 +17,7 @@ struct td_ctx {
   bool pending = false;                // leaves' K/V rows not yet stored in the pools
   std::vector<uint8_t> layer_written;  // per layer, while pending
   int32_t* d_plen = nullptr;
+  int splits_override = 0;             // TD_ATTN_SPLITS (tuning): WGs per attention unit
   std::vector<void*> allocs;
   std::string err;
 };
@@ -143,13 +145,13 @@ td_status td_create(const td_desc* d, td_ctx** out) {
       (e = alloc(c, &s.newpos, tc)) != hipSuccess || (e = alloc(c, &s.moves, tc)) != hipSuccess ||
       (e = alloc(c, &s.n_moves, (size_t)s.T)) != hipSuccess ||
       (e = alloc(c, &s.attn_part, (size_t)s.attn_part_floats)) != hipSuccess ||
-      (e = alloc(c, &s.attn_count, (size_t)s.attn_pairs_max)) != hipSuccess ||
       (e = alloc(c, &c->d_plen, (size_t)s.T)) != hipSuccess) {
     td_destroy(c);
     return hip_fail(nullptr, e, "allocating trie metadata / workspace");
   }
   c->inited.assign(s.T, 0);
   c->layer_written.assign(s.L, 0);
+  if (const char* sp = getenv("TD_ATTN_SPLITS")) c->splits_override = atoi(sp) > 0 ? (atoi(sp) < 64 ? atoi(sp) : 64) : 0;
   *out = c;
   return TD_OK;
 }
@@ -213,10 +215,11 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   a.kv_pending = c->pending ? 1 : 0;
   const int rpb = mfma ? td::attn_mfma_rows_per_block() : td::attn_valu_rows_per_block();
   a.row_blocks = (s.b * (s.Hq / s.Hkv) + rpb - 1) / rpb;
-  a.splits = td::attn_choose_splits(s, n_layers, a.row_blocks);
+  a.splits = c->splits_override > 0 ? c->splits_override : td::attn_choose_splits(s, n_layers, a.row_blocks);
   const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;
   hipError_t e = mfma ? td::launch_attn_mfma(s, a, st) : td::launch_attn_valu(s, a, st);
+  if (e == hipSuccess && a.splits > 1) e = td::launch_attn_combine(s, a, rpb, st);
   if (e != hipSuccess) return hip_fail(c, e, "trie_attn_decode launch");
   if (c->pending) {
     for (int l = layer_begin; l < layer_begin + n_layers; ++l) c->layer_written[l] = 1;

@@ -41,7 +41,6 @@ struct DevState {
   int2* moves;           // [T][cap] (src phys, dst phys) rows to move, ascending src
   int32_t* n_moves;      // [T]
   float* attn_part;      // split-combine partials
-  int32_t* attn_count;   // [pairs] arrival counters of split WGs (self-resetting)
   int lse_chunks, sel_chunks, attn_part_floats, attn_pairs_max;
 };
 
@@ -72,6 +71,7 @@ hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const in
                               int stride, hipStream_t st);
 hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st);
 hipError_t launch_attn_valu(const DevState& s, const AttnArgs& a, hipStream_t st);
+hipError_t launch_attn_combine(const DevState& s, const AttnArgs& a, int rows_per_block, hipStream_t st);
 int attn_mfma_rows_per_block();
 int attn_valu_rows_per_block();
 int attn_choose_splits(const DevState& s, int n_layers, int row_blocks);

@@ -11,8 +11,10 @@
 // Kernels:
 //   k_lse_partials  grid (lse_chunks, b, T): max and fp64 sum of exp of a 4096-logit chunk
 //   k_select        grid (sel_chunks, T): lse of the rows it touches (from the partials),
-//                   keys of 8192 candidates, the WG's top-b; the last WG of a trie to
-//                   finish merges all WGs' top-b lists into the final selection.
+//                   keys of 8192 candidates, the WG's top-b list
+//   k_merge         grid (T): merges the WG lists of a trie into the final selection
+// (separate launches instead of a last-arriving-WG merge: a device-scope fence costs an
+// L2 writeback + invalidate per WG on this multi-XCD part)
 // Top-b of a set split into groups (threads or WGs) whose maxima are known: the b-th
 // largest group maximum is a lower bound of the b-th largest key, so only keys at or
 // above it (at most b groups' worth) are ranked, each by counting larger candidates.
@@ -136,12 +138,7 @@ __device__ inline uint64_t bth_largest(const uint64_t* gmax, int n, int b, uint6
   return r;
 }
 
-__global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float* logits,
-                                                        int32_t* sel_parent, int32_t* sel_token,
-                                                        float* sel_score, float* sel_logprob,
-                                                        float* lse_out, const int32_t* pair_parent,
-                                                        const int32_t* pair_token,
-                                                        float* pair_score) {
+__global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float* logits) {
   const int c = blockIdx.x, t = blockIdx.y;
   const int b = s.b, V = s.V;
   const int n_live = s.hdr[t].n_live;
@@ -154,7 +151,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float*
   __shared__ uint64_t red[kSelThreads / 64];
   __shared__ uint64_t best[kMaxBeam];
   __shared__ float row_lse[kMaxBeam];
-  __shared__ int ncand, ticket;
+  __shared__ int ncand;
 
   const int f0 = c * kSelChunk;
   const int f1 = min(total, f0 + kSelChunk);
@@ -197,37 +194,45 @@ __global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float*
   __syncthreads();
   uint64_t* my = s.topk_keys + ((size_t)t * s.sel_chunks + c) * b;
   for (int j = threadIdx.x; j < b; j += kSelThreads) my[j] = best[j];
+}
 
-  // arrival: the last WG of trie t merges
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) ticket = atomicAdd(&s.topk_count[t], 1);
-  __syncthreads();
-  if (ticket != n_active - 1) return;
-  __threadfence();
-  if (threadIdx.x == 0) {
-    s.topk_count[t] = 0;
-    ncand = 0;
-  }
+// Merge of the per-WG top-b lists of one trie (one WG per trie), then the outputs.
+__global__ __launch_bounds__(kSelThreads) void k_merge(DevState s, const float* logits,
+                                                       int32_t* sel_parent, int32_t* sel_token,
+                                                       float* sel_score, float* sel_logprob,
+                                                       float* lse_out, const int32_t* pair_parent,
+                                                       const int32_t* pair_token, float* pair_score) {
+  const int t = blockIdx.x;
+  const int b = s.b, V = s.V;
+  const int n_live = s.hdr[t].n_live;
+  const int total = n_live * V;
+  const int n_active = (total + kSelChunk - 1) / kSelChunk;
+  __shared__ uint64_t cand[kCandMax];
+  __shared__ uint64_t red[kSelThreads / 64];
+  __shared__ uint64_t best[kMaxBeam];
+  __shared__ float row_lse[kMaxBeam];
+  __shared__ int ncand;
+  const float* lrow = logits + (size_t)t * s.b * V;
+  const float* scores = s.leaf_score + (size_t)t * b;
+  if (threadIdx.x == 0) ncand = 0;
   const uint64_t* all = s.topk_keys + (size_t)t * s.sel_chunks * b;
-  // group maxima = first (largest) key of every WG list; at most kSelThreads per pass
-  uint64_t* gm = cand;  // reuse: group maxima of up to kCandMax WGs
+  // group maxima = first (largest) key of every WG list
+  uint64_t* gm = cand;
   for (int i = threadIdx.x; i < n_active; i += kSelThreads) gm[i] = all[(size_t)i * b];
   __syncthreads();
   const uint64_t thr2 = bth_largest(gm, n_active, b, red);
   __syncthreads();
-  uint64_t* cand2 = cand;  // overwrite after the threshold is known
   for (int i = threadIdx.x; i < n_active * b; i += kSelThreads) {
     const uint64_t k = all[i];
     if (k != 0 && k >= thr2) {
       const int slot = atomicAdd(&ncand, 1);
       // <= b WGs hold keys >= thr2 (or < b WGs exist): at most b*b <= kCandMax keys
-      if (slot < kCandMax) cand2[slot] = k;
+      if (slot < kCandMax) cand[slot] = k;
     }
   }
   for (int j = threadIdx.x; j < b; j += kSelThreads) best[j] = 0;
   __syncthreads();
-  rank_topb(cand2, min(ncand, kCandMax), b, best);
+  rank_topb(cand, min(ncand, kCandMax), b, best);
   for (int r = threadIdx.x; r < n_live; r += kSelThreads) row_lse[r] = row_lse32(s, t, r);
   __syncthreads();
   for (int j = threadIdx.x; j < b; j += kSelThreads) {
@@ -272,9 +277,11 @@ hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_
   hipLaunchKernelGGL(k_lse_partials, dim3(nch, s.b, s.T), dim3(kLseThreads), 0, st, s, logits);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_select, dim3(s.sel_chunks, s.T), dim3(kSelThreads), 0, st, s, logits,
-                     sel_parent, sel_token, sel_score, sel_logprob, lse, pair_parent, pair_token,
-                     pair_score);
+  hipLaunchKernelGGL(k_select, dim3(s.sel_chunks, s.T), dim3(kSelThreads), 0, st, s, logits);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_merge, dim3(s.T), dim3(kSelThreads), 0, st, s, logits, sel_parent, sel_token,
+                     sel_score, sel_logprob, lse, pair_parent, pair_token, pair_score);
   return hipGetLastError();
 }
 
