@@ -9,9 +9,14 @@
 //   S^T[node][row] = K_tile . Q^T     A = K rows (a lane holds half a node row: the
 //                                     contraction index d is permuted so that every lane
 //                                     loads D contiguous bytes straight from HBM)
-//   O^T[d][row]   += V_tile^T . P^T   A = V^T (V goes through LDS; a lane gathers one
-//                                     column), B = P^T taken from the S^T accumulator
-//                                     registers as they are (node order permuted to match)
+//   O^T[d][row]   += V_tile^T . P^T   A = V^T: V rows go straight from HBM into LDS
+//                                     (global_load_lds) and come back transposed with
+//                                     ds_read_b64_tr_b16; B = P^T taken from the S^T
+//                                     accumulator registers as they are (node order
+//                                     permuted to match)
+//
+// Each wave double-buffers its V tiles, so the next tile's K/V loads are in flight while
+// the current tile's softmax and PV run.
 //
 // The S^T layout puts one query row per lane, so the online softmax needs one cross-lane
 // step (the two half-waves) per tile.  Tiles inside the shared prefix (every beam's
@@ -25,8 +30,10 @@ namespace td {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kRows = 32;
 constexpr float kNegBig = -1.0e30f;
@@ -35,13 +42,23 @@ template <int D, int NW>
 struct MfmaCfg {
   static constexpr int KSTEPS = D / 16;       // 32x32x16 steps of S^T
   static constexpr int DT = D / 32;           // 32-wide d tiles of O^T
-  static constexpr int RS = D + 8;            // LDS row stride of a V tile (elements)
-  static constexpr int VCH = D / 16;          // 16-byte V chunks per lane per tile
+  static constexpr int CPR = D / 8;           // 16-byte chunks per node row
+  static constexpr int NBLK = CPR / 4;        // 64-byte blocks per row (bank rotation period)
+  static constexpr int VINST = 32 * CPR / 64; // direct-to-LDS loads per 32-node V tile
+  static constexpr int TILE_BYTES = 32 * D * 2;
   static constexpr int OS = D + 4;            // LDS row stride of the O merge buffer (floats)
-  static constexpr int V_LDS = NW * 32 * RS * 2;
+  static constexpr int V_LDS = NW * 2 * TILE_BYTES;  // two V tiles per wave
   static constexpr int O_LDS = kRows * OS * 4 + 2 * NW * kRows * 4;
   static constexpr int LDS = V_LDS > O_LDS ? V_LDS : O_LDS;
 };
+
+// Physical 16-byte chunk of logical chunk c of tile row r: rows are rotated by whole
+// 64-byte blocks so that the transposed reads of four consecutive rows hit four
+// different groups of 16 banks.
+template <int CPR, int NBLK>
+__device__ inline int phys_chunk(int r, int c) {
+  return (c + 4 * (r % NBLK)) % CPR;
+}
 
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
@@ -52,12 +69,16 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   const int N = h.n_nodes, base = h.base, n_live = h.n_live, Dq = h.leaf_depth;
   const int G = s.Hq / s.Hkv;
   const int lab = a.layer_begin + u.li;
-  if (a.kv_pending && u.split == 0 && u.rb == 0) store_leaf_kv<__bf16>(s, a, u, base, N, n_live);
 
   const int lo = window_lo(s, u.t, base, N, Dq);
-  const int leaf0 = a.kv_pending ? N - n_live : N;
   const int per = (N - lo + a.splits - 1) / a.splits;
   const int n0 = lo + u.split * per, n1 = min(N, n0 + per);
+  // pending leaf rows: a WG whose node range holds them stores them into the pool first
+  // (identical data if several WGs do), so the main loop only reads the pool
+  if (a.kv_pending && n0 < n1 && n1 > N - n_live) {
+    store_leaf_kv<__bf16>(s, a, u, base, N, n_live);
+    __syncthreads();
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 31, hh = lane >> 5;
 
@@ -79,13 +100,14 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     }
   }
 
-  const __bf16* kpool = static_cast<const __bf16*>(s.k_pool) + pool_row(s, u.t, lab, u.g, 0);
-  const __bf16* vpool = static_cast<const __bf16*>(s.v_pool) + pool_row(s, u.t, lab, u.g, 0);
-  const __bf16* knew = static_cast<const __bf16*>(a.k_new);
-  const __bf16* vnew = static_cast<const __bf16*>(a.v_new);
-  const size_t new_base = (((size_t)u.li * s.T + u.t) * s.b) * s.Hkv + u.g;  // row (li,t,0,g)
+  const __bf16* kpool = static_cast<const __bf16*>(s.k_pool) + pool_row(s, u.t, lab, u.g, base);
+  const __bf16* vpool = static_cast<const __bf16*>(s.v_pool) + pool_row(s, u.t, lab, u.g, base);
   const uint64_t* maskp = s.mask + (size_t)u.t * s.cap + base;
-  __bf16* vt = reinterpret_cast<__bf16*>(lds) + wave * 32 * C::RS;
+  unsigned char* vbuf = lds + wave * 2 * C::TILE_BYTES;
+
+  // transposed-read geometry of this lane: 16-lane group g, row m of the group's 16x4
+  // block, 4-element column quarter q
+  const int grp = lane >> 4, tm = (lane & 15) >> 2, tq = lane & 3;
 
   float m = kNegBig, lsum = 0.0f;
   f32x16 o[C::DT];
@@ -95,52 +117,84 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     for (int v = 0; v < 16; ++v) o[dt][v] = 0.0f;
 
   const int ntiles = n1 > n0 ? (n1 - n0 + 31) / 32 : 0;
-  for (int tile = wave; tile < ntiles; tile += NW) {
+  const int my_tiles = ntiles > wave ? (ntiles - wave + NW - 1) / NW : 0;
+  bf16x8 kv[C::KSTEPS];
+
+  // K of a tile -> registers (lane: node tb + col, half hh); V of a tile -> LDS buffer
+  // (direct loads, 16 bytes per lane, rows rotated by phys_chunk); rows past the range
+  // end are clamped to its last node and masked out later
+  auto issue = [&](int tile, int buf) {
     const int tb = n0 + tile * 32;
-    // K: lane -> node tb + col, half hh of its row
-    bf16x8 kv[C::KSTEPS];
-    {
-      const int nk = min(tb + col, n1 - 1);
-      const __bf16* kr = nk >= leaf0 ? knew + (new_base + (size_t)(nk - leaf0) * s.Hkv) * D
-                                     : kpool + (size_t)(base + nk) * D;
-      const uint4* kp = reinterpret_cast<const uint4*>(kr + hh * (D / 2));
+    const int nk = min(tb + col, n1 - 1);
+    const uint4* kp = reinterpret_cast<const uint4*>(kpool + (size_t)nk * D + hh * (D / 2));
 #pragma unroll
-      for (int t = 0; t < C::KSTEPS; ++t) kv[t] = __builtin_bit_cast(bf16x8, kp[t]);
-    }
-    // V tile -> LDS (row-major, coalesced 16-byte chunks)
-    uint4 vch[C::VCH];
+    for (int t = 0; t < C::KSTEPS; ++t) kv[t] = __builtin_bit_cast(bf16x8, kp[t]);
+    unsigned char* dst = vbuf + buf * C::TILE_BYTES;
 #pragma unroll
-    for (int i = 0; i < C::VCH; ++i) {
-      const int c = lane + 64 * i;
-      const int row = c / (D / 8), c8 = c % (D / 8);
+    for (int i = 0; i < C::VINST; ++i) {
+      const int p = 64 * i + lane;
+      const int row = p / C::CPR, pc = p % C::CPR;
+      const int c = (pc + C::CPR - 4 * (row % C::NBLK)) % C::CPR;  // inverse of phys_chunk
       const int nv = min(tb + row, n1 - 1);
-      const __bf16* vr = nv >= leaf0 ? vnew + (new_base + (size_t)(nv - leaf0) * s.Hkv) * D
-                                     : vpool + (size_t)(base + nv) * D;
-      vch[i] = reinterpret_cast<const uint4*>(vr)[c8];
+      const __bf16* src = vpool + (size_t)nv * D + c * 8;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                       (__attribute__((address_space(3))) void*)(dst + i * 1024), 16, 0, 0);
     }
+  };
+
+  if (my_tiles > 0) issue(wave, 0);
+  for (int k = 0; k < my_tiles; ++k) {
+    const int tile = wave + NW * k;
+    const int tb = n0 + tile * 32;
+    const int buf = k & 1;
+    __builtin_amdgcn_s_waitcnt(0);  // this tile's K registers and V rows have landed
     f32x16 acc;
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
 #pragma unroll
     for (int t = 0; t < C::KSTEPS; ++t)
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv[t], qv[t], acc, 0, 0, 0);
+
+    // masks of this lane's nodes 8(v/4) + 4hh + v%4 (tiles past the shared prefix only)
+    const bool masked = tb + 31 >= h.n_shared;
+    uint32_t vis = 0;
 #pragma unroll
-    for (int i = 0; i < C::VCH; ++i) {
-      const int c = lane + 64 * i;
-      const int row = c / (D / 8), c8 = c % (D / 8);
-      *reinterpret_cast<uint4*>(vt + row * C::RS + c8 * 8) = vch[i];
+    for (int v = 0; v < 16; ++v) {
+      const int n = tb + 8 * (v >> 2) + 4 * hh + (v & 3);
+      bool ok = n < n1;
+      if (masked && ok) ok = (maskp[n] >> beam_bit) & 1ull;
+      vis |= (uint32_t)ok << v;
     }
 
-    // scores of this lane's row at nodes 8(v/4) + 4hh + v%4 of the tile
-    const bool masked = tb + 31 >= h.n_shared;
+    // V^T operands from LDS: for 16 nodes (uu) and 32 d (dt), two transposed reads, each
+    // giving this lane column d = 32 dt + col at 4 nodes 16uu + 8 half + 4hh + tm'
+    bf16x8 va[2][C::DT];
+    const __bf16* vb = reinterpret_cast<const __bf16*>(vbuf + buf * C::TILE_BYTES);
+#pragma unroll
+    for (int uu = 0; uu < 2; ++uu) {
+#pragma unroll
+      for (int dt = 0; dt < C::DT; ++dt) {
+        i16x4 part[2];
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int n = 16 * uu + 8 * half + 4 * hh + tm;
+          const int c = 4 * dt + 2 * (grp & 1) + (tq >> 1);
+          const int pc = phys_chunk<C::CPR, C::NBLK>(n, c);
+          const __bf16* ptr = vb + n * D + pc * 8 + 4 * (tq & 1);
+          part[half] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(ptr));
+        }
+        const i16x8 both = __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3, 4, 5, 6, 7);
+        va[uu][dt] = __builtin_bit_cast(bf16x8, both);
+      }
+    }
+    // the next tile's loads overlap this tile's softmax and PV
+    if (k + 1 < my_tiles) issue(tile + NW, buf ^ 1);
+
     float sc[16];
     float tmax = -INFINITY;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int n = tb + 8 * (v >> 2) + 4 * hh + (v & 3);
-      bool vis = n < n1;
-      if (masked && vis) vis = (maskp[n] >> beam_bit) & 1ull;
-      sc[v] = vis ? acc[v] * a.scale_log2 : -INFINITY;
+      sc[v] = ((vis >> v) & 1u) ? acc[v] * a.scale_log2 : -INFINITY;
       tmax = fmaxf(tmax, sc[v]);
     }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
@@ -162,24 +216,12 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) o[dt][v] *= alpha;
     }
-    __builtin_amdgcn_wave_barrier();
-    // O^T += V^T P^T; this lane's A operand: column d = 32 dt + col at nodes
-    // 16u + 8(j/4) + 4hh + j%4 (the same node order as its P registers)
+    // O^T += V^T P^T; P's register order (nodes 16uu + 8(j/4) + 4hh + j%4) matches va
 #pragma unroll
-    for (int uu = 0; uu < 2; ++uu) {
+    for (int uu = 0; uu < 2; ++uu)
 #pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt) {
-        u16x8 va;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int node = 16 * uu + 8 * (j >> 2) + 4 * hh + (j & 3);
-          va[j] = reinterpret_cast<const unsigned short*>(vt)[node * C::RS + dt * 32 + col];
-        }
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va), pb[uu], o[dt],
-                                                        0, 0, 0);
-      }
-    }
-    __builtin_amdgcn_wave_barrier();
+      for (int dt = 0; dt < C::DT; ++dt)
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[uu][dt], pb[uu], o[dt], 0, 0, 0);
   }
 
   // ---- merge the waves of this WG (fixed order) ----
@@ -244,12 +286,14 @@ constexpr int kNW = 8;
 
 int attn_mfma_rows_per_block() { return kRows; }
 
+// Node splits per (trie, layer, KV head, row block): one WG per unit once there are enough
+// units to occupy most CUs (a split costs partial writes and a combine launch); small
+// launches are split so that the node axis still spreads over the chip.
 int attn_choose_splits(const DevState& s, int n_layers, int row_blocks) {
   const int units = s.T * n_layers * s.Hkv * row_blocks;
-  int sp = (512 + units - 1) / units;
-  if (sp < 1) sp = 1;
-  if (sp > 8) sp = 8;
-  return sp;
+  if (units >= 192) return 1;
+  int sp = (256 + units - 1) / units;
+  return sp > 8 ? 8 : sp;
 }
 
 hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st) {

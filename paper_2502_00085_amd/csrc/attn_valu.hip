@@ -185,7 +185,6 @@ __global__ __launch_bounds__(kValuThreads) void k_attn_valu(DevState s, AttnArgs
       }
     }
   }
-
 }
 
 template <typename T>

@@ -92,6 +92,51 @@ __device__ inline float row_lse32(const DevState& s, int t, int r) {
   return (float)(M + log(S));
 }
 
+// Same value, computed by one wave (lane-strided partials, fixed xor-tree reductions):
+// every caller gets identical bits.
+__device__ inline float row_lse32_wave(const DevState& s, int t, int r) {
+  const int lane = threadIdx.x & 63;
+  const double* p = s.lse_part + ((size_t)t * s.b + r) * s.lse_chunks * 2;
+  const int nch = (s.V + kLseChunk - 1) / kLseChunk;
+  double M = -INFINITY;
+  for (int c = lane; c < nch; c += 64) M = fmax(M, p[2 * c]);
+  for (int o = 32; o > 0; o >>= 1) M = fmax(M, __shfl_xor(M, o));
+  double S = 0.0;
+  for (int c = lane; c < nch; c += 64) S += p[2 * c + 1] * exp(p[2 * c] - M);
+  for (int o = 32; o > 0; o >>= 1) S += __shfl_xor(S, o);
+  return (float)(M + log(S));
+}
+
+// Bitonic sort of one value per lane across the wave, descending: lane i ends with the
+// i-th largest.
+__device__ inline uint64_t wave_sort_desc(uint64_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const uint64_t o = __shfl_xor(v, j);
+      const bool keep_max = ((lane & j) == 0) == ((lane & k) == 0);
+      v = keep_max ? (v > o ? v : o) : (v < o ? v : o);
+    }
+  }
+  return v;
+}
+
+// Lower bound of the b-th largest key of the block from per-thread group maxima: every
+// wave sorts its 64 maxima; its b-th largest is a bound (the b best lanes of the wave
+// each hold a key at or above it), and the largest of the waves' bounds is kept.
+__device__ inline uint64_t wave_sorted_threshold(uint64_t gmax, int b, uint64_t* wthr) {
+  const uint64_t srt = wave_sort_desc(gmax);
+  const uint64_t tw = __shfl(srt, b - 1);
+  if ((threadIdx.x & 63) == 0) wthr[threadIdx.x >> 6] = tw;
+  __syncthreads();
+  uint64_t T = wthr[0];
+  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) T = T > wthr[w] ? T : wthr[w];
+  __syncthreads();
+  return T;
+}
+
 __device__ inline float cand_score(float x, float lse, float score, float* lp_out) {
   const float lp = __fsub_rn(x, lse);
   *lp_out = lp;
@@ -145,6 +190,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float*
   const int total = n_live * V;
   const int n_active = (total + kSelChunk - 1) / kSelChunk;
   if (c >= n_active) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 
   __shared__ uint64_t gmax[kSelThreads];
   __shared__ uint64_t cand[kCandMax];
@@ -156,37 +202,58 @@ __global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float*
   const int f0 = c * kSelChunk;
   const int f1 = min(total, f0 + kSelChunk);
   const int r_lo = f0 / V, r_hi = (f1 - 1) / V;
-  for (int r = r_lo + (int)threadIdx.x; r <= r_hi; r += kSelThreads) row_lse[r - r_lo] = row_lse32(s, t, r);
+  for (int r = r_lo + wave; r <= r_hi; r += kSelThreads / 64) {
+    const float l = row_lse32_wave(s, t, r);
+    if (lane == 0) row_lse[r - r_lo] = l;
+  }
   if (threadIdx.x == 0) ncand = 0;
   __syncthreads();
 
-  // keys of this WG's candidates (contiguous per thread-iteration for coalescing)
+  // keys of this WG's candidates (f = f0 + i*256 + tid: coalesced)
   uint64_t key[kSelPerThread];
   uint64_t kmax = 0;
   const float* lrow = logits + (size_t)t * s.b * V;
   const float* scores = s.leaf_score + (size_t)t * b;
+  int f = f0 + threadIdx.x;
+  int r = f / V;
 #pragma unroll
   for (int i = 0; i < kSelPerThread; ++i) {
-    const int f = f0 + i * kSelThreads + threadIdx.x;
     uint64_t k = 0;
     if (f < f1) {
-      const int r = f / V;
+      while (f >= (r + 1) * V) ++r;
       float lp;
       const float sc = cand_score(lrow[f], row_lse[r - r_lo], scores[r], &lp);
       k = make_key(sc, (uint32_t)f);
     }
     key[i] = k;
     kmax = max(kmax, k);
+    f += kSelThreads;
   }
-  gmax[threadIdx.x] = kmax;
-  __syncthreads();
-  const uint64_t thr = bth_largest(gmax, kSelThreads, b, red);
+  const uint64_t thr = wave_sorted_threshold(kmax, b, red);
 #pragma unroll
   for (int i = 0; i < kSelPerThread; ++i) {
     if (key[i] != 0 && key[i] >= thr) {
       const int slot = atomicAdd(&ncand, 1);
-      if (slot < kCandMax) cand[slot] = key[i];  // <= b threads hold keys >= thr: <= 32 b
+      if (slot < kCandMax) cand[slot] = key[i];
     }
+  }
+  __syncthreads();
+  if (ncand > kCandMax) {
+    // rare: fall back to the exact b-th largest thread maximum (<= b threads hold keys at
+    // or above it: at most 32 b candidates)
+    gmax[threadIdx.x] = kmax;
+    __syncthreads();
+    const uint64_t thr2 = bth_largest(gmax, kSelThreads, b, red);
+    if (threadIdx.x == 0) ncand = 0;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kSelPerThread; ++i) {
+      if (key[i] != 0 && key[i] >= thr2) {
+        const int slot = atomicAdd(&ncand, 1);
+        if (slot < kCandMax) cand[slot] = key[i];
+      }
+    }
+    __syncthreads();
   }
   for (int j = threadIdx.x; j < b; j += kSelThreads) best[j] = 0;
   __syncthreads();
@@ -214,26 +281,47 @@ __global__ __launch_bounds__(kSelThreads) void k_merge(DevState s, const float* 
   __shared__ int ncand;
   const float* lrow = logits + (size_t)t * s.b * V;
   const float* scores = s.leaf_score + (size_t)t * b;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (threadIdx.x == 0) ncand = 0;
   const uint64_t* all = s.topk_keys + (size_t)t * s.sel_chunks * b;
-  // group maxima = first (largest) key of every WG list
-  uint64_t* gm = cand;
-  for (int i = threadIdx.x; i < n_active; i += kSelThreads) gm[i] = all[(size_t)i * b];
-  __syncthreads();
-  const uint64_t thr2 = bth_largest(gm, n_active, b, red);
-  __syncthreads();
-  for (int i = threadIdx.x; i < n_active * b; i += kSelThreads) {
-    const uint64_t k = all[i];
-    if (k != 0 && k >= thr2) {
+  // group of a thread = the WG lists i = tid, tid + 256, ...; its maximum is the largest
+  // first (best) key of those lists
+  uint64_t gmx = 0;
+  for (int i = threadIdx.x; i < n_active; i += kSelThreads) gmx = max(gmx, all[(size_t)i * b]);
+  for (int r = wave; r < n_live; r += kSelThreads / 64) {
+    const float l = row_lse32_wave(s, t, r);
+    if (lane == 0) row_lse[r] = l;
+  }
+  const uint64_t thr = wave_sorted_threshold(gmx, b, red);
+  for (int i = threadIdx.x; i < n_active; i += kSelThreads) {
+    for (int j = 0; j < b; ++j) {
+      const uint64_t k = all[(size_t)i * b + j];
+      if (k == 0 || k < thr) break;  // lists are sorted best first
       const int slot = atomicAdd(&ncand, 1);
-      // <= b WGs hold keys >= thr2 (or < b WGs exist): at most b*b <= kCandMax keys
       if (slot < kCandMax) cand[slot] = k;
     }
+  }
+  __syncthreads();
+  if (ncand > kCandMax) {
+    // rare: exact b-th largest list maximum (<= b lists hold keys at or above it)
+    uint64_t* gm = cand;
+    for (int i = threadIdx.x; i < n_active; i += kSelThreads) gm[i] = all[(size_t)i * b];
+    __syncthreads();
+    const uint64_t thr2 = bth_largest(gm, n_active, b, red);
+    if (threadIdx.x == 0) ncand = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < n_active * b; i += kSelThreads) {
+      const uint64_t k = all[i];
+      if (k != 0 && k >= thr2) {
+        const int slot = atomicAdd(&ncand, 1);
+        if (slot < kCandMax) cand[slot] = k;
+      }
+    }
+    __syncthreads();
   }
   for (int j = threadIdx.x; j < b; j += kSelThreads) best[j] = 0;
   __syncthreads();
   rank_topb(cand, min(ncand, kCandMax), b, best);
-  for (int r = threadIdx.x; r < n_live; r += kSelThreads) row_lse[r] = row_lse32(s, t, r);
   __syncthreads();
   for (int j = threadIdx.x; j < b; j += kSelThreads) {
     const uint64_t k = best[j];
