@@ -44,6 +44,8 @@ def parse():
     p.add_argument("--eager", action="store_true", help="time eager launches instead of a graph replay")
     p.add_argument("--profile-only", action="store_true",
                    help="run warmup + timed steps only (for rocprofv3), no CPU baseline")
+    p.add_argument("--copy-ref-mib", type=int, default=0,
+                   help="also run one plain device copy of this many MiB (reference for HBM counters)")
     return p.parse_args()
 
 
@@ -143,6 +145,14 @@ class Bench:
 
 def gpu_bench(args, w, K):
     import torch
+    if args.copy_ref_mib > 0:
+        n = args.copy_ref_mib * 1024 * 1024 // 2
+        src = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] reference copy: {args.copy_ref_mib} MiB read + {args.copy_ref_mib} MiB written")
+        del src, dst
     bench = Bench(w, K, args.seed)
     stream = torch.cuda.current_stream().cuda_stream
     # warmup (eager)

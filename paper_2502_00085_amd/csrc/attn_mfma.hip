@@ -120,25 +120,43 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   const int my_tiles = ntiles > wave ? (ntiles - wave + NW - 1) / NW : 0;
   bf16x8 kv[C::KSTEPS];
 
+  // this lane's V chunks: load i writes LDS chunk p = 64 i + lane of the tile, i.e. tile
+  // row p / CPR at physical chunk p % CPR, which holds logical chunk c (phys_chunk inverse)
+  int voff[C::VINST];
+#pragma unroll
+  for (int i = 0; i < C::VINST; ++i) {
+    const int p = 64 * i + lane;
+    const int row = p / C::CPR, pc = p % C::CPR;
+    const int c = (pc + C::CPR - 4 * (row % C::NBLK)) % C::CPR;
+    voff[i] = row * D + c * 8;
+  }
+
   // K of a tile -> registers (lane: node tb + col, half hh); V of a tile -> LDS buffer
-  // (direct loads, 16 bytes per lane, rows rotated by phys_chunk); rows past the range
+  // (direct loads, 16 bytes per lane); in the range's last, partial tile rows past the
   // end are clamped to its last node and masked out later
   auto issue = [&](int tile, int buf) {
     const int tb = n0 + tile * 32;
-    const int nk = min(tb + col, n1 - 1);
+    unsigned char* dst = vbuf + buf * C::TILE_BYTES;
+    const bool full = tb + 32 <= n1;
+    const int nk = full ? tb + col : min(tb + col, n1 - 1);
     const uint4* kp = reinterpret_cast<const uint4*>(kpool + (size_t)nk * D + hh * (D / 2));
 #pragma unroll
     for (int t = 0; t < C::KSTEPS; ++t) kv[t] = __builtin_bit_cast(bf16x8, kp[t]);
-    unsigned char* dst = vbuf + buf * C::TILE_BYTES;
+    if (full) {
+      const __bf16* vt = vpool + (size_t)tb * D;
 #pragma unroll
-    for (int i = 0; i < C::VINST; ++i) {
-      const int p = 64 * i + lane;
-      const int row = p / C::CPR, pc = p % C::CPR;
-      const int c = (pc + C::CPR - 4 * (row % C::NBLK)) % C::CPR;  // inverse of phys_chunk
-      const int nv = min(tb + row, n1 - 1);
-      const __bf16* src = vpool + (size_t)nv * D + c * 8;
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                       (__attribute__((address_space(3))) void*)(dst + i * 1024), 16, 0, 0);
+      for (int i = 0; i < C::VINST; ++i)
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(vt + voff[i]),
+                                         (__attribute__((address_space(3))) void*)(dst + i * 1024), 16, 0, 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < C::VINST; ++i) {
+        const int row = (64 * i + lane) / C::CPR;
+        const int nv = min(tb + row, n1 - 1);
+        const __bf16* src = vpool + (size_t)nv * D + (voff[i] - row * D);
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                         (__attribute__((address_space(3))) void*)(dst + i * 1024), 16, 0, 0);
+      }
     }
   };
 
@@ -155,15 +173,18 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     for (int t = 0; t < C::KSTEPS; ++t)
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv[t], qv[t], acc, 0, 0, 0);
 
-    // masks of this lane's nodes 8(v/4) + 4hh + v%4 (tiles past the shared prefix only)
-    const bool masked = tb + 31 >= h.n_shared;
-    uint32_t vis = 0;
+    // visibility of this lane's nodes 8(v/4) + 4hh + v%4: all inside the shared prefix of
+    // a full tile; otherwise range end and the ancestor bit of the row's beam
+    uint32_t vis = 0xffffu;
+    if (tb + 32 > n1 || tb + 32 > h.n_shared) {
+      vis = 0;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int n = tb + 8 * (v >> 2) + 4 * hh + (v & 3);
-      bool ok = n < n1;
-      if (masked && ok) ok = (maskp[n] >> beam_bit) & 1ull;
-      vis |= (uint32_t)ok << v;
+      for (int v = 0; v < 16; ++v) {
+        const int n = tb + 8 * (v >> 2) + 4 * hh + (v & 3);
+        bool ok = n < n1;
+        if (ok && n >= h.n_shared) ok = (maskp[n] >> beam_bit) & 1ull;
+        vis |= (uint32_t)ok << v;
+      }
     }
 
     // V^T operands from LDS: for 16 nodes (uu) and 32 d (dt), two transposed reads, each
@@ -199,13 +220,14 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
     const float mn = fmaxf(m, tmax);
-    const float alpha = exp2f(m - mn);
+    // arguments are <= 0 (or -inf): the bare v_exp_f32 (results below 2^-126 flush to 0)
+    const float alpha = __builtin_amdgcn_exp2f(m - mn);
     m = mn;
     bf16x8 pb[2];
     float ps = 0.0f;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const __bf16 pv = (__bf16)exp2f(sc[v] - mn);
+      const __bf16 pv = (__bf16)__builtin_amdgcn_exp2f(sc[v] - mn);
       ps += (float)pv;
       pb[v >> 3][v & 7] = pv;
     }
