@@ -6,17 +6,18 @@
 // r / G, query head g*G + r % G) and streams the KV head's nodes once, 32 nodes per wave
 // tile, through two dense contractions on v_mfma_f32_32x32x16_bf16:
 //
-//   S^T[node][row] = K_tile . Q^T     A = K rows (a lane holds half a node row: the
-//                                     contraction index d is permuted so that every lane
-//                                     loads D contiguous bytes straight from HBM)
-//   O^T[d][row]   += V_tile^T . P^T   A = V^T: V rows go straight from HBM into LDS
-//                                     (global_load_lds) and come back transposed with
+//   S^T[node][row] = K_tile . Q^T     A = K rows (a lane holds half a node row, read
+//                                     from LDS; the contraction index d is permuted so
+//                                     that each lane's half row is contiguous)
+//   O^T[d][row]   += V_tile^T . P^T   A = V^T: read back transposed with
 //                                     ds_read_b64_tr_b16; B = P^T taken from the S^T
 //                                     accumulator registers as they are (node order
 //                                     permuted to match)
 //
-// Each wave double-buffers its V tiles, so the next tile's K/V loads are in flight while
-// the current tile's softmax and PV run.
+// K and V rows go straight from HBM into the wave's LDS buffers with coalesced 16-byte
+// direct loads (global_load_lds: 1 KB contiguous per instruction); the next tile's loads
+// are issued as soon as the current tile's LDS reads have returned, so they overlap its
+// softmax and PV.
 //
 // The S^T layout puts one query row per lane, so the online softmax needs one cross-lane
 // step (the two half-waves) per tile.  Tiles inside the shared prefix (every beam's
@@ -32,6 +33,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
@@ -47,8 +49,8 @@ struct MfmaCfg {
   static constexpr int VINST = 32 * CPR / 64; // direct-to-LDS loads per 32-node V tile
   static constexpr int TILE_BYTES = 32 * D * 2;
   static constexpr int OS = D + 4;            // LDS row stride of the O merge buffer (floats)
-  static constexpr int V_LDS = NW * 2 * TILE_BYTES;  // two V tiles per wave
-  static constexpr int O_LDS = kRows * OS * 4 + 2 * NW * kRows * 4;
+  static constexpr int V_LDS = NW * 2 * TILE_BYTES;  // one K and one V tile per wave
+  static constexpr int O_LDS = kRows * OS * 4 + 2 * NW * kRows * 4 + 2 * kRows * 4;
   static constexpr int LDS = V_LDS > O_LDS ? V_LDS : O_LDS;
 };
 
@@ -59,6 +61,11 @@ template <int CPR, int NBLK>
 __device__ inline int phys_chunk(int r, int c) {
   return (c + 4 * (r % NBLK)) % CPR;
 }
+
+// s_waitcnt immediates (gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14,
+// expcnt in 6:4, lgkmcnt in 11:8)
+constexpr int kWaitVmAll = 0 | (7 << 4) | (15 << 8);            // vmcnt(0)
+constexpr int kWaitLgkmAll = 15 | (3 << 14) | (7 << 4) | (0 << 8);  // lgkmcnt(0)
 
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
@@ -79,7 +86,8 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     store_leaf_kv<__bf16>(s, a, u, base, N, n_live);
     __syncthreads();
   }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
   const int col = lane & 31, hh = lane >> 5;
 
   // this lane's query row (B operand of S^T): half hh of the row's d range
@@ -103,7 +111,8 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   const __bf16* kpool = static_cast<const __bf16*>(s.k_pool) + pool_row(s, u.t, lab, u.g, base);
   const __bf16* vpool = static_cast<const __bf16*>(s.v_pool) + pool_row(s, u.t, lab, u.g, base);
   const uint64_t* maskp = s.mask + (size_t)u.t * s.cap + base;
-  unsigned char* vbuf = lds + wave * 2 * C::TILE_BYTES;
+  unsigned char* kbuf = lds + wave * 2 * C::TILE_BYTES;
+  unsigned char* vbuf = kbuf + C::TILE_BYTES;
 
   // transposed-read geometry of this lane: 16-lane group g, row m of the group's 16x4
   // block, 4-element column quarter q
@@ -118,79 +127,57 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
 
   const int ntiles = n1 > n0 ? (n1 - n0 + 31) / 32 : 0;
   const int my_tiles = ntiles > wave ? (ntiles - wave + NW - 1) / NW : 0;
-  bf16x8 kv[C::KSTEPS];
 
-  // this lane's V chunks: load i writes LDS chunk p = 64 i + lane of the tile, i.e. tile
-  // row p / CPR at physical chunk p % CPR, which holds logical chunk c (phys_chunk inverse)
-  int voff[C::VINST];
+  // Direct load i of a tile (K or V) writes LDS chunk p = 64 i + lane: tile row p / CPR at
+  // physical chunk p % CPR.  K rows are rotated by one chunk per row (the MFMA-layout
+  // reads of 16 consecutive rows then hit 16 different bank groups); V rows by one
+  // 64-byte block per row (transposed reads of 4 consecutive rows use 4 bank groups).
+  // koff / voff: element offset, inside the row, of the logical chunk this lane loads.
+  int vrow[C::VINST], koff[C::VINST], voff[C::VINST];
 #pragma unroll
   for (int i = 0; i < C::VINST; ++i) {
     const int p = 64 * i + lane;
     const int row = p / C::CPR, pc = p % C::CPR;
-    const int c = (pc + C::CPR - 4 * (row % C::NBLK)) % C::CPR;
-    voff[i] = row * D + c * 8;
+    vrow[i] = row;
+    koff[i] = (pc + C::CPR - row % C::CPR) % C::CPR * 8;
+    voff[i] = (pc + C::CPR - 4 * (row % C::NBLK)) % C::CPR * 8;
   }
+  // this lane's K operand chunks for the 32x32x16 steps: row col, logical chunk
+  // hh * CPR / 2 + t, rotated by col
+  int kread[C::KSTEPS];
+#pragma unroll
+  for (int t = 0; t < C::KSTEPS; ++t) kread[t] = col * (2 * D) + (hh * (C::CPR / 2) + t + col) % C::CPR * 16;
 
-  // K of a tile -> registers (lane: node tb + col, half hh); V of a tile -> LDS buffer
-  // (direct loads, 16 bytes per lane); in the range's last, partial tile rows past the
-  // end are clamped to its last node and masked out later
-  auto issue = [&](int tile, int buf) {
+  // K and V rows of a tile -> the wave's LDS buffers (coalesced 16-byte direct loads); in
+  // the range's last, partial tile, rows past the end are clamped to its last node and
+  // masked out later
+  auto issue = [&](int tile) {
     const int tb = n0 + tile * 32;
-    unsigned char* dst = vbuf + buf * C::TILE_BYTES;
     const bool full = tb + 32 <= n1;
-    const int nk = full ? tb + col : min(tb + col, n1 - 1);
-    const uint4* kp = reinterpret_cast<const uint4*>(kpool + (size_t)nk * D + hh * (D / 2));
 #pragma unroll
-    for (int t = 0; t < C::KSTEPS; ++t) kv[t] = __builtin_bit_cast(bf16x8, kp[t]);
-    if (full) {
-      const __bf16* vt = vpool + (size_t)tb * D;
-#pragma unroll
-      for (int i = 0; i < C::VINST; ++i)
-        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(vt + voff[i]),
-                                         (__attribute__((address_space(3))) void*)(dst + i * 1024), 16, 0, 0);
-    } else {
-#pragma unroll
-      for (int i = 0; i < C::VINST; ++i) {
-        const int row = (64 * i + lane) / C::CPR;
-        const int nv = min(tb + row, n1 - 1);
-        const __bf16* src = vpool + (size_t)nv * D + (voff[i] - row * D);
-        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                         (__attribute__((address_space(3))) void*)(dst + i * 1024), 16, 0, 0);
-      }
+    for (int i = 0; i < C::VINST; ++i) {
+      const int nv = full ? tb + vrow[i] : min(tb + vrow[i], n1 - 1);
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(kpool + (size_t)nv * D + koff[i]),
+                                       (__attribute__((address_space(3))) void*)(kbuf + i * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(vpool + (size_t)nv * D + voff[i]),
+                                       (__attribute__((address_space(3))) void*)(vbuf + i * 1024), 16, 0, 0);
     }
   };
 
-  if (my_tiles > 0) issue(wave, 0);
+  const float scale = a.scale_log2;
+  if (my_tiles > 0) issue(wave);
   for (int k = 0; k < my_tiles; ++k) {
     const int tile = wave + NW * k;
     const int tb = n0 + tile * 32;
-    const int buf = k & 1;
-    __builtin_amdgcn_s_waitcnt(0);  // this tile's K registers and V rows have landed
-    f32x16 acc;
+    __builtin_amdgcn_s_waitcnt(kWaitVmAll);  // this tile's K and V rows have landed in LDS
+    // all LDS reads of the tile first: K operands (MFMA layout) and V^T operands (two
+    // transposed reads per 16 nodes x 32 d, giving this lane column d = 32 dt + col at 4
+    // nodes 16uu + 8 half + 4hh + tm')
+    bf16x8 kv[C::KSTEPS];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
-#pragma unroll
-    for (int t = 0; t < C::KSTEPS; ++t)
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv[t], qv[t], acc, 0, 0, 0);
-
-    // visibility of this lane's nodes 8(v/4) + 4hh + v%4: all inside the shared prefix of
-    // a full tile; otherwise range end and the ancestor bit of the row's beam
-    uint32_t vis = 0xffffu;
-    if (tb + 32 > n1 || tb + 32 > h.n_shared) {
-      vis = 0;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int n = tb + 8 * (v >> 2) + 4 * hh + (v & 3);
-        bool ok = n < n1;
-        if (ok && n >= h.n_shared) ok = (maskp[n] >> beam_bit) & 1ull;
-        vis |= (uint32_t)ok << v;
-      }
-    }
-
-    // V^T operands from LDS: for 16 nodes (uu) and 32 d (dt), two transposed reads, each
-    // giving this lane column d = 32 dt + col at 4 nodes 16uu + 8 half + 4hh + tm'
+    for (int t = 0; t < C::KSTEPS; ++t) kv[t] = *reinterpret_cast<const bf16x8*>(kbuf + kread[t]);
     bf16x8 va[2][C::DT];
-    const __bf16* vb = reinterpret_cast<const __bf16*>(vbuf + buf * C::TILE_BYTES);
+    const __bf16* vb = reinterpret_cast<const __bf16*>(vbuf);
 #pragma unroll
     for (int uu = 0; uu < 2; ++uu) {
 #pragma unroll
@@ -208,28 +195,49 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
         va[uu][dt] = __builtin_bit_cast(bf16x8, both);
       }
     }
-    // the next tile's loads overlap this tile's softmax and PV
-    if (k + 1 < my_tiles) issue(tile + NW, buf ^ 1);
+    // once they have returned, the next tile's loads overwrite the buffers and overlap all
+    // of this tile's math
+    __builtin_amdgcn_s_waitcnt(kWaitLgkmAll);
+    if (k + 1 < my_tiles) issue(tile + NW);
 
-    float sc[16];
-    float tmax = -INFINITY;
+    f32x16 acc;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      sc[v] = ((vis >> v) & 1u) ? acc[v] * a.scale_log2 : -INFINITY;
-      tmax = fmaxf(tmax, sc[v]);
+    for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+#pragma unroll
+    for (int t = 0; t < C::KSTEPS; ++t)
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv[t], qv[t], acc, 0, 0, 0);
+
+    // visibility of this lane's nodes 8(v/4) + 4hh + v%4: all inside the shared prefix of
+    // a full tile (wave-uniform test); otherwise range end and the ancestor bit of the
+    // row's beam; hidden scores become -inf
+    if (tb + 32 > n1 || tb + 32 > h.n_shared) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int n = tb + 8 * (v >> 2) + 4 * hh + (v & 3);
+        bool ok = n < n1;
+        if (ok && n >= h.n_shared) ok = (maskp[n] >> beam_bit) & 1ull;
+        if (!ok) acc[v] = -INFINITY;
+      }
     }
+    float tmax = acc[0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) tmax = fmaxf(tmax, acc[v]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-    const float mn = fmaxf(m, tmax);
-    // arguments are <= 0 (or -inf): the bare v_exp_f32 (results below 2^-126 flush to 0)
+    // running max in the scaled log2 domain; p = 2^(scale * s - m) in one FMA + v_exp
+    // (arguments are <= 0 or -inf: the bare v_exp_f32, results below 2^-126 flush to 0)
+    const float mn = fmaxf(m, tmax * scale);
     const float alpha = __builtin_amdgcn_exp2f(m - mn);
     m = mn;
     bf16x8 pb[2];
-    float ps = 0.0f;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const __bf16 pv = (__bf16)__builtin_amdgcn_exp2f(sc[v] - mn);
-      ps += (float)pv;
-      pb[v >> 3][v & 7] = pv;
+    for (int v = 0; v < 16; ++v) pb[v >> 3][v & 7] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(acc[v], scale, -mn));
+    // row sum of the rounded weights (the ones PV uses), two bf16 per dot2
+    float ps = 0.0f;
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+    for (int v = 0; v < 16; v += 2) {
+      const bf16x2 pair = {pb[v >> 3][v & 7], pb[v >> 3][(v & 7) + 1]};
+      ps = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, ps, false);
     }
     lsum = lsum * alpha + ps;
     if (__any(alpha != 1.0f)) {
@@ -259,7 +267,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   __syncthreads();
   float M = smx[col];
   for (int w = 1; w < NW; ++w) M = fmaxf(M, smx[w * kRows + col]);
-  const float f = exp2f(m - M);
+  const float f = __builtin_amdgcn_exp2f(m - M);
   for (int w = 0; w < NW; ++w) {
     if (wave == w) {
 #pragma unroll
@@ -274,14 +282,25 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     __syncthreads();
   }
 
+  // per-row max and sum over the waves, once per row
+  float* rowm = ssum + NW * kRows;
+  float* rowl = rowm + kRows;
+  if (threadIdx.x < kRows) {
+    const int i = threadIdx.x;
+    float Mi = smx[i], L = 0.0f;
+    for (int w = 1; w < NW; ++w) Mi = fmaxf(Mi, smx[w * kRows + i]);
+    for (int w = 0; w < NW; ++w) L += ssum[w * kRows + i] * __builtin_amdgcn_exp2f(smx[w * kRows + i] - Mi);
+    rowm[i] = Mi;
+    rowl[i] = L;
+  }
+  __syncthreads();
+
   __bf16* outp = static_cast<__bf16*>(a.out);
   const int unit = blockIdx.x / a.splits;
   float* part = s.attn_part + (size_t)unit * a.splits * kRows * (D + 2);
   for (int idx = threadIdx.x; idx < kRows * D; idx += NW * 64) {
     const int i = idx / D, c = idx % D;
-    float Mi = smx[i], L = 0.0f;
-    for (int w = 1; w < NW; ++w) Mi = fmaxf(Mi, smx[w * kRows + i]);
-    for (int w = 0; w < NW; ++w) L += ssum[w * kRows + i] * exp2f(smx[w * kRows + i] - Mi);
+    const float Mi = rowm[i], L = rowl[i];
     const float O = obuf[i * C::OS + c];
     if (a.splits == 1) {
       const int rr = u.rb * kRows + i;

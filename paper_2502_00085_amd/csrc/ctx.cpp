@@ -18,6 +18,7 @@ struct td_ctx {
   std::vector<uint8_t> layer_written;  // per layer, while pending
   int32_t* d_plen = nullptr;
   int splits_override = 0;             // TD_ATTN_SPLITS (tuning): WGs per attention unit
+  int mfma_pipe = 0;                   // TD_ATTN_PIPE (tuning): deep-pipelined MFMA kernel
   std::vector<void*> allocs;
   std::string err;
 };
@@ -151,6 +152,7 @@ td_status td_create(const td_desc* d, td_ctx** out) {
   }
   c->inited.assign(s.T, 0);
   c->layer_written.assign(s.L, 0);
+  if (const char* pp = getenv("TD_ATTN_PIPE")) c->mfma_pipe = atoi(pp);
   if (const char* sp = getenv("TD_ATTN_SPLITS")) c->splits_override = atoi(sp) > 0 ? (atoi(sp) < 64 ? atoi(sp) : 64) : 0;
   *out = c;
   return TD_OK;
@@ -218,7 +220,8 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   a.splits = c->splits_override > 0 ? c->splits_override : td::attn_choose_splits(s, n_layers, a.row_blocks);
   const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;
-  hipError_t e = mfma ? td::launch_attn_mfma(s, a, st) : td::launch_attn_valu(s, a, st);
+  hipError_t e = !mfma ? td::launch_attn_valu(s, a, st)
+                 : c->mfma_pipe ? td::launch_attn_mfma_pipe(s, a, st) : td::launch_attn_mfma(s, a, st);
   if (e == hipSuccess && a.splits > 1) e = td::launch_attn_combine(s, a, rpb, st);
   if (e != hipSuccess) return hip_fail(c, e, "trie_attn_decode launch");
   if (c->pending) {

@@ -70,6 +70,7 @@ struct AttnArgs {
 hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const int32_t* d_tokens,
                               int stride, hipStream_t st);
 hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st);
+hipError_t launch_attn_mfma_pipe(const DevState& s, const AttnArgs& a, hipStream_t st);
 hipError_t launch_attn_valu(const DevState& s, const AttnArgs& a, hipStream_t st);
 hipError_t launch_attn_combine(const DevState& s, const AttnArgs& a, int rows_per_block, hipStream_t st);
 int attn_mfma_rows_per_block();
