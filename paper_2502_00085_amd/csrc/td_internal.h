@@ -88,4 +88,38 @@ hipError_t launch_append_prune(const DevState& s, const int32_t* sel_parent,
 // ---------------------------------------------------------------------------------------
 __device__ inline void set_status(int32_t* status, int code) { atomicCAS(status, 0, code); }
 
+// Number of threads of the block with f set (every thread gets the total).  scratch holds
+// one int per wave.  Contains two block barriers: call from uniform control flow.
+__device__ inline int block_count(bool f, int* scratch) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int c = __popcll(__ballot(f));
+  if (lane == 0) scratch[wave] = c;
+  __syncthreads();
+  int tot = 0;
+  for (int w = 0; w < nw; ++w) tot += scratch[w];
+  __syncthreads();
+  return tot;
+}
+
+// Smallest n in [0, N) with dep[n] > thr (N if there is none), for non-decreasing dep:
+// a block-parallel search that narrows the range by the block size per round (two
+// rounds of independent loads for N up to blockDim^2, instead of log2 N dependent ones).
+__device__ inline int block_first_above(const int32_t* dep, int N, int thr, int* scratch) {
+  int lo = 0, hi = N;  // dep < lo are <= thr, dep >= hi are > thr
+  const int P = blockDim.x;
+  while (hi - lo > P) {
+    const int S = (hi - lo + P - 1) / P;
+    const int pos = lo + (int)threadIdx.x * S;
+    const bool le = pos < hi && dep[pos] <= thr;
+    const int c = block_count(le, scratch);  // samples lo, lo + S, ... lo + (c-1) S are <= thr
+    if (c == 0) return lo;
+    const int nlo = lo + (c - 1) * S + 1;
+    hi = min(hi, lo + c * S);
+    lo = nlo;
+  }
+  const int pos = lo + (int)threadIdx.x;
+  const bool le = pos < hi && dep[pos] <= thr;
+  return lo + block_count(le, scratch);
+}
+
 }  // namespace td

@@ -214,6 +214,16 @@ __global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float*
   uint64_t kmax = 0;
   const float* lrow = logits + (size_t)t * s.b * V;
   const float* scores = s.leaf_score + (size_t)t * b;
+  // all loads first (independent, in flight together), then the keys
+  float xv[kSelPerThread];
+#pragma unroll
+  for (int i = 0; i < kSelPerThread; ++i) {
+    const int f = f0 + i * kSelThreads + (int)threadIdx.x;
+    xv[i] = f < f1 ? lrow[f] : 0.0f;
+  }
+  float rsc[2];  // leaf scores of the (usually at most two) rows this WG's chunk touches
+  rsc[0] = scores[r_lo];
+  rsc[1] = scores[min(r_lo + 1, n_live - 1)];
   int f = f0 + threadIdx.x;
   int r = f / V;
 #pragma unroll
@@ -221,8 +231,9 @@ __global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float*
     uint64_t k = 0;
     if (f < f1) {
       while (f >= (r + 1) * V) ++r;
+      const float sr = r - r_lo < 2 ? rsc[r - r_lo] : scores[r];
       float lp;
-      const float sc = cand_score(lrow[f], row_lse[r - r_lo], scores[r], &lp);
+      const float sc = cand_score(xv[i], row_lse[r - r_lo], sr, &lp);
       k = make_key(sc, (uint32_t)f);
     }
     key[i] = k;
@@ -293,12 +304,21 @@ __global__ __launch_bounds__(kSelThreads) void k_merge(DevState s, const float* 
     if (lane == 0) row_lse[r] = l;
   }
   const uint64_t thr = wave_sorted_threshold(gmx, b, red);
-  for (int i = threadIdx.x; i < n_active; i += kSelThreads) {
-    for (int j = 0; j < b; ++j) {
-      const uint64_t k = all[(size_t)i * b + j];
-      if (k == 0 || k < thr) break;  // lists are sorted best first
-      const int slot = atomicAdd(&ncand, 1);
-      if (slot < kCandMax) cand[slot] = k;
+  // every key of every list, four independent loads per thread per round
+  const int nkeys = n_active * b;
+  for (int i0 = 0; i0 < nkeys; i0 += 4 * kSelThreads) {
+    uint64_t kk[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = i0 + q * kSelThreads + (int)threadIdx.x;
+      kk[q] = i < nkeys ? all[i] : 0;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (kk[q] != 0 && kk[q] >= thr) {
+        const int slot = atomicAdd(&ncand, 1);
+        if (slot < kCandMax) cand[slot] = kk[q];
+      }
     }
   }
   __syncthreads();

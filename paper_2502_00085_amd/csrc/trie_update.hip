@@ -80,7 +80,7 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
   const size_t off = (size_t)t * s.cap;
   __shared__ int sp[kMaxBeam], stok[kMaxBeam];
   __shared__ float ssc[kMaxBeam];
-  __shared__ int err, sh_e, wave_cnt[kAppWaves], wave_cnt2[kAppWaves];
+  __shared__ int err, wave_cnt[kAppWaves], wave_cnt2[kAppWaves];
   __shared__ int full_cnt;
 
   const TrieHdr h = s.hdr[t];
@@ -115,24 +115,94 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
 
   const int d_new = h.leaf_depth + 1;
   // window eviction: the leading run of slots with depth <= d_new - W (depth is sorted)
-  if (tid == 0) {
-    int e = 0;
-    if (s.W > 0) {
-      const int thr = d_new - s.W;
-      int lo = 0, hi = N;  // first logical slot with depth > thr
-      while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (s.depth[off + base + mid] <= thr) lo = mid + 1; else hi = mid;
-      }
-      e = lo;
-    }
-    sh_e = e;
-  }
-  __syncthreads();
-  const int e = sh_e;
+  const int e = s.W > 0 ? block_first_above(s.depth + off + base, N, d_new - s.W, wave_cnt) : 0;
   const int r0 = max(e, h.n_shared);
   const int base_new = base + e;
   const uint64_t full_b = (b == 64) ? ~0ull : ((1ull << b) - 1ull);
+
+  if (N - r0 <= kAppThreads) {
+    // common case: the slots after the shared prefix fit one pass of the block; every
+    // field is loaded up front and new positions stay in LDS
+    __shared__ int lpos[kAppThreads];
+    const int n = r0 + tid;
+    const bool in = n < N;
+    uint64_t m = 0;
+    int id = 0, tk = 0, dp = 0, pp = -1;
+    if (in) {
+      m = s.mask[off + base + n];
+      id = s.node_id[off + base + n];
+      tk = s.token[off + base + n];
+      dp = s.depth[off + base + n];
+      pp = s.parent[off + base + n];
+    }
+    const uint64_t nm = in ? remap_mask(m, sp, b) : 0ull;
+    const bool alive = in && nm != 0ull;
+    int n_alive;
+    const int rank = block_rank(alive, wave_cnt, &n_alive);
+    const int n_full = block_count(alive && nm == full_b, wave_cnt2);
+    const int np = alive ? (r0 - e) + rank : -1;
+    lpos[tid] = np;
+    const int n_new = (r0 - e) + n_alive + b;
+    if (base_new + n_new > s.cap) {
+      if (tid == 0) {
+        set_status(s.status, kDevEcapacity);
+        s.status[1] = 1;
+        s.n_moves[t] = 0;
+      }
+      return;
+    }
+    __syncthreads();
+    auto new_phys = [&](int lp) -> int {  // new physical slot of old logical slot lp < N
+      if (lp < e) return -1;
+      if (lp < r0) return base + lp;
+      const int q = lpos[lp - r0];
+      return q >= 0 ? base_new + q : -1;
+    };
+    int par = -1;
+    if (alive && pp >= 0) {
+      const int lp = pp - base;
+      par = (lp >= 0 && lp < n) ? new_phys(lp) : -1;
+    }
+    const bool moved = alive && (np + e != n);
+    int n_moved;
+    const int mrank = block_rank(moved, wave_cnt2, &n_moved);
+    if (moved) s.moves[off + mrank] = make_int2(base + n, base_new + np);
+    // all fields were read before the first barrier: rewrite in place
+    if (alive) {
+      const size_t dst = off + base_new + np;
+      s.node_id[dst] = id;
+      s.token[dst] = tk;
+      s.depth[dst] = dp;
+      s.parent[dst] = par;
+      s.mask[dst] = nm;
+    }
+    if (n_live != b) {
+      for (int x = e + tid; x < r0; x += kAppThreads) s.mask[off + base + x] = full_b;
+    }
+    if (tid == 0 && e > 0 && e < r0) s.parent[off + base + e] = -1;
+    if (tid < b) {
+      const size_t dst = off + base_new + (r0 - e) + n_alive + tid;
+      s.node_id[dst] = h.next_id + tid;
+      s.token[dst] = stok[tid];
+      s.depth[dst] = d_new;
+      s.parent[dst] = new_phys(N - n_live + sp[tid]);
+      s.mask[dst] = 1ull << tid;
+      s.leaf_score[(size_t)t * b + tid] = ssc[tid];
+    }
+    if (tid == 0) {
+      TrieHdr nh;
+      nh.n_nodes = n_new;
+      nh.base = base_new;
+      nh.n_live = b;
+      nh.n_shared = (r0 - e) + n_full + (b == 1 ? 1 : 0);
+      nh.leaf_depth = d_new;
+      nh.next_id = h.next_id + b;
+      nh.pad0 = nh.pad1 = 0;
+      s.hdr[t] = nh;
+      s.n_moves[t] = n_moved;
+    }
+    return;
+  }
 
   // pass 1: new masks of the slots after the shared prefix, survivors' new positions
   int alive_run = 0;
