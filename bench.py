@@ -107,13 +107,11 @@ class Bench:
         L, ctx = self.B.lib(), self.dec.ctx
         pend = i > 0
         if ev is not None:
-            ev[0].record()
+            self.B.td_set_attn_events(ctx, ev.start, ev.stop)
         st = L.trie_attn_decode(ctx, 0, self.w.n_layers, self.q[i].data_ptr(),
                                 self.kn[i].data_ptr() if pend else None,
                                 self.vn[i].data_ptr() if pend else None, self.out.data_ptr(),
                                 ctypes.c_float(self.scale), stream)
-        if ev is not None:
-            ev[1].record()
         st |= L.beam_logsoftmax_topk(ctx, self.logits[i].data_ptr(), self.sp.data_ptr(), self.st.data_ptr(),
                                      self.ss.data_ptr(), self.sl.data_ptr(), self.lse.data_ptr(),
                                      self.par[i].data_ptr(), self.tok[i].data_ptr(), self.ps.data_ptr(),
@@ -161,17 +159,20 @@ def gpu_bench(args, w, K):
         bench.step(i, stream)
     torch.cuda.synchronize()
 
-    # attention kernel duration: HIP events around every launch of an eager pass over the
-    # same K steps (events cannot be recorded inside a graph on this platform)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(K)]
+    # attention kernel duration: kernel-timestamp HIP events (dispatch -> completion of the
+    # attention launch, the interval a kernel profiler reports) on every launch of an eager
+    # pass over the same K steps, on the stream the kernels run on (events cannot be
+    # recorded inside a graph on this platform)
+    evs = [bench.B.KernelEvents() for _ in range(K)]
     bench.init()
     t0 = time.perf_counter()
     for i in range(K):
         bench.step(i, stream, evs[i])
     torch.cuda.synchronize()
     eager_s = time.perf_counter() - t0
-    attn_ms = np.array([a.elapsed_time(b) for a, b in evs])
+    attn_ms = np.array([e.elapsed_ms() for e in evs])
+    for e in evs:
+        e.close()
 
     mode, graph = ("eager", None) if args.eager else ("graph", None)
     if mode == "graph":

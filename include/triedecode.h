@@ -129,6 +129,15 @@ td_status trie_attn_decode(td_ctx* ctx, int32_t layer_begin, int32_t n_layers, c
                            const void* d_k_new, const void* d_v_new, void* d_out, float scale,
                            hipStream_t stream);
 
+/* Measurement hook, not part of the method: the next trie_attn_decode call (only that
+ * one) launches its kernels with kernel-timestamp events (hipExtLaunchKernel): `start`
+ * takes the dispatch time of its first kernel and `stop` the completion time of its last,
+ * so hipEventElapsedTime(start, stop) is the call's device time as a kernel profiler
+ * reports it, without the fences that hipEventRecord adds between launches.  Both events
+ * are created by the caller (hipEventCreate) and must outlive that call; both NULL clears
+ * a pending request.  One NULL and one non-NULL: TD_EINVAL. */
+td_status td_set_attn_events(td_ctx* ctx, hipEvent_t start, hipEvent_t stop);
+
 /* Alg 1 / Alg 2 top-b with cumulative log-probability scores.  For every trie, row r <
  * n_live:  lse_r = fp32 rounding of the fp64 log-sum-exp of the row;  per candidate
  * (r, v):  lp = fl32(x - lse_r),  s = fl32(leaf_score_r + lp)  (IEEE round to nearest

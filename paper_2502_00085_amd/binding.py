@@ -70,13 +70,14 @@ def lib() -> ctypes.CDLL:
         L.td_read_state.argtypes = [vp, i32, ctypes.POINTER(TdState)]
         L.td_load_state.argtypes = [vp, i32, ctypes.POINTER(TdState)]
         L.td_get_status.argtypes = [vp]
+        L.td_set_attn_events.argtypes = [vp, vp, vp]
         L.td_error_string.argtypes = [vp]
         L.td_error_string.restype = ctypes.c_char_p
         L.td_status_name.argtypes = [i32]
         L.td_status_name.restype = ctypes.c_char_p
         for name in ("td_create", "td_destroy", "td_init_prompt", "trie_attn_decode",
                      "beam_logsoftmax_topk", "trie_append_prune", "td_read_state", "td_load_state",
-                     "td_get_status"):
+                     "td_get_status", "td_set_attn_events"):
             getattr(L, name).restype = ctypes.c_int32
         _lib = L
     return _lib
@@ -154,6 +155,48 @@ def trie_attn_decode(ctx, dims: Dims, layer_begin: int, n_layers: int, q, k_new,
     _check(ctx, lib().trie_attn_decode(
         ctx, int(layer_begin), int(n_layers), _ptr(q, tdt, nq, "q"), _ptr(k_new, tdt, nk, "k_new"),
         _ptr(v_new, tdt, nk, "v_new"), _ptr(out, tdt, nq, "out"), float(scale), _stream(stream)))
+
+
+def td_set_attn_events(ctx, start, stop):
+    """Kernel-timestamp events for the next trie_attn_decode call (raw hipEvent_t handles,
+    e.g. KernelEvents.start / .stop; None, None clears)."""
+    _check(ctx, lib().td_set_attn_events(ctx, start, stop))
+
+
+class KernelEvents:
+    """A pair of plain HIP events (hipEventCreate) for td_set_attn_events; elapsed_ms()
+    synchronises on the stop event."""
+
+    _hip = None
+
+    def __init__(self):
+        if KernelEvents._hip is None:
+            H = ctypes.CDLL("libamdhip64.so")
+            H.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+            H.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            H.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+            H.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                              ctypes.c_void_p]
+            KernelEvents._hip = H
+        self.start, self.stop = ctypes.c_void_p(), ctypes.c_void_p()
+        for e in (self.start, self.stop):
+            if KernelEvents._hip.hipEventCreate(ctypes.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+
+    def elapsed_ms(self) -> float:
+        H = KernelEvents._hip
+        if H.hipEventSynchronize(self.stop) != 0:
+            raise RuntimeError("hipEventSynchronize failed")
+        ms = ctypes.c_float()
+        if H.hipEventElapsedTime(ctypes.byref(ms), self.start, self.stop) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def close(self):
+        for e in (self.start, self.stop):
+            if e.value:
+                KernelEvents._hip.hipEventDestroy(e)
+                e.value = None
 
 
 def beam_logsoftmax_topk(ctx, dims: Dims, logits, sel_parent, sel_token, sel_score, sel_logprob,

@@ -46,12 +46,13 @@ __global__ __launch_bounds__(256) void k_attn_combine(DevState s, AttnArgs a, in
 
 }  // namespace
 
-hipError_t launch_attn_combine(const DevState& s, const AttnArgs& a, int rows_per_block, hipStream_t st) {
+hipError_t launch_attn_combine(const DevState& s, const AttnArgs& a, int rows_per_block, hipStream_t st,
+                               hipEvent_t ev0, hipEvent_t ev1) {
   const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks);
   if (s.dtype == TD_F32)
-    hipLaunchKernelGGL(k_attn_combine<float>, grid, dim3(256), 0, st, s, a, rows_per_block);
+    hipExtLaunchKernelGGL(k_attn_combine<float>, grid, dim3(256), 0, st, ev0, ev1, 0, s, a, rows_per_block);
   else
-    hipLaunchKernelGGL(k_attn_combine<__bf16>, grid, dim3(256), 0, st, s, a, rows_per_block);
+    hipExtLaunchKernelGGL(k_attn_combine<__bf16>, grid, dim3(256), 0, st, ev0, ev1, 0, s, a, rows_per_block);
   return hipGetLastError();
 }
 

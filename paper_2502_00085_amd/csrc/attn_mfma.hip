@@ -337,12 +337,13 @@ int attn_choose_splits(const DevState& s, int n_layers, int row_blocks) {
   return sp > 8 ? 8 : sp;
 }
 
-hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st) {
-  const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * a.splits);
+hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
+                            hipEvent_t ev1) {
+  const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * a.splits), block(kNW * 64);
   switch (s.D) {
-    case 64: hipLaunchKernelGGL((k_attn_mfma<64, kNW>), grid, dim3(kNW * 64), 0, st, s, a); break;
-    case 96: hipLaunchKernelGGL((k_attn_mfma<96, kNW>), grid, dim3(kNW * 64), 0, st, s, a); break;
-    case 128: hipLaunchKernelGGL((k_attn_mfma<128, kNW>), grid, dim3(kNW * 64), 0, st, s, a); break;
+    case 64: hipExtLaunchKernelGGL((k_attn_mfma<64, kNW>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
+    case 96: hipExtLaunchKernelGGL((k_attn_mfma<96, kNW>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
+    case 128: hipExtLaunchKernelGGL((k_attn_mfma<128, kNW>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -188,11 +188,13 @@ __global__ __launch_bounds__(kValuThreads) void k_attn_valu(DevState s, AttnArgs
 }
 
 template <typename T>
-hipError_t launch_t(const DevState& s, const AttnArgs& a, dim3 grid, hipStream_t st) {
+hipError_t launch_t(const DevState& s, const AttnArgs& a, dim3 grid, hipStream_t st, hipEvent_t ev0,
+                    hipEvent_t ev1) {
+  const dim3 block(kValuThreads);
   switch (s.D) {
-    case 64: hipLaunchKernelGGL((k_attn_valu<T, 4>), grid, dim3(kValuThreads), 0, st, s, a); break;
-    case 96: hipLaunchKernelGGL((k_attn_valu<T, 6>), grid, dim3(kValuThreads), 0, st, s, a); break;
-    case 128: hipLaunchKernelGGL((k_attn_valu<T, 8>), grid, dim3(kValuThreads), 0, st, s, a); break;
+    case 64: hipExtLaunchKernelGGL((k_attn_valu<T, 4>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
+    case 96: hipExtLaunchKernelGGL((k_attn_valu<T, 6>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
+    case 128: hipExtLaunchKernelGGL((k_attn_valu<T, 8>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -202,10 +204,11 @@ hipError_t launch_t(const DevState& s, const AttnArgs& a, dim3 grid, hipStream_t
 
 int attn_valu_rows_per_block() { return kValuRows; }
 
-hipError_t launch_attn_valu(const DevState& s, const AttnArgs& a, hipStream_t st) {
+hipError_t launch_attn_valu(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
+                            hipEvent_t ev1) {
   const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * a.splits);
-  if (s.dtype == TD_F32) return launch_t<float>(s, a, grid, st);
-  return launch_t<__bf16>(s, a, grid, st);
+  if (s.dtype == TD_F32) return launch_t<float>(s, a, grid, st, ev0, ev1);
+  return launch_t<__bf16>(s, a, grid, st, ev0, ev1);
 }
 
 }  // namespace td

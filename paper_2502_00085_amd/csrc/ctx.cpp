@@ -18,7 +18,8 @@ struct td_ctx {
   std::vector<uint8_t> layer_written;  // per layer, while pending
   int32_t* d_plen = nullptr;
   int splits_override = 0;             // TD_ATTN_SPLITS (tuning): WGs per attention unit
-  int mfma_pipe = 0;                   // TD_ATTN_PIPE (tuning): deep-pipelined MFMA kernel
+  hipEvent_t attn_ev0 = nullptr;       // td_set_attn_events: kernel-timestamp events of the
+  hipEvent_t attn_ev1 = nullptr;       //   next trie_attn_decode launch
   std::vector<void*> allocs;
   std::string err;
 };
@@ -152,7 +153,6 @@ td_status td_create(const td_desc* d, td_ctx** out) {
   }
   c->inited.assign(s.T, 0);
   c->layer_written.assign(s.L, 0);
-  if (const char* pp = getenv("TD_ATTN_PIPE")) c->mfma_pipe = atoi(pp);
   if (const char* sp = getenv("TD_ATTN_SPLITS")) c->splits_override = atoi(sp) > 0 ? (atoi(sp) < 64 ? atoi(sp) : 64) : 0;
   *out = c;
   return TD_OK;
@@ -220,9 +220,11 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   a.splits = c->splits_override > 0 ? c->splits_override : td::attn_choose_splits(s, n_layers, a.row_blocks);
   const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;
-  hipError_t e = !mfma ? td::launch_attn_valu(s, a, st)
-                 : c->mfma_pipe ? td::launch_attn_mfma_pipe(s, a, st) : td::launch_attn_mfma(s, a, st);
-  if (e == hipSuccess && a.splits > 1) e = td::launch_attn_combine(s, a, rpb, st);
+  hipEvent_t ev0 = c->attn_ev0, ev1 = c->attn_ev1;
+  c->attn_ev0 = c->attn_ev1 = nullptr;
+  hipEvent_t main_ev1 = a.splits > 1 ? nullptr : ev1;
+  hipError_t e = mfma ? td::launch_attn_mfma(s, a, st, ev0, main_ev1) : td::launch_attn_valu(s, a, st, ev0, main_ev1);
+  if (e == hipSuccess && a.splits > 1) e = td::launch_attn_combine(s, a, rpb, st, nullptr, ev1);
   if (e != hipSuccess) return hip_fail(c, e, "trie_attn_decode launch");
   if (c->pending) {
     for (int l = layer_begin; l < layer_begin + n_layers; ++l) c->layer_written[l] = 1;
@@ -230,6 +232,15 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
     for (int l = 0; l < s.L; ++l) all = all && c->layer_written[l];
     if (all) c->pending = false;
   }
+  return TD_OK;
+}
+
+td_status td_set_attn_events(td_ctx* c, hipEvent_t start, hipEvent_t stop) {
+  if (!c) return TD_EINVAL;
+  c->err.clear();
+  if ((start == nullptr) != (stop == nullptr)) return fail(c, TD_EINVAL, "pass both events or neither");
+  c->attn_ev0 = start;
+  c->attn_ev1 = stop;
   return TD_OK;
 }
 

@@ -1,6 +1,7 @@
 // Internal definitions shared by the host ABI (ctx.cpp) and the gfx950 kernels.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -69,10 +70,14 @@ struct AttnArgs {
 
 hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const int32_t* d_tokens,
                               int stride, hipStream_t st);
-hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st);
-hipError_t launch_attn_mfma_pipe(const DevState& s, const AttnArgs& a, hipStream_t st);
-hipError_t launch_attn_valu(const DevState& s, const AttnArgs& a, hipStream_t st);
-hipError_t launch_attn_combine(const DevState& s, const AttnArgs& a, int rows_per_block, hipStream_t st);
+// The attention launchers take optional kernel-timestamp events (hipExtLaunchKernel):
+// ev0 records the dispatch of the launched kernel, ev1 its completion (null = none).
+hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
+                            hipEvent_t ev1);
+hipError_t launch_attn_valu(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
+                            hipEvent_t ev1);
+hipError_t launch_attn_combine(const DevState& s, const AttnArgs& a, int rows_per_block, hipStream_t st,
+                               hipEvent_t ev0, hipEvent_t ev1);
 int attn_mfma_rows_per_block();
 int attn_valu_rows_per_block();
 int attn_choose_splits(const DevState& s, int n_layers, int row_blocks);
