@@ -92,8 +92,8 @@ td_status td_create(const td_desc* d, td_ctx** out) {
   if (d->vocab < d->beam_width) return fail(nullptr, TD_EINVAL, "vocab must be >= beam_width");
   if ((int64_t)d->vocab * d->beam_width >= (int64_t(1) << 31))
     return fail(nullptr, TD_EINVAL, "vocab * beam_width must be < 2^31");
-  if (((int64_t)d->vocab * d->beam_width + td::kSelChunk - 1) / td::kSelChunk > 4096)
-    return fail(nullptr, TD_EUNSUPPORTED, "vocab * beam_width above 2^25 is not supported");
+  if ((int64_t)d->beam_width * ((d->vocab + td::kLseChunk - 1) / td::kLseChunk) > td::topb_max_chunk_lists())
+    return fail(nullptr, TD_EUNSUPPORTED, "beam_width * ceil(vocab / 4096) must be <= %d", td::topb_max_chunk_lists());
   if (d->n_layers < 1 || d->n_kv_heads < 1 || d->n_q_heads < d->n_kv_heads ||
       d->n_q_heads % d->n_kv_heads != 0)
     return fail(nullptr, TD_EINVAL, "need n_layers >= 1, n_kv_heads >= 1, n_q_heads %% n_kv_heads == 0");
@@ -131,7 +131,6 @@ td_status td_create(const td_desc* d, td_ctx** out) {
   s.k_pool = d->k_pool;
   s.v_pool = d->v_pool;
   s.lse_chunks = (s.V + td::kLseChunk - 1) / td::kLseChunk;
-  s.sel_chunks = (int)(((int64_t)s.V * s.b + td::kSelChunk - 1) / td::kSelChunk);
   s.attn_pairs_max = 1024;
   s.attn_part_floats = s.attn_pairs_max * 32 * (s.D + 2);
   const size_t tc = (size_t)s.T * s.cap;
@@ -142,8 +141,7 @@ td_status td_create(const td_desc* d, td_ctx** out) {
       (e = alloc(c, &s.leaf_score, (size_t)s.T * s.b)) != hipSuccess ||
       (e = alloc(c, &s.status, 2)) != hipSuccess ||
       (e = alloc(c, &s.lse_part, (size_t)s.T * s.b * s.lse_chunks * 2)) != hipSuccess ||
-      (e = alloc(c, &s.topk_keys, (size_t)s.T * s.sel_chunks * s.b)) != hipSuccess ||
-      (e = alloc(c, &s.topk_count, (size_t)s.T)) != hipSuccess ||
+      (e = alloc(c, &s.topk_keys, (size_t)s.T * s.b * s.lse_chunks * 16)) != hipSuccess ||
       (e = alloc(c, &s.newpos, tc)) != hipSuccess || (e = alloc(c, &s.moves, tc)) != hipSuccess ||
       (e = alloc(c, &s.n_moves, (size_t)s.T)) != hipSuccess ||
       (e = alloc(c, &s.attn_part, (size_t)s.attn_part_floats)) != hipSuccess ||

@@ -36,20 +36,16 @@ struct DevState {
                          // was rejected (the trie kept its previous state)
   // workspace
   double* lse_part;      // [T][b][lse_chunks][2]  (chunk max, chunk sum of exp)
-  uint64_t* topk_keys;   // [T][sel_chunks][b]
-  int32_t* topk_count;   // [T] arrival counters of the select kernel (self-resetting)
+  uint64_t* topk_keys;   // [T][b][lse_chunks][16]  largest logit (key) of each 256-logit sub-chunk
   int32_t* newpos;       // [T][cap] new logical position of each old logical slot, -1 dead
   int2* moves;           // [T][cap] (src phys, dst phys) rows to move, ascending src
   int32_t* n_moves;      // [T]
   float* attn_part;      // split-combine partials
-  int lse_chunks, sel_chunks, attn_part_floats, attn_pairs_max;
+  int lse_chunks, attn_part_floats, attn_pairs_max;
 };
 
 // selection / log-softmax geometry
-constexpr int kLseChunk = 4096;      // logits per WG in the log-sum-exp pass
-constexpr int kSelThreads = 256;
-constexpr int kSelPerThread = 32;
-constexpr int kSelChunk = kSelThreads * kSelPerThread;  // candidates per WG in the select pass
+constexpr int kLseChunk = 4096;      // logits of one row per WG in the chunk pass
 constexpr int kMaxBeam = 64;
 
 // status codes written by kernels (same values as td_status)
@@ -85,6 +81,7 @@ hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_
                                   int32_t* sel_token, float* sel_score, float* sel_logprob,
                                   float* lse, const int32_t* pair_parent, const int32_t* pair_token,
                                   float* pair_score, hipStream_t st);
+int topb_max_chunk_lists();  // limit of b * lse_chunks per trie
 hipError_t launch_append_prune(const DevState& s, const int32_t* sel_parent,
                                const int32_t* sel_token, const float* sel_score, hipStream_t st);
 

@@ -5,373 +5,446 @@
 //   lse_r = fl32( m_r + log(sum_v exp(x_rv - m_r)) )   accumulated in fp64
 //   lp    = fl32(x - lse_r),   s = fl32(score_r + lp)   (round to nearest even)
 // Candidates are ranked by the 64-bit key  (ord(s) << 32) | (2^32 - 1 - (r*V + v)),
-// where ord() maps floats to order-preserving unsigned integers: a larger key is a
-// better candidate and equal scores go to the lower flat index.  Keys are unique.
+// where ord() maps floats to order-preserving unsigned integers (-0 and +0 merged): a
+// larger key is a better candidate and equal scores go to the lower flat index.  Keys are
+// unique.
 //
-// Kernels:
-//   k_lse_partials  grid (lse_chunks, b, T): max and fp64 sum of exp of a 4096-logit chunk
-//   k_select        grid (sel_chunks, T): lse of the rows it touches (from the partials),
-//                   keys of 8192 candidates, the WG's top-b list
-//   k_merge         grid (T): merges the WG lists of a trie into the final selection
-// (separate launches instead of a last-arriving-WG merge: a device-scope fence costs an
-// L2 writeback + invalidate per WG on this multi-XCD part)
-// Top-b of a set split into groups (threads or WGs) whose maxima are known: the b-th
-// largest group maximum is a lower bound of the b-th largest key, so only keys at or
-// above it (at most b groups' worth) are ranked, each by counting larger candidates.
+// Two launches:
+//   k_topb_chunk  grid (chunks of 4096 logits, rows, tries): the chunk's max and its fp64
+//                 sum of exp(x - max), and the largest logit (key, with its index) of each
+//                 of its 16 sub-chunks (the 256 logits of one wave: 4 runs of 64);
+//   k_topb_final  grid (tries): every row's lse from its chunk partials; the score of each
+//                 sub-chunk's largest logit; a bound L at most the b-th largest of those;
+//                 the "hot" sub-chunks whose largest score reaches L, read again; the exact
+//                 top-b of their logits scoring at or above L.
+// Exactness: within a row s is a non-decreasing function of x (fl32 subtraction and
+// addition are monotone), so a sub-chunk's best score is that of its largest logit.  At
+// least b sub-chunk maxima score >= L, hence the b-th best score is >= L, and every logit
+// scoring >= L lies in a sub-chunk whose best score is >= L: a hot one.
+// (Two launches instead of a last-arriving-WG merge: a device-scope fence costs an L2
+// writeback + invalidate per WG on this multi-XCD part.)
 #include "td_internal.h"
 
 namespace td {
 
 namespace {
 
-__device__ inline uint32_t float_ord(float f) {
-  if (f == 0.0f) f = 0.0f;  // -0 and +0 compare equal: give them one key
+constexpr int kChunkThreads = 1024;
+constexpr int kChunkPer = kLseChunk / kChunkThreads;  // logits per thread
+constexpr int kChunkWaves = kChunkThreads / 64;
+constexpr int kFinalThreads = 1024;
+constexpr int kFinalWaves = kFinalThreads / 64;
+constexpr int kCandMax = 4096;
+constexpr int kSub = kChunkWaves;                     // sub-chunks (waves) per chunk
+constexpr int kSubPer = 4;                            // sub-chunk maxima per thread
+
+// Order-preserving maps of floats to unsigned integers: raw (-0 below +0) for logits, so
+// a key keeps the logit's exact bits; merged zeros for scores (equal scores tie).
+__device__ inline uint32_t ord_raw(float f) {
   const uint32_t u = __float_as_uint(f);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
-
-__device__ inline float wave_max_f(float v) {
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+__device__ inline float ord_inv(uint32_t o) {
+  return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
 }
-__device__ inline double wave_sum_d(double v) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
+__device__ inline uint32_t ord_score(float f) { return ord_raw(f == 0.0f ? 0.0f : f); }
 
-constexpr int kLseThreads = 256;
-constexpr int kLsePer = kLseChunk / kLseThreads;
-
-__global__ __launch_bounds__(kLseThreads) void k_lse_partials(DevState s, const float* logits) {
-  const int c = blockIdx.x, r = blockIdx.y, t = blockIdx.z;
-  if (r >= s.hdr[t].n_live) return;
-  const float* row = logits + ((size_t)t * s.b + r) * s.V;
-  const int v0 = c * kLseChunk;
-  float x[kLsePer];
-  float m = -INFINITY;
-#pragma unroll
-  for (int i = 0; i < kLsePer; ++i) {
-    const int v = v0 + i * kLseThreads + threadIdx.x;
-    x[i] = v < s.V ? row[v] : -INFINITY;
-    m = fmaxf(m, x[i]);
-  }
-  __shared__ float wm[kLseThreads / 64];
-  __shared__ double ws[kLseThreads / 64];
-  m = wave_max_f(m);
-  if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
-  __syncthreads();
-  m = wm[0];
-  for (int w = 1; w < kLseThreads / 64; ++w) m = fmaxf(m, wm[w]);
-  double acc = 0.0;
-  const double md = (double)m;
-#pragma unroll
-  for (int i = 0; i < kLsePer; ++i) {
-    const int v = v0 + i * kLseThreads + threadIdx.x;
-    if (v < s.V) acc += exp((double)x[i] - md);
-  }
-  acc = wave_sum_d(acc);
-  if ((threadIdx.x & 63) == 0) ws[threadIdx.x >> 6] = acc;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    double tot = 0.0;
-    for (int w = 0; w < kLseThreads / 64; ++w) tot += ws[w];
-    double* p = s.lse_part + (((size_t)t * s.b + r) * s.lse_chunks + c) * 2;
-    p[0] = md;
-    p[1] = tot;
-  }
+__device__ inline uint64_t x_key(float x, uint32_t flat) {
+  return ((uint64_t)ord_raw(x) << 32) | (uint64_t)(0xffffffffu - flat);
 }
-
-// fp64 log-sum-exp of row r from its chunk partials (fixed order: bit-reproducible)
-__device__ inline float row_lse32(const DevState& s, int t, int r) {
-  const double* p = s.lse_part + ((size_t)t * s.b + r) * s.lse_chunks * 2;
-  const int nch = (s.V + kLseChunk - 1) / kLseChunk;
-  double M = p[0];
-  for (int c = 1; c < nch; ++c) M = fmax(M, p[2 * c]);
-  double S = 0.0;
-  for (int c = 0; c < nch; ++c) S += p[2 * c + 1] * exp(p[2 * c] - M);
-  return (float)(M + log(S));
+__device__ inline uint64_t s_key(float sc, uint32_t flat) {
+  return ((uint64_t)ord_score(sc) << 32) | (uint64_t)(0xffffffffu - flat);
 }
-
-// Same value, computed by one wave (lane-strided partials, fixed xor-tree reductions):
-// every caller gets identical bits.
-__device__ inline float row_lse32_wave(const DevState& s, int t, int r) {
-  const int lane = threadIdx.x & 63;
-  const double* p = s.lse_part + ((size_t)t * s.b + r) * s.lse_chunks * 2;
-  const int nch = (s.V + kLseChunk - 1) / kLseChunk;
-  double M = -INFINITY;
-  for (int c = lane; c < nch; c += 64) M = fmax(M, p[2 * c]);
-  for (int o = 32; o > 0; o >>= 1) M = fmax(M, __shfl_xor(M, o));
-  double S = 0.0;
-  for (int c = lane; c < nch; c += 64) S += p[2 * c + 1] * exp(p[2 * c] - M);
-  for (int o = 32; o > 0; o >>= 1) S += __shfl_xor(S, o);
-  return (float)(M + log(S));
-}
-
-// Bitonic sort of one value per lane across the wave, descending: lane i ends with the
-// i-th largest.
-__device__ inline uint64_t wave_sort_desc(uint64_t v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int k = 2; k <= 64; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const uint64_t o = __shfl_xor(v, j);
-      const bool keep_max = ((lane & j) == 0) == ((lane & k) == 0);
-      v = keep_max ? (v > o ? v : o) : (v < o ? v : o);
-    }
-  }
-  return v;
-}
-
-// Lower bound of the b-th largest key of the block from per-thread group maxima: every
-// wave sorts its 64 maxima; its b-th largest is a bound (the b best lanes of the wave
-// each hold a key at or above it), and the largest of the waves' bounds is kept.
-__device__ inline uint64_t wave_sorted_threshold(uint64_t gmax, int b, uint64_t* wthr) {
-  const uint64_t srt = wave_sort_desc(gmax);
-  const uint64_t tw = __shfl(srt, b - 1);
-  if ((threadIdx.x & 63) == 0) wthr[threadIdx.x >> 6] = tw;
-  __syncthreads();
-  uint64_t T = wthr[0];
-  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) T = T > wthr[w] ? T : wthr[w];
-  __syncthreads();
-  return T;
-}
+__device__ inline uint32_t key_flat(uint64_t k) { return 0xffffffffu - (uint32_t)(k & 0xffffffffu); }
+__device__ inline float key_x(uint64_t kx) { return ord_inv((uint32_t)(kx >> 32)); }
 
 __device__ inline float cand_score(float x, float lse, float score, float* lp_out) {
   const float lp = __fsub_rn(x, lse);
   *lp_out = lp;
   return __fadd_rn(score, lp);
 }
-
-__device__ inline uint64_t make_key(float s, uint32_t flat) {
-  return ((uint64_t)float_ord(s) << 32) | (uint64_t)(0xffffffffu - flat);
+__device__ inline float score_only(float x, float lse, float score) {
+  float lp;
+  return cand_score(x, lse, score, &lp);
 }
 
-constexpr int kCandMax = 4096;
+// Wave reductions in a fixed (DPP) order: bit-reproducible.
+extern "C" __device__ float __ockl_wfred_max_f32(float);
+extern "C" __device__ uint32_t __ockl_wfred_max_u32(uint32_t);
+extern "C" __device__ double __ockl_wfred_add_f64(double);
+extern "C" __device__ double __ockl_wfred_max_f64(double);
 
-// Rank candidates cand[0..n) by counting larger keys; writes the b best in order to out.
-__device__ inline void rank_topb(const uint64_t* cand, int n, int b, uint64_t* out) {
+__device__ inline uint64_t wave_max_u64(uint64_t v) {
+  const uint32_t hi = __ockl_wfred_max_u32((uint32_t)(v >> 32));
+  const uint32_t lo = __ockl_wfred_max_u32((uint32_t)(v >> 32) == hi ? (uint32_t)v : 0u);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ inline uint64_t lanes_below() {
+  const int lane = threadIdx.x & 63;
+  return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+}
+
+// b-th largest of the wave's values v[0..K) over all lanes, with multiplicity (the
+// largest T with #{values >= T} >= b; 0 when there are fewer than b values > 0), by
+// bitwise descent with ballots: no LDS traffic.
+template <int K>
+__device__ inline uint32_t wave_bth32(const uint32_t (&v)[K], int b) {
+  uint32_t T = 0;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t c = T | (1u << bit);
+    int n = 0;
+#pragma unroll
+    for (int q = 0; q < K; ++q) n += __popcll(__ballot(v[q] >= c));
+    if (n >= b) T = c;
+  }
+  return T;
+}
+
+// Appends the values val[q] with take[q] of this wave to dst (and val2 to dst2) at slots
+// counted by one atomic on *count per wave; slots at or beyond cap are dropped (the count
+// still grows).
+template <int K, typename T1, typename T2>
+__device__ inline void wave_append(const T1* val, const T2* val2, const bool* take, T1* dst, T2* dst2,
+                                   int cap, int* count) {
+  uint64_t bal[K];
+  int tot = 0;
+#pragma unroll
+  for (int q = 0; q < K; ++q) {
+    bal[q] = __ballot(take[q]);
+    tot += __popcll(bal[q]);
+  }
+  if (tot == 0) return;
+  int base = 0;
+  if ((threadIdx.x & 63) == 0) base = atomicAdd(count, tot);
+  base = __builtin_amdgcn_readfirstlane(base);
+  const uint64_t below = lanes_below();
+#pragma unroll
+  for (int q = 0; q < K; ++q) {
+    const int slot = base + __popcll(bal[q] & below);
+    if (take[q] && slot < cap) {
+      dst[slot] = val[q];
+      if (dst2) dst2[slot] = val2[q];
+    }
+    base += __popcll(bal[q]);
+  }
+}
+
+// Writes the b largest of the distinct keys cand[0..n) to out[0..b) in order, with their
+// companions.  Wave 0 alone ranks up to 64 keys held in registers; more keys are ranked by
+// the whole block by counting.  Call from uniform control flow.
+__device__ inline void rank_topb(const uint64_t* cand, const uint64_t* comp, int n, int b, uint64_t* out,
+                                 uint64_t* out_comp) {
+  if (n <= 64) {
+    if (threadIdx.x < 64) {
+      const int lane = threadIdx.x;
+      const uint64_t k = lane < n ? cand[lane] : 0;
+      int rank = 0;
+      for (int j = 0; j < n; ++j) {
+        const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)k, j);
+        const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(k >> 32), j);
+        rank += (((uint64_t)hi << 32) | lo) > k;
+      }
+      if (lane < n && rank < b) {
+        out[rank] = k;
+        out_comp[rank] = comp[lane];
+      }
+    }
+    return;
+  }
   for (int i = threadIdx.x; i < n; i += blockDim.x) {
     const uint64_t k = cand[i];
     int rank = 0;
     for (int j = 0; j < n; ++j) rank += cand[j] > k;
-    if (rank < b) out[rank] = k;
+    if (rank < b) {
+      out[rank] = k;
+      out_comp[rank] = comp[i];
+    }
   }
 }
 
-// Lower bound of the b-th largest key from the group maxima gmax[0..n): the b-th largest
-// maximum when there are at least b groups (each of the b largest groups holds a key at or
-// above it), else 0 (every key is a candidate).  Zero entries (empty groups) are allowed.
-__device__ inline uint64_t bth_largest(const uint64_t* gmax, int n, int b, uint64_t* red) {
-  if (n < b) return 0;
-  uint64_t mine = ~0ull;
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    const uint64_t k = gmax[i];
-    int rank = 0;
-    for (int j = 0; j < n; ++j) rank += gmax[j] > k;
-    if (rank < b) mine = min(mine, k);
-  }
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint64_t other = __shfl_xor(mine, o);
-    mine = min(mine, other);
-  }
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mine;
-  __syncthreads();
-  uint64_t r = red[0];
-  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) r = min(r, red[w]);
-  __syncthreads();
-  return r;
-}
-
-__global__ __launch_bounds__(kSelThreads) void k_select(DevState s, const float* logits) {
-  const int c = blockIdx.x, t = blockIdx.y;
-  const int b = s.b, V = s.V;
-  const int n_live = s.hdr[t].n_live;
-  const int total = n_live * V;
-  const int n_active = (total + kSelChunk - 1) / kSelChunk;
-  if (c >= n_active) return;
+// One chunk of one row: max, fp64 sum of exp(x - max), largest logit key of each wave.
+__global__ __launch_bounds__(kChunkThreads) void k_topb_chunk(DevState s, const float* logits) {
+  const int c = blockIdx.x, r = blockIdx.y, t = blockIdx.z;
+  const int V = s.V, b = s.b;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const float* row = logits + ((size_t)t * b + r) * V;
+  const int v0 = c * kLseChunk;
+  __shared__ float wm[kChunkWaves];
+  __shared__ double ws[kChunkWaves];
 
-  __shared__ uint64_t gmax[kSelThreads];
-  __shared__ uint64_t cand[kCandMax];
-  __shared__ uint64_t red[kSelThreads / 64];
-  __shared__ uint64_t best[kMaxBeam];
-  __shared__ float row_lse[kMaxBeam];
-  __shared__ int ncand;
-
-  const int f0 = c * kSelChunk;
-  const int f1 = min(total, f0 + kSelChunk);
-  const int r_lo = f0 / V, r_hi = (f1 - 1) / V;
-  for (int r = r_lo + wave; r <= r_hi; r += kSelThreads / 64) {
-    const float l = row_lse32_wave(s, t, r);
-    if (lane == 0) row_lse[r - r_lo] = l;
-  }
-  if (threadIdx.x == 0) ncand = 0;
-  __syncthreads();
-
-  // keys of this WG's candidates (f = f0 + i*256 + tid: coalesced)
-  uint64_t key[kSelPerThread];
-  uint64_t kmax = 0;
-  const float* lrow = logits + (size_t)t * s.b * V;
-  const float* scores = s.leaf_score + (size_t)t * b;
-  // all loads first (independent, in flight together), then the keys
-  float xv[kSelPerThread];
+  // the loads go out before n_live is known (every row of the [T][b][V] block exists)
+  float x[kChunkPer];
 #pragma unroll
-  for (int i = 0; i < kSelPerThread; ++i) {
-    const int f = f0 + i * kSelThreads + (int)threadIdx.x;
-    xv[i] = f < f1 ? lrow[f] : 0.0f;
+  for (int i = 0; i < kChunkPer; ++i) {
+    const int v = v0 + i * kChunkThreads + (int)threadIdx.x;
+    x[i] = v < V ? row[v] : -INFINITY;
   }
-  float rsc[2];  // leaf scores of the (usually at most two) rows this WG's chunk touches
-  rsc[0] = scores[r_lo];
-  rsc[1] = scores[min(r_lo + 1, n_live - 1)];
-  int f = f0 + threadIdx.x;
-  int r = f / V;
+  if (r >= s.hdr[t].n_live) return;
+  float m = -INFINITY;
+  uint64_t km = 0;
+  const uint32_t flat0 = (uint32_t)r * (uint32_t)V + (uint32_t)v0 + threadIdx.x;
 #pragma unroll
-  for (int i = 0; i < kSelPerThread; ++i) {
-    uint64_t k = 0;
-    if (f < f1) {
-      while (f >= (r + 1) * V) ++r;
-      const float sr = r - r_lo < 2 ? rsc[r - r_lo] : scores[r];
-      float lp;
-      const float sc = cand_score(xv[i], row_lse[r - r_lo], sr, &lp);
-      k = make_key(sc, (uint32_t)f);
-    }
-    key[i] = k;
-    kmax = max(kmax, k);
-    f += kSelThreads;
+  for (int i = 0; i < kChunkPer; ++i) {
+    const int v = v0 + i * kChunkThreads + (int)threadIdx.x;
+    m = fmaxf(m, x[i]);
+    const uint64_t k = v < V ? x_key(x[i], flat0 + (uint32_t)(i * kChunkThreads)) : 0;
+    km = k > km ? k : km;
   }
-  const uint64_t thr = wave_sorted_threshold(kmax, b, red);
-#pragma unroll
-  for (int i = 0; i < kSelPerThread; ++i) {
-    if (key[i] != 0 && key[i] >= thr) {
-      const int slot = atomicAdd(&ncand, 1);
-      if (slot < kCandMax) cand[slot] = key[i];
-    }
+  m = __ockl_wfred_max_f32(m);
+  km = wave_max_u64(km);
+  const size_t list = ((size_t)t * b + r) * s.lse_chunks + c;
+  if (lane == 0) {
+    wm[wave] = m;
+    s.topk_keys[list * kSub + wave] = km;  // 0 when the wave holds no logit
   }
   __syncthreads();
-  if (ncand > kCandMax) {
-    // rare: fall back to the exact b-th largest thread maximum (<= b threads hold keys at
-    // or above it: at most 32 b candidates)
-    gmax[threadIdx.x] = kmax;
-    __syncthreads();
-    const uint64_t thr2 = bth_largest(gmax, kSelThreads, b, red);
-    if (threadIdx.x == 0) ncand = 0;
-    __syncthreads();
+  m = wm[0];
+  for (int w = 1; w < kChunkWaves; ++w) m = fmaxf(m, wm[w]);
+  const double md = (double)m;
+  double acc = 0.0;
 #pragma unroll
-    for (int i = 0; i < kSelPerThread; ++i) {
-      if (key[i] != 0 && key[i] >= thr2) {
-        const int slot = atomicAdd(&ncand, 1);
-        if (slot < kCandMax) cand[slot] = key[i];
-      }
-    }
-    __syncthreads();
+  for (int i = 0; i < kChunkPer; ++i) {
+    const int v = v0 + i * kChunkThreads + (int)threadIdx.x;
+    if (v < V) acc += exp((double)x[i] - md);
   }
-  for (int j = threadIdx.x; j < b; j += kSelThreads) best[j] = 0;
+  acc = __ockl_wfred_add_f64(acc);
+  if (lane == 0) ws[wave] = acc;
   __syncthreads();
-  rank_topb(cand, min(ncand, kCandMax), b, best);
-  __syncthreads();
-  uint64_t* my = s.topk_keys + ((size_t)t * s.sel_chunks + c) * b;
-  for (int j = threadIdx.x; j < b; j += kSelThreads) my[j] = best[j];
+  if (threadIdx.x == 0) {
+    double tot = 0.0;
+    for (int w = 0; w < kChunkWaves; ++w) tot += ws[w];
+    s.lse_part[list * 2] = md;
+    s.lse_part[list * 2 + 1] = tot;
+  }
 }
 
-// Merge of the per-WG top-b lists of one trie (one WG per trie), then the outputs.
-__global__ __launch_bounds__(kSelThreads) void k_merge(DevState s, const float* logits,
-                                                       int32_t* sel_parent, int32_t* sel_token,
-                                                       float* sel_score, float* sel_logprob,
-                                                       float* lse_out, const int32_t* pair_parent,
-                                                       const int32_t* pair_token, float* pair_score) {
+// fp64 log-sum-exp of row r from its chunk partials, computed by one wave (lane-strided
+// partials, fixed-order wave reductions): bit-reproducible.
+__device__ inline float row_lse32_wave(const double* p, int nch) {
+  const int lane = threadIdx.x & 63;
+  double M = -INFINITY;
+  for (int c = lane; c < nch; c += 64) M = fmax(M, p[2 * c]);
+  M = __ockl_wfred_max_f64(M);
+  double S = 0.0;
+  for (int c = lane; c < nch; c += 64) S += p[2 * c + 1] * exp(p[2 * c] - M);
+  S = __ockl_wfred_add_f64(S);
+  return (float)(M + log(S));
+}
+
+// b-th largest (with multiplicity) of the 16 values w[0..16) in LDS, computed by every
+// wave: lane i < 16 ranks w[i] against all 16 (ties by position, so exactly one lane has
+// rank b-1), and that lane's value is read back.  Needs b <= 16.
+__device__ inline uint32_t wave_bth_of16(const uint32_t* w, int b) {
+  const int lane = threadIdx.x & 63;
+  const uint4* w4 = reinterpret_cast<const uint4*>(w);
+  uint32_t v[16];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint4 x = w4[q];
+    v[4 * q] = x.x;
+    v[4 * q + 1] = x.y;
+    v[4 * q + 2] = x.z;
+    v[4 * q + 3] = x.w;
+  }
+  const int i = lane & 15;
+  uint32_t u = v[0];
+#pragma unroll
+  for (int j = 1; j < 16; ++j) u = i == j ? v[j] : u;
+  int above = 0;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) above += (v[j] > u) | ((v[j] == u) & (j < i));
+  const uint64_t own = __ballot(lane < 16 && above == b - 1);
+  return __builtin_amdgcn_readlane(u, __ffsll((unsigned long long)own) - 1);
+}
+
+// i / d for 0 <= i < 2^21 and d >= 1, with inv = 1.0f / d: (i + 0.5) / d is at least
+// 0.5 / d away from an integer, and the float error, below (i / d) * 2^-22, is smaller.
+__device__ inline int div_small(int i, float inv) { return (int)(((float)i + 0.5f) * inv); }
+
+// Merge of one trie's chunks into the final selection, then the outputs.
+__global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const float* logits,
+                                                              int32_t* sel_parent, int32_t* sel_token,
+                                                              float* sel_score, float* sel_logprob,
+                                                              float* lse_out, const int32_t* pair_parent,
+                                                              const int32_t* pair_token, float* pair_score) {
   const int t = blockIdx.x;
-  const int b = s.b, V = s.V;
-  const int n_live = s.hdr[t].n_live;
-  const int total = n_live * V;
-  const int n_active = (total + kSelChunk - 1) / kSelChunk;
-  __shared__ uint64_t cand[kCandMax];
-  __shared__ uint64_t red[kSelThreads / 64];
-  __shared__ uint64_t best[kMaxBeam];
-  __shared__ float row_lse[kMaxBeam];
-  __shared__ int ncand;
-  const float* lrow = logits + (size_t)t * s.b * V;
-  const float* scores = s.leaf_score + (size_t)t * b;
+  const int b = s.b, V = s.V, nch = s.lse_chunks;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (threadIdx.x == 0) ncand = 0;
-  const uint64_t* all = s.topk_keys + (size_t)t * s.sel_chunks * b;
-  // group of a thread = the WG lists i = tid, tid + 256, ...; its maximum is the largest
-  // first (best) key of those lists
-  uint64_t gmx = 0;
-  for (int i = threadIdx.x; i < n_active; i += kSelThreads) gmx = max(gmx, all[(size_t)i * b]);
-  for (int r = wave; r < n_live; r += kSelThreads / 64) {
-    const float l = row_lse32_wave(s, t, r);
+  __shared__ uint64_t cand[kCandMax], cand_x[kCandMax];
+  __shared__ __align__(16) uint32_t wt[kFinalWaves];
+  __shared__ int wsum[kFinalWaves];
+  __shared__ uint64_t best_k[kMaxBeam], best_c[kMaxBeam];
+  __shared__ float row_lse[kMaxBeam], row_score[kMaxBeam];
+  __shared__ int ncand, nhot;
+  __shared__ int hot[kCandMax];
+  const float* lrow = logits + (size_t)t * b * V;
+  const uint64_t* smax = s.topk_keys + (size_t)t * b * nch * kSub;  // [row][chunk][sub]
+  const int per_row = nch * kSub;
+
+  // Independent loads first: the sub-chunk maxima of every row (rows >= n_live are dropped
+  // once n_live is known), pair logits, leaf scores, every row's lse, then n_live.
+  uint64_t km0[kSubPer];
+#pragma unroll
+  for (int q = 0; q < kSubPer; ++q) {
+    const int i = q * kFinalThreads + (int)threadIdx.x;
+    km0[q] = i < b * per_row ? smax[i] : 0;
+  }
+  float pair_x = 0.0f;
+  int pp = -1, pv = -1;
+  if (pair_parent != nullptr && (int)threadIdx.x < b) {
+    pp = pair_parent[(size_t)t * b + threadIdx.x];
+    pv = pair_token[(size_t)t * b + threadIdx.x];
+    if (pp >= 0 && pp < b && pv >= 0 && pv < V) pair_x = lrow[(size_t)pp * V + pv];
+  }
+  for (int r = threadIdx.x; r < b; r += kFinalThreads) row_score[r] = s.leaf_score[(size_t)t * b + r];
+  for (int r = wave; r < b; r += kFinalWaves) {
+    const float l = row_lse32_wave(s.lse_part + ((size_t)t * b + r) * nch * 2, nch);
     if (lane == 0) row_lse[r] = l;
   }
-  const uint64_t thr = wave_sorted_threshold(gmx, b, red);
-  // every key of every list, four independent loads per thread per round
-  const int nkeys = n_active * b;
-  for (int i0 = 0; i0 < nkeys; i0 += 4 * kSelThreads) {
-    uint64_t kk[4];
+  const int n_live = s.hdr[t].n_live;
+  if (threadIdx.x == 0) ncand = nhot = 0;
+  __syncthreads();
+  const int nsub = n_live * per_row;
+  const float inv_per_row = 1.0f / (float)per_row;
+
+  // Bound L (ord of a score): with b <= 16, the b-th largest of the 16 waves' maxima of
+  // the sub-chunk maximum scores (16 distinct sub-chunks reach their wave's maximum);
+  // otherwise the largest of the waves' exact b-th largest.  Rounds of kSubPer *
+  // kFinalThreads sub-chunks.
+  uint32_t o[kSubPer];
+  uint32_t L = 0, lmax = 0;
+  for (int i0 = 0; i0 < nsub; i0 += kSubPer * kFinalThreads) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int i = i0 + q * kSelThreads + (int)threadIdx.x;
-      kk[q] = i < nkeys ? all[i] : 0;
+    for (int q = 0; q < kSubPer; ++q) {
+      const int i = i0 + q * kFinalThreads + (int)threadIdx.x;
+      const uint64_t km = i >= nsub ? 0 : i0 == 0 ? km0[q] : smax[i];
+      const int r = div_small(i, inv_per_row);
+      o[q] = km != 0 ? ord_score(score_only(key_x(km), row_lse[r], row_score[r])) : 0u;
+      lmax = o[q] > lmax ? o[q] : lmax;
     }
+    if (b > kFinalWaves) {
+      const uint32_t tw = wave_bth32<kSubPer>(o, b);
+      L = tw > L ? tw : L;
+    }
+  }
+  if (b <= kFinalWaves) L = __ockl_wfred_max_u32(lmax);
+  if (lane == 0) wt[wave] = L;
+  __syncthreads();
+  if (b <= kFinalWaves) {
+    L = wave_bth_of16(wt, b);
+  } else {
+    L = 0;
+    for (int w = 0; w < kFinalWaves; ++w) L = wt[w] > L ? wt[w] : L;
+  }
+  // hot sub-chunks: largest score >= L (at least b of them)
+  for (int i0 = 0; i0 < nsub; i0 += kSubPer * kFinalThreads) {
+    int id[kSubPer];
+    bool take[kSubPer];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (kk[q] != 0 && kk[q] >= thr) {
-        const int slot = atomicAdd(&ncand, 1);
-        if (slot < kCandMax) cand[slot] = kk[q];
+    for (int q = 0; q < kSubPer; ++q) {
+      const int i = i0 + q * kFinalThreads + (int)threadIdx.x;
+      // (o[] holds the last round of the bound loop: recompute from the keys)
+      const uint64_t km = i >= nsub ? 0 : i0 == 0 ? km0[q] : smax[i];
+      const int r = div_small(i, inv_per_row);
+      const uint32_t oq = km != 0 ? ord_score(score_only(key_x(km), row_lse[r], row_score[r])) : 0u;
+      id[q] = i;
+      take[q] = i < nsub && oq != 0 && oq >= L;
+    }
+    wave_append<kSubPer, int, int>(id, nullptr, take, hot, nullptr, kCandMax, &nhot);
+  }
+  __syncthreads();
+  const int n_hot = nhot;
+  if (n_hot <= kCandMax) {
+    // one wave per hot sub-chunk: its 4 runs of 64 logits; keep those scoring >= L
+    for (int h = wave; h < n_hot; h += kFinalWaves) {
+      const int i = hot[h];
+      const int r = i / per_row, c = (i / kSub) % nch, sw = i % kSub;
+      float xs[kChunkPer];
+#pragma unroll
+      for (int q = 0; q < kChunkPer; ++q) {
+        const int v = c * kLseChunk + q * kChunkThreads + sw * 64 + lane;
+        xs[q] = v < V ? lrow[(size_t)r * V + v] : 0.0f;
       }
+      uint64_t ks[kChunkPer], kx[kChunkPer];
+      bool take[kChunkPer];
+#pragma unroll
+      for (int q = 0; q < kChunkPer; ++q) {
+        const int v = c * kLseChunk + q * kChunkThreads + sw * 64 + lane;
+        const uint32_t flat = (uint32_t)r * (uint32_t)V + (uint32_t)v;
+        const float sc = score_only(xs[q], row_lse[r], row_score[r]);
+        take[q] = v < V && ord_score(sc) >= L;
+        ks[q] = s_key(sc, flat);
+        kx[q] = x_key(xs[q], flat);
+      }
+      wave_append<kChunkPer, uint64_t, uint64_t>(ks, kx, take, cand, cand_x, kCandMax, &ncand);
     }
   }
   __syncthreads();
-  if (ncand > kCandMax) {
-    // rare: exact b-th largest list maximum (<= b lists hold keys at or above it)
-    uint64_t* gm = cand;
-    for (int i = threadIdx.x; i < n_active; i += kSelThreads) gm[i] = all[(size_t)i * b];
-    __syncthreads();
-    const uint64_t thr2 = bth_largest(gm, n_active, b, red);
+  if (n_hot > kCandMax || ncand > kCandMax) {
+    // rare (many equal scores at the bound): exact b-th largest key by bisection over the
+    // key space, counting over every live logit; then exactly b keys lie at or above it
+    const int total = n_live * V;
+    uint64_t lo = 1, hi = ~0ull;
+    while (lo < hi) {
+      const uint64_t mid = lo + (hi - lo) / 2 + 1;
+      int cnt = 0;
+      for (int f = threadIdx.x; f < total; f += kFinalThreads) {
+        const int r = f / V;
+        cnt += s_key(score_only(lrow[f], row_lse[r], row_score[r]), (uint32_t)f) >= mid;
+      }
+      for (int sh = 32; sh > 0; sh >>= 1) cnt += __shfl_xor(cnt, sh);
+      if (lane == 0) wsum[wave] = cnt;
+      __syncthreads();
+      int tot = 0;
+      for (int w = 0; w < kFinalWaves; ++w) tot += wsum[w];
+      __syncthreads();
+      if (tot >= b) lo = mid;
+      else hi = mid - 1;
+    }
     if (threadIdx.x == 0) ncand = 0;
     __syncthreads();
-    for (int i = threadIdx.x; i < n_active * b; i += kSelThreads) {
-      const uint64_t k = all[i];
-      if (k != 0 && k >= thr2) {
-        const int slot = atomicAdd(&ncand, 1);
-        if (slot < kCandMax) cand[slot] = k;
+    for (int f = threadIdx.x; f < total; f += kFinalThreads) {
+      const int r = f / V;
+      const float x = lrow[f];
+      const uint64_t ks = s_key(score_only(x, row_lse[r], row_score[r]), (uint32_t)f);
+      if (ks >= lo) {
+        const int slot = atomicAdd(&ncand, 1);  // exactly b
+        cand[slot] = ks;
+        cand_x[slot] = x_key(x, (uint32_t)f);
       }
     }
     __syncthreads();
   }
-  for (int j = threadIdx.x; j < b; j += kSelThreads) best[j] = 0;
+  for (int j = threadIdx.x; j < b; j += kFinalThreads) best_k[j] = best_c[j] = 0;
   __syncthreads();
-  rank_topb(cand, min(ncand, kCandMax), b, best);
+  rank_topb(cand, cand_x, min(ncand, kCandMax), b, best_k, best_c);
   __syncthreads();
-  for (int j = threadIdx.x; j < b; j += kSelThreads) {
-    const uint64_t k = best[j];
-    uint32_t f = 0xffffffffu - (uint32_t)(k & 0xffffffffu);
-    if (k == 0 || f >= (uint32_t)total) {  // unreachable: there are >= b candidates
+
+  for (int j = threadIdx.x; j < b; j += kFinalThreads) {
+    const uint64_t kx = best_c[j];
+    uint32_t f = key_flat(kx);
+    float x = key_x(kx);
+    if (best_k[j] == 0 || f >= (uint32_t)(n_live * V)) {  // unreachable: there are >= b candidates
       set_status(s.status, kDevEinval);
       f = 0;
+      x = 0.0f;
     }
     const int r = (int)(f / (uint32_t)V), v = (int)(f % (uint32_t)V);
     float lp;
-    const float sc = cand_score(lrow[f], row_lse[r], scores[r], &lp);
+    const float sc = cand_score(x, row_lse[r], row_score[r], &lp);
     sel_parent[(size_t)t * b + j] = r;
     sel_token[(size_t)t * b + j] = v;
     sel_score[(size_t)t * b + j] = sc;
     sel_logprob[(size_t)t * b + j] = lp;
   }
   if (lse_out != nullptr) {
-    for (int r = threadIdx.x; r < b; r += kSelThreads)
+    for (int r = threadIdx.x; r < b; r += kFinalThreads)
       lse_out[(size_t)t * b + r] = r < n_live ? row_lse[r] : 0.0f;
   }
-  if (pair_parent != nullptr) {
-    for (int j = threadIdx.x; j < b; j += kSelThreads) {
-      const int p = pair_parent[(size_t)t * b + j], v = pair_token[(size_t)t * b + j];
-      float sc = __uint_as_float(0x7fc00000u);  // NaN for an out-of-range pair
-      if (p >= 0 && p < n_live && v >= 0 && v < V) {
-        float lp;
-        sc = cand_score(lrow[(size_t)p * V + v], row_lse[p], scores[p], &lp);
-      }
-      pair_score[(size_t)t * b + j] = sc;
-    }
+  if (pair_parent != nullptr && (int)threadIdx.x < b) {
+    float sc = __uint_as_float(0x7fc00000u);  // NaN for an out-of-range pair
+    if (pp >= 0 && pp < n_live && pv >= 0 && pv < V) sc = score_only(pair_x, row_lse[pp], row_score[pp]);
+    pair_score[(size_t)t * b + threadIdx.x] = sc;
   }
 }
 
@@ -381,16 +454,14 @@ hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_
                                   int32_t* sel_token, float* sel_score, float* sel_logprob,
                                   float* lse, const int32_t* pair_parent, const int32_t* pair_token,
                                   float* pair_score, hipStream_t st) {
-  const int nch = (s.V + kLseChunk - 1) / kLseChunk;
-  hipLaunchKernelGGL(k_lse_partials, dim3(nch, s.b, s.T), dim3(kLseThreads), 0, st, s, logits);
+  hipLaunchKernelGGL(k_topb_chunk, dim3(s.lse_chunks, s.b, s.T), dim3(kChunkThreads), 0, st, s, logits);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_select, dim3(s.sel_chunks, s.T), dim3(kSelThreads), 0, st, s, logits);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_merge, dim3(s.T), dim3(kSelThreads), 0, st, s, logits, sel_parent, sel_token,
-                     sel_score, sel_logprob, lse, pair_parent, pair_token, pair_score);
+  hipLaunchKernelGGL(k_topb_final, dim3(s.T), dim3(kFinalThreads), 0, st, s, logits, sel_parent,
+                     sel_token, sel_score, sel_logprob, lse, pair_parent, pair_token, pair_score);
   return hipGetLastError();
 }
+
+int topb_max_chunk_lists() { return kCandMax; }
 
 }  // namespace td

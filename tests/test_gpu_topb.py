@@ -1,0 +1,121 @@
+"""GPU parity of beam_logsoftmax_topk alone on constructed logits and leaf scores.
+
+The trie is loaded with td_load_state (a prompt chain whose tail has n_live children), so
+the leaf scores can be set freely; logits are crafted to reach the selection's corner cases:
+several 4096-logit chunks with a ragged tail, a last chunk with fewer logits than b, rows
+of equal logits (every candidate tied), and logits so close together that the float32
+score s = fl32(score + fl32(x - lse)) merges many distinct logits into one value at the
+b-th place.  Expected values come from oracle.beam (full sort).  Integers and float32 bits
+must match exactly.
+"""
+import numpy as np
+import pytest
+
+import oracle.beam as obeam
+from gpu_harness import log
+
+pytestmark = pytest.mark.gpu
+
+
+def chain_with_leaves(P, n_live, scores):
+    """State of a prompt chain of P nodes whose tail has n_live leaf children."""
+    N = P + n_live
+    full = (1 << n_live) - 1 if n_live < 64 else (1 << 64) - 1
+    mask = [full] * P + [1 << j for j in range(n_live)]
+    return dict(n_nodes=N, n_live=n_live, next_id=N, kv_pending=0,
+                node_id=np.arange(N), parent_slot=[-1] + list(range(P - 1)) + [P - 1] * n_live,
+                token=np.zeros(N), depth=list(range(P)) + [P] * n_live,
+                mask=np.array(mask, dtype=np.uint64), leaf_slot=np.arange(P, N),
+                leaf_score=np.asarray(scores, np.float32))
+
+
+def run_topb(b, logits, scores, pairs=None):
+    import torch
+    import paper_2502_00085_amd.binding as B
+    n_live, V = logits.shape
+    log(f"topb case b={b} n_live={n_live} V={V}")
+    P = 5
+    dec = B.TrieDecoder(1, b, P + b + 2, V, 1, 1, 1, 64, 0, "bf16")
+    try:
+        dec.load_state(0, chain_with_leaves(P, n_live, scores))
+        full = np.zeros((b, V), np.float32)
+        full[:n_live] = logits
+        lg = torch.from_numpy(full).reshape(1, b, V).cuda()
+        i32 = dict(dtype=torch.int32, device="cuda")
+        f32 = dict(dtype=torch.float32, device="cuda")
+        sp, st = torch.empty((1, b), **i32), torch.empty((1, b), **i32)
+        ss, sl, lse = torch.empty((1, b), **f32), torch.empty((1, b), **f32), torch.empty((1, b), **f32)
+        pp = pt = ps = None
+        if pairs is not None:
+            pp = torch.tensor(pairs[0], **i32).reshape(1, b)
+            pt = torch.tensor(pairs[1], **i32).reshape(1, b)
+            ps = torch.empty((1, b), **f32)
+        dec.logsoftmax_topk(lg, sp, st, ss, sl, lse, pp, pt, ps)
+        torch.cuda.synchronize()
+        assert dec.status() == B.TD_OK
+        ref = obeam.select(logits, np.asarray(scores, np.float32), b)
+        assert np.array_equal(sp.cpu().numpy()[0], ref["sel_parent"]), (sp.cpu().numpy()[0], ref["sel_parent"])
+        assert np.array_equal(st.cpu().numpy()[0], ref["sel_token"]), (st.cpu().numpy()[0], ref["sel_token"])
+        for got, want in ((ss, ref["sel_score"]), (sl, ref["sel_logprob"]), (lse, ref["lse"])):
+            g = got.cpu().numpy()[0][:len(want)]
+            assert np.array_equal(g.view(np.uint32), np.asarray(want, np.float32).view(np.uint32)), (g, want)
+        if pairs is not None:
+            want, _ = obeam.pair_scores(logits, ref["lse"], scores, pairs[0], pairs[1])
+            g = ps.cpu().numpy()[0]
+            assert np.array_equal(g.view(np.uint32), want.view(np.uint32))
+    finally:
+        dec.close()
+
+
+def test_random_rows_several_chunks_ragged_tail():
+    g = np.random.default_rng(1)
+    b, V = 8, 3 * 4096 + 17
+    logits = g.normal(0, 3, (b, V)).astype(np.float32)
+    scores = -np.sort(g.uniform(0, 4, b)).astype(np.float32)
+    pairs = (g.integers(0, b, b), g.integers(0, V, b))
+    run_topb(b, logits, scores, pairs)
+
+
+def test_last_chunk_shorter_than_beam():
+    g = np.random.default_rng(2)
+    b, V = 8, 4096 + 3
+    logits = g.normal(0, 3, (3, V)).astype(np.float32)
+    logits[:, -3:] += 20.0  # the best candidates sit in the 3-logit tail chunk
+    run_topb(b, logits, np.array([0.0, -0.5, -1.0], np.float32))
+
+
+def test_all_candidates_tied():
+    b, V = 6, 2 * 4096 + 100
+    run_topb(b, np.full((4, V), 1.5, np.float32), np.zeros(4, np.float32))
+
+
+@pytest.mark.parametrize("direction", [1.0, -1.0])
+def test_score_rounding_merges_logits_at_the_boundary(direction):
+    """Logits 1e-7 apart and leaf scores near -1000 (float32 spacing 6e-5): hundreds of
+    candidates share the b-th score, and the lowest flat indices among them are not the
+    largest logits of their chunk, so the chunk has to be rescanned."""
+    b, V = 4, 5000
+    x = (10.0 + direction * 1e-7 * np.arange(V)).astype(np.float32)
+    logits = np.stack([x, x])
+    run_topb(b, logits, np.array([-1000.0, -1000.0], np.float32))
+
+
+def test_score_rounding_random_rows():
+    g = np.random.default_rng(3)
+    b, V = 8, 3 * 4096
+    logits = (5.0 + g.normal(0, 1e-4, (6, V))).astype(np.float32)
+    run_topb(b, logits, np.array([-2000.0] * 5 + [-2000.001], np.float32))
+
+
+def test_widest_beam_large_vocab():
+    g = np.random.default_rng(4)
+    b, V = 64, 32000
+    logits = g.normal(0, 3, (b, V)).astype(np.float32)
+    scores = -np.sort(g.uniform(0, 1, b)).astype(np.float32)
+    run_topb(b, logits, scores)
+
+
+def test_single_live_beam():
+    g = np.random.default_rng(5)
+    b, V = 16, 128256
+    run_topb(b, g.normal(0, 3, (1, V)).astype(np.float32), np.array([-3.25], np.float32))
