@@ -122,8 +122,9 @@ td_status td_init_prompt(td_ctx* ctx, const int32_t* h_prompt_len, const int32_t
  * and query head h:  out = softmax(scale * q . K_P^T) V_P  over the nodes P on leaf i's
  * root-to-leaf path (Alg 3 mask) with D - depth < W when a window is set; query head h
  * reads KV head h / (Hq/Hkv).  When the leaves' K/V are pending (after an append), the
- * call first stores k_new/v_new into the leaves' pool rows and the leaves attend to
- * them; otherwise d_k_new/d_v_new must be NULL.  fp32 accumulation; out rows of beams
+ * call first copies the rows the append's compaction moved (layers not done yet), then
+ * stores k_new/v_new into the leaves' pool rows, and the leaves attend to them;
+ * otherwise d_k_new/d_v_new must be NULL.  fp32 accumulation; out rows of beams
  * >= n_live are zeroed.  scale is normally 1/sqrt(d). */
 td_status trie_attn_decode(td_ctx* ctx, int32_t layer_begin, int32_t n_layers, const void* d_q,
                            const void* d_k_new, const void* d_v_new, void* d_out, float scale,
@@ -158,9 +159,11 @@ td_status beam_logsoftmax_topk(td_ctx* ctx, const float* d_logits, int32_t* d_se
  * score sel_score[j], depth D+1 and id next_id+j; every stored node's mask is remapped
  * (new bit j = old bit sel_parent[j]).  A node dies when its new mask is 0 (no live leaf
  * reaches it) or, with a window, when depth <= D+1-W.  Survivors are compacted stably
- * (parent slots remapped, -1 if the parent died) and the K/V rows of moved survivors are
- * copied to their new slots in every layer and KV head.  The new leaves become the last
- * b slots in rank j order; their K/V rows are pending until the next trie_attn_decode.
+ * (parent slots remapped, -1 if the parent died).  The K/V rows of moved survivors are
+ * copied to their new slots by the next trie_attn_decode call of each layer, before it
+ * reads them (until then the pools hold those rows at their old slots; td_init_prompt and
+ * td_load_state drop copies still due).  The new leaves become the last b slots in rank
+ * j order; their K/V rows are pending until the next trie_attn_decode.
  * Inputs [T][b] device.  Invalid selections / capacity overflow: sticky device status,
  * trie unchanged. */
 td_status trie_append_prune(td_ctx* ctx, const int32_t* d_sel_parent, const int32_t* d_sel_token,

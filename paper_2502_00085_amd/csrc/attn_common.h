@@ -38,6 +38,38 @@ __device__ inline size_t pool_row(const DevState& s, int t, int l, int g, int p)
   return ((((size_t)t * s.L + l) * s.Hkv + g) * s.cap + p) * s.D;
 }
 
+// Copies the K and V rows of the survivors moved by the last compaction (s.moves of trie
+// t: physical (source, destination), ascending source, every destination below its
+// source) inside the pools of (trie t, absolute layer l, KV head g), by the whole block,
+// in batches staged in LDS (stage: room for stage_chunks 16-byte chunks): every read of a
+// batch completes (barrier) before its writes, and a later batch reads only slots above
+// every slot an earlier batch wrote.  Ends with a barrier when there is anything to move.
+// Call from uniform control flow.
+template <typename T>
+__device__ inline void move_rows_block(const DevState& s, int t, int l, int g, uint4* stage, int stage_chunks) {
+  const int nm = s.n_moves[t];
+  if (nm == 0) return;
+  const int cpr = s.D * (int)sizeof(T) / 16;  // 16-byte chunks per row
+  const int per_row = 2 * cpr;                // K and V
+  const int rows_per_batch = stage_chunks / per_row;
+  uint4* kp = reinterpret_cast<uint4*>(static_cast<T*>(s.k_pool) + pool_row(s, t, l, g, 0));
+  uint4* vp = reinterpret_cast<uint4*>(static_cast<T*>(s.v_pool) + pool_row(s, t, l, g, 0));
+  const int2* mv = s.moves + (size_t)t * s.cap;
+  for (int i0 = 0; i0 < nm; i0 += rows_per_batch) {
+    const int n = min(rows_per_batch, nm - i0) * per_row;
+    for (int idx = threadIdx.x; idx < n; idx += blockDim.x) {
+      const int row = idx / per_row, ch = idx % per_row;
+      stage[idx] = (ch < cpr ? kp : vp)[(size_t)mv[i0 + row].x * cpr + ch % cpr];
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < n; idx += blockDim.x) {
+      const int row = idx / per_row, ch = idx % per_row;
+      (ch < cpr ? kp : vp)[(size_t)mv[i0 + row].y * cpr + ch % cpr] = stage[idx];
+    }
+    __syncthreads();
+  }
+}
+
 // Stores the pending leaves' K/V rows of one (trie, layer, KV head) into the pools
 // (16-byte chunks, whole block).
 template <typename T>

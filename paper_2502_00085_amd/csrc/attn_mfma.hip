@@ -80,6 +80,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   const int lo = window_lo(s, u.t, base, N, Dq);
   const int per = (N - lo + a.splits - 1) / a.splits;
   const int n0 = lo + u.split * per, n1 = min(N, n0 + per);
+  // rows moved by the last compaction (this WG is the only one of its layer and head);
+  // before the leaf store, whose slots may be sources of moves
+  if (a.moves) move_rows_block<__bf16>(s, u.t, lab, u.g, reinterpret_cast<uint4*>(lds), C::LDS / 16);
   // pending leaf rows: a WG whose node range holds them stores them into the pool first
   // (identical data if several WGs do), so the main loop only reads the pool
   if (a.kv_pending && n0 < n1 && n1 > N - n_live) {

@@ -48,6 +48,10 @@ __global__ __launch_bounds__(kValuThreads) void k_attn_valu(DevState s, AttnArgs
   const int N = h.n_nodes, base = h.base, n_live = h.n_live, Dq = h.leaf_depth;
   const int G = s.Hq / s.Hkv;
   const int lab = a.layer_begin + u.li;
+  // rows moved by the last compaction (this WG is the only one of its layer and head),
+  // before the leaf store, whose slots may be sources of moves
+  __shared__ uint4 stage[1024];
+  if (a.moves) move_rows_block<T>(s, u.t, lab, u.g, stage, 1024);
   if (a.kv_pending && u.split == 0 && u.rb == 0) store_leaf_kv<T>(s, a, u, base, N, n_live);
 
   const int lo = window_lo(s, u.t, base, N, Dq);

@@ -5,6 +5,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "td_internal.h"
@@ -16,6 +17,8 @@ struct td_ctx {
   std::vector<uint8_t> inited;         // per trie: initialised by init_prompt / load_state
   bool pending = false;                // leaves' K/V rows not yet stored in the pools
   std::vector<uint8_t> layer_written;  // per layer, while pending
+  bool moves_pending = false;          // rows moved by the last compaction not yet copied
+                                       //   (for the layers not yet written)
   int32_t* d_plen = nullptr;
   int splits_override = 0;             // TD_ATTN_SPLITS (tuning): WGs per attention unit
   hipEvent_t attn_ev0 = nullptr;       // td_set_attn_events: kernel-timestamp events of the
@@ -181,7 +184,7 @@ td_status td_init_prompt(td_ctx* c, const int32_t* h_plen, const int32_t* d_toke
   if (e == hipSuccess) e = td::launch_init_prompt(c->dev, c->d_plen, d_tokens, stride, st);
   if (e != hipSuccess) return hip_fail(c, e, "td_init_prompt");
   c->inited.assign(c->dev.T, 1);
-  c->pending = false;
+  c->pending = c->moves_pending = false;
   c->layer_written.assign(c->dev.L, 0);
   return TD_OK;
 }
@@ -218,17 +221,41 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   a.splits = c->splits_override > 0 ? c->splits_override : td::attn_choose_splits(s, n_layers, a.row_blocks);
   const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;
+  // Rows moved by the last compaction are copied before the layer's first attention: by
+  // the attention WGs themselves when each owns a whole (layer, KV head) and every layer
+  // of the call is still due, else by a copy launch per due layer range.
+  a.moves = 0;
+  std::vector<std::pair<int, int>> due;
+  if (c->pending && c->moves_pending) {
+    for (int l = layer_begin; l < layer_begin + n_layers;) {
+      if (c->layer_written[l]) {
+        ++l;
+        continue;
+      }
+      int j = l;
+      while (j < layer_begin + n_layers && !c->layer_written[j]) ++j;
+      due.emplace_back(l, j - l);
+      l = j;
+    }
+    if (due.size() == 1 && due[0].second == n_layers && a.splits == 1 && a.row_blocks == 1) {
+      a.moves = 1;
+      due.clear();
+    }
+  }
   hipEvent_t ev0 = c->attn_ev0, ev1 = c->attn_ev1;
   c->attn_ev0 = c->attn_ev1 = nullptr;
   hipEvent_t main_ev1 = a.splits > 1 ? nullptr : ev1;
-  hipError_t e = mfma ? td::launch_attn_mfma(s, a, st, ev0, main_ev1) : td::launch_attn_valu(s, a, st, ev0, main_ev1);
+  hipError_t e = hipSuccess;
+  for (const auto& d : due)
+    if (e == hipSuccess) e = td::launch_move_rows(s, d.first, d.second, st);
+  if (e == hipSuccess) e = mfma ? td::launch_attn_mfma(s, a, st, ev0, main_ev1) : td::launch_attn_valu(s, a, st, ev0, main_ev1);
   if (e == hipSuccess && a.splits > 1) e = td::launch_attn_combine(s, a, rpb, st, nullptr, ev1);
   if (e != hipSuccess) return hip_fail(c, e, "trie_attn_decode launch");
   if (c->pending) {
     for (int l = layer_begin; l < layer_begin + n_layers; ++l) c->layer_written[l] = 1;
     bool all = true;
     for (int l = 0; l < s.L; ++l) all = all && c->layer_written[l];
-    if (all) c->pending = false;
+    if (all) c->pending = c->moves_pending = false;
   }
   return TD_OK;
 }
@@ -271,6 +298,7 @@ td_status trie_append_prune(td_ctx* c, const int32_t* d_sel_parent, const int32_
   hipError_t e = td::launch_append_prune(c->dev, d_sel_parent, d_sel_token, d_sel_score, st);
   if (e != hipSuccess) return hip_fail(c, e, "trie_append_prune launch");
   c->pending = true;
+  c->moves_pending = true;
   c->layer_written.assign(c->dev.L, 0);
   return TD_OK;
 }
@@ -371,6 +399,7 @@ td_status td_load_state(td_ctx* c, int32_t trie, const td_state* in) {
   if (e != hipSuccess) return hip_fail(c, e, "td_load_state");
   c->inited[trie] = 1;
   c->pending = in->kv_pending != 0;
+  c->moves_pending = false;
   c->layer_written.assign(s.L, 0);
   return TD_OK;
 }
@@ -385,7 +414,7 @@ td_status td_get_status(td_ctx* c) {
   if (v[1] && c->dev.T == 1) {
     // a rejected append left the trie as it was: the leaves' K/V are stored, not pending
     // (with several tries the others advanced; such a context needs td_load_state)
-    c->pending = false;
+    c->pending = c->moves_pending = false;
     c->layer_written.assign(c->dev.L, 0);
   }
   return static_cast<td_status>(v[0]);

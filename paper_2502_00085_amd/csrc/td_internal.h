@@ -60,6 +60,8 @@ struct AttnArgs {
   int layer_begin, n_layers;
   float scale_log2;      // scale * log2(e)
   int kv_pending;
+  int moves;             // 1: first copy the rows moved by the last compaction (one WG per
+                         //    trie, layer and KV head: splits == row_blocks == 1)
   int splits;            // WGs per (trie, layer, kv head, row block) along the node axis
   int row_blocks;        // ceil(b * G / rows_per_block)
 };
@@ -84,6 +86,8 @@ hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_
 int topb_max_chunk_lists();  // limit of b * lse_chunks per trie
 hipError_t launch_append_prune(const DevState& s, const int32_t* sel_parent,
                                const int32_t* sel_token, const float* sel_score, hipStream_t st);
+// Copies the K/V rows moved by the last compaction for layers [layer_begin, +n_layers).
+hipError_t launch_move_rows(const DevState& s, int layer_begin, int n_layers, hipStream_t st);
 
 // ---------------------------------------------------------------------------------------
 // small device helpers

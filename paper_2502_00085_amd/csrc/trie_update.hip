@@ -319,10 +319,11 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
 constexpr int kMoveThreads = 256;
 constexpr int kMoveLdsBytes = 64 * 1024;
 
-__global__ __launch_bounds__(kMoveThreads) void k_move_rows(DevState s) {
+__global__ __launch_bounds__(kMoveThreads) void k_move_rows(DevState s, int layer_begin, int n_layers) {
   const int which = blockIdx.x & 1;
-  const int pair = blockIdx.x >> 1;           // (t * L + l) * Hkv + g
-  const int t = pair / (s.L * s.Hkv);
+  const int x = blockIdx.x >> 1;              // (t * n_layers + li) * Hkv + g
+  const int g = x % s.Hkv, li = (x / s.Hkv) % n_layers, t = x / (s.Hkv * n_layers);
+  const int pair = (t * s.L + layer_begin + li) * s.Hkv + g;
   const int nm = s.n_moves[t];
   if (nm == 0) return;
   extern __shared__ uint4 stage[];
@@ -359,10 +360,12 @@ hipError_t launch_append_prune(const DevState& s, const int32_t* sel_parent,
                                const int32_t* sel_token, const float* sel_score, hipStream_t st) {
   hipLaunchKernelGGL(k_append_prune, dim3(s.T), dim3(kAppThreads), 0, st, s, sel_parent, sel_token,
                      sel_score);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_move_rows, dim3(s.T * s.L * s.Hkv * 2), dim3(kMoveThreads), kMoveLdsBytes, st,
-                     s);
+  return hipGetLastError();
+}
+
+hipError_t launch_move_rows(const DevState& s, int layer_begin, int n_layers, hipStream_t st) {
+  hipLaunchKernelGGL(k_move_rows, dim3(s.T * n_layers * s.Hkv * 2), dim3(kMoveThreads), kMoveLdsBytes, st,
+                     s, layer_begin, n_layers);
   return hipGetLastError();
 }
 
