@@ -50,7 +50,7 @@ struct MfmaCfg {
   static constexpr int TILE_BYTES = 32 * D * 2;
   static constexpr int OS = D + 4;            // LDS row stride of the O merge buffer (floats)
   static constexpr int V_LDS = NW * 2 * TILE_BYTES;  // one K and one V tile per wave
-  static constexpr int O_LDS = kRows * OS * 4 + 2 * NW * kRows * 4 + 2 * kRows * 4;
+  static constexpr int O_LDS = NW * kRows * OS * 4 + 3 * NW * kRows * 4 + 2 * kRows * 4;
   static constexpr int LDS = V_LDS > O_LDS ? V_LDS : O_LDS;
 };
 
@@ -81,38 +81,21 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   const int per = (N - lo + a.splits - 1) / a.splits;
   const int n0 = lo + u.split * per, n1 = min(N, n0 + per);
   // rows moved by the last compaction (this WG is the only one of its layer and head);
-  // before the leaf store, whose slots may be sources of moves
+  // before the leaf store at the end, whose slots may be sources of moves
   if (a.moves) move_rows_block<__bf16>(s, u.t, lab, u.g, reinterpret_cast<uint4*>(lds), C::LDS / 16);
-  // pending leaf rows: a WG whose node range holds them stores them into the pool first
-  // (identical data if several WGs do), so the main loop only reads the pool
-  if (a.kv_pending && n0 < n1 && n1 > N - n_live) {
-    store_leaf_kv<__bf16>(s, a, u, base, N, n_live);
-    __syncthreads();
-  }
+  // pending leaf rows are read from k_new / v_new by the main loop and stored into the
+  // pool after it (by every WG whose node range holds them: identical data)
+  const int leaf0 = a.kv_pending ? N - n_live : N;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
   const int col = lane & 31, hh = lane >> 5;
 
-  // this lane's query row (B operand of S^T): half hh of the row's d range
-  const int r = u.rb * kRows + col;
-  const int beam = r / G;
-  const bool row_ok = r < s.b * G && beam < n_live;
-  const int beam_bit = beam < 64 ? beam : 63;
-  bf16x8 qv[C::KSTEPS];
-  {
-    const uint4* qp = reinterpret_cast<const uint4*>(
-        static_cast<const __bf16*>(a.q) +
-        ((((size_t)u.li * s.T + u.t) * s.b + (row_ok ? beam : 0)) * s.Hq + u.g * G + r % G) * D +
-        hh * (D / 2));
-#pragma unroll
-    for (int t = 0; t < C::KSTEPS; ++t) {
-      const uint4 x = row_ok ? qp[t] : make_uint4(0, 0, 0, 0);
-      qv[t] = __builtin_bit_cast(bf16x8, x);
-    }
-  }
-
   const __bf16* kpool = static_cast<const __bf16*>(s.k_pool) + pool_row(s, u.t, lab, u.g, base);
   const __bf16* vpool = static_cast<const __bf16*>(s.v_pool) + pool_row(s, u.t, lab, u.g, base);
+  const size_t leaf_off = (((size_t)u.li * s.T + u.t) * s.b * s.Hkv + u.g) * D;  // leaf 0 of k_new
+  const __bf16* knew = static_cast<const __bf16*>(a.k_new) + leaf_off;
+  const __bf16* vnew = static_cast<const __bf16*>(a.v_new) + leaf_off;
+  const int leaf_stride = s.Hkv * D;
   const uint64_t* maskp = s.mask + (size_t)u.t * s.cap + base;
   unsigned char* kbuf = lds + wave * 2 * C::TILE_BYTES;
   unsigned char* vbuf = kbuf + C::TILE_BYTES;
@@ -151,24 +134,47 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
 #pragma unroll
   for (int t = 0; t < C::KSTEPS; ++t) kread[t] = col * (2 * D) + (hh * (C::CPR / 2) + t + col) % C::CPR * 16;
 
-  // K and V rows of a tile -> the wave's LDS buffers (coalesced 16-byte direct loads); in
-  // the range's last, partial tile, rows past the end are clamped to its last node and
-  // masked out later
+  // K and V rows of a tile -> the wave's LDS buffers (coalesced 16-byte direct loads; the
+  // pending leaves' rows come from k_new / v_new); in the range's last, partial tile, rows
+  // past the end are clamped to its last node and masked out later
   auto issue = [&](int tile) {
     const int tb = n0 + tile * 32;
     const bool full = tb + 32 <= n1;
 #pragma unroll
     for (int i = 0; i < C::VINST; ++i) {
       const int nv = full ? tb + vrow[i] : min(tb + vrow[i], n1 - 1);
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(kpool + (size_t)nv * D + koff[i]),
+      const bool leaf = nv >= leaf0;
+      const size_t kr = leaf ? (size_t)(nv - leaf0) * leaf_stride : (size_t)nv * D;
+      const __bf16* ks = (leaf ? knew : kpool) + kr + koff[i];
+      const __bf16* vs = (leaf ? vnew : vpool) + kr + voff[i];
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)ks,
                                        (__attribute__((address_space(3))) void*)(kbuf + i * 1024), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(vpool + (size_t)nv * D + voff[i]),
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)vs,
                                        (__attribute__((address_space(3))) void*)(vbuf + i * 1024), 16, 0, 0);
     }
   };
 
   const float scale = a.scale_log2;
   if (my_tiles > 0) issue(wave);
+  // (the query rows load while the first tile is in flight)
+  // this lane's query row (B operand of S^T): half hh of the row's d range
+  const int r = u.rb * kRows + col;
+  const int beam = r / G;
+  const bool row_ok = r < s.b * G && beam < n_live;
+  const int beam_bit = beam < 64 ? beam : 63;
+  bf16x8 qv[C::KSTEPS];
+  {
+    const uint4* qp = reinterpret_cast<const uint4*>(
+        static_cast<const __bf16*>(a.q) +
+        ((((size_t)u.li * s.T + u.t) * s.b + (row_ok ? beam : 0)) * s.Hq + u.g * G + r % G) * D +
+        hh * (D / 2));
+#pragma unroll
+    for (int t = 0; t < C::KSTEPS; ++t) {
+      const uint4 x = row_ok ? qp[t] : make_uint4(0, 0, 0, 0);
+      qv[t] = __builtin_bit_cast(bf16x8, x);
+    }
+  }
+
   for (int k = 0; k < my_tiles; ++k) {
     const int tile = wave + NW * k;
     const int tb = n0 + tile * 32;
@@ -257,64 +263,75 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[uu][dt], pb[uu], o[dt], 0, 0, 0);
   }
 
-  // ---- merge the waves of this WG (fixed order) ----
+  // ---- merge the waves of this WG: every wave stores its state, one combine ----
   lsum += __shfl_xor(lsum, 32);
-  __syncthreads();  // V staging is reused below
-  float* obuf = reinterpret_cast<float*>(lds);
-  float* smx = obuf + kRows * C::OS;
-  float* ssum = smx + NW * kRows;
+  __syncthreads();  // the tile buffers are reused below
+  float* obuf = reinterpret_cast<float*>(lds);  // [NW][kRows][OS] unscaled O of each wave
+  float* smx = obuf + NW * kRows * C::OS;        // [NW][kRows] running max
+  float* ssum = smx + NW * kRows;                // [NW][kRows] weight sum
+  float* fw = ssum + NW * kRows;                 // [NW][kRows] wave weight 2^(m_w - M)
+  float* rowm = fw + NW * kRows;                 // [kRows] M
+  float* rowl = rowm + kRows;                    // [kRows] sum of weights
   if (hh == 0) {
     smx[wave * kRows + col] = m;
     ssum[wave * kRows + col] = lsum;
   }
-  __syncthreads();
-  float M = smx[col];
-  for (int w = 1; w < NW; ++w) M = fmaxf(M, smx[w * kRows + col]);
-  const float f = __builtin_amdgcn_exp2f(m - M);
-  for (int w = 0; w < NW; ++w) {
-    if (wave == w) {
+  {
+    float* ow = obuf + (wave * kRows + col) * C::OS;
 #pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt)
+    for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int d = dt * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-          float* p = obuf + col * C::OS + d;
-          *p = (w == 0 ? 0.0f : *p) + o[dt][v] * f;
-        }
-    }
-    __syncthreads();
+      for (int v = 0; v < 16; ++v) ow[dt * 32 + 8 * (v >> 2) + 4 * hh + (v & 3)] = o[dt][v];
   }
-
-  // per-row max and sum over the waves, once per row
-  float* rowm = ssum + NW * kRows;
-  float* rowl = rowm + kRows;
+  __syncthreads();
   if (threadIdx.x < kRows) {
     const int i = threadIdx.x;
-    float Mi = smx[i], L = 0.0f;
+    float Mi = smx[i];
     for (int w = 1; w < NW; ++w) Mi = fmaxf(Mi, smx[w * kRows + i]);
-    for (int w = 0; w < NW; ++w) L += ssum[w * kRows + i] * __builtin_amdgcn_exp2f(smx[w * kRows + i] - Mi);
+    float L = 0.0f;
+    for (int w = 0; w < NW; ++w) {
+      const float f = __builtin_amdgcn_exp2f(smx[w * kRows + i] - Mi);
+      fw[w * kRows + i] = f;
+      L += ssum[w * kRows + i] * f;  // fixed wave order
+    }
     rowm[i] = Mi;
     rowl[i] = L;
   }
   __syncthreads();
 
+  // 8 consecutive output elements per thread: 16-byte LDS reads, one 16-byte store
   __bf16* outp = static_cast<__bf16*>(a.out);
   const int unit = blockIdx.x / a.splits;
   float* part = s.attn_part + (size_t)unit * a.splits * kRows * (D + 2);
-  for (int idx = threadIdx.x; idx < kRows * D; idx += NW * 64) {
-    const int i = idx / D, c = idx % D;
+  for (int idx = threadIdx.x; idx < kRows * (D / 8); idx += NW * 64) {
+    const int i = idx / (D / 8), c = idx % (D / 8) * 8;
+    float O[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) O[e] = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float f = fw[w * kRows + i];
+      const float4* src = reinterpret_cast<const float4*>(obuf + (w * kRows + i) * C::OS + c);
+      const float4 x0 = src[0], x1 = src[1];
+      O[0] += x0.x * f; O[1] += x0.y * f; O[2] += x0.z * f; O[3] += x0.w * f;
+      O[4] += x1.x * f; O[5] += x1.y * f; O[6] += x1.z * f; O[7] += x1.w * f;
+    }
     const float Mi = rowm[i], L = rowl[i];
-    const float O = obuf[i * C::OS + c];
     if (a.splits == 1) {
       const int rr = u.rb * kRows + i;
       if (rr < s.b * G) {
         const int bm = rr / G;
-        const float val = (bm < n_live && L > 0.0f) ? O / L : 0.0f;
-        outp[((((size_t)u.li * s.T + u.t) * s.b + bm) * s.Hq + u.g * G + rr % G) * D + c] = (__bf16)val;
+        const bool live = bm < n_live && L > 0.0f;
+        const float inv = live ? 1.0f / L : 0.0f;
+        bf16x8 y;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = (__bf16)(O[e] * inv);
+        *reinterpret_cast<bf16x8*>(outp + ((((size_t)u.li * s.T + u.t) * s.b + bm) * s.Hq + u.g * G + rr % G) * D + c) = y;
       }
     } else {
       float* pp = part + ((size_t)u.split * kRows + i) * (D + 2);
-      pp[c] = O;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pp[c + e] = O[e];
       if (c == 0) {
         pp[D] = Mi;
         pp[D + 1] = L;
@@ -322,6 +339,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     }
   }
 
+  // the pending leaves' rows into the pool, for later calls (this call read them from
+  // k_new / v_new)
+  if (a.kv_pending && n0 < n1 && n1 > N - n_live) store_leaf_kv<__bf16>(s, a, u, base, N, n_live);
 }
 
 constexpr int kNW = 8;
