@@ -51,7 +51,8 @@ struct MfmaCfg {
   static constexpr int OS = D + 4;            // LDS row stride of the O merge buffer (floats)
   static constexpr int V_LDS = NW * 2 * TILE_BYTES;  // one K and one V tile per wave
   static constexpr int O_LDS = NW * kRows * OS * 4 + 3 * NW * kRows * 4 + 2 * kRows * 4;
-  static constexpr int LDS = V_LDS > O_LDS ? V_LDS : O_LDS;
+  static constexpr int MOVE_LDS = 8192;    // staging of compaction moves, past the tiles
+  static constexpr int LDS = V_LDS + MOVE_LDS > O_LDS ? V_LDS + MOVE_LDS : O_LDS;
 };
 
 // Physical 16-byte chunk of logical chunk c of tile row r: rows are rotated by whole
@@ -80,14 +81,18 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   const int lo = window_lo(s, u.t, base, N, Dq);
   const int per = (N - lo + a.splits - 1) / a.splits;
   const int n0 = lo + u.split * per, n1 = min(N, n0 + per);
-  // rows moved by the last compaction (this WG is the only one of its layer and head);
-  // before the leaf store at the end, whose slots may be sources of moves
-  if (a.moves) move_rows_block<__bf16>(s, u.t, lab, u.g, reinterpret_cast<uint4*>(lds), C::LDS / 16);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
+  // Rows moved by the last compaction (this WG is the only one of its layer and head) are
+  // copied by the whole block right after the first tile's loads are issued, so their
+  // round trips overlap that tile's (see the main loop).  A first tile that itself
+  // reaches a moved slot is issued after the copy instead.  The leaf store at the end,
+  // whose slots may be sources of moves, follows the merge's block barriers.
+  const int nmoves = a.moves ? s.n_moves[u.t] : 0;
+  const int first_moved = nmoves > 0 ? s.moves[(size_t)u.t * s.cap].y - base : INT_MAX;
   // pending leaf rows are read from k_new / v_new by the main loop and stored into the
   // pool after it (by every WG whose node range holds them: identical data)
   const int leaf0 = a.kv_pending ? N - n_live : N;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
   const int col = lane & 31, hh = lane >> 5;
 
   const __bf16* kpool = static_cast<const __bf16*>(s.k_pool) + pool_row(s, u.t, lab, u.g, base);
@@ -155,7 +160,14 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   };
 
   const float scale = a.scale_log2;
-  if (my_tiles > 0) issue(wave);
+  // first tile of every wave, unless it reaches a moved slot (then after the copy)
+  const bool early = my_tiles > 0 && min(n0 + wave * 32 + 32, n1) <= first_moved;
+  if (early) issue(wave);
+  if (nmoves > 0) {
+    // staged past the tile buffers (the first tiles are landing in them)
+    move_rows_block<__bf16>(s, u.t, lab, u.g, reinterpret_cast<uint4*>(lds + C::V_LDS), C::MOVE_LDS / 16);
+  }
+  if (my_tiles > 0 && !early) issue(wave);
   // (the query rows load while the first tile is in flight)
   // this lane's query row (B operand of S^T): half hh of the row's d range
   const int r = u.rb * kRows + col;
