@@ -67,7 +67,7 @@ __device__ inline int block_rank(bool flag, int* wave_cnt, int* total) {
 
 __device__ inline uint64_t remap_mask(uint64_t m, const int* sp, int b) {
   uint64_t r = 0;
-  for (int j = 0; j < b; ++j) r |= ((m >> sp[j]) & 1ull) << j;
+  for (int j = 0; j < b; ++j) r |= ((m >> (sp[j] & 63)) & 1ull) << j;  // (ranks are checked)
   return r;
 }
 
@@ -82,37 +82,19 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
   __shared__ float ssc[kMaxBeam];
   __shared__ int err, wave_cnt[kAppWaves], wave_cnt2[kAppWaves];
   __shared__ int full_cnt;
+  __shared__ int wa[kAppWaves], wf[kAppWaves], wd[kAppWaves];
+  __shared__ int lpos[kAppThreads];
 
+  // the header and the selection go out together
   const TrieHdr h = s.hdr[t];
-  const int N = h.n_nodes, base = h.base, n_live = h.n_live;
-  if (tid == 0) {
-    err = 0;
-    full_cnt = 0;
-  }
-  __syncthreads();
+  int p = 0, v = 0;
+  float sc = 0.0f;
   if (tid < b) {
-    const int p = sel_parent[(size_t)t * b + tid];
-    const int v = sel_token[(size_t)t * b + tid];
-    sp[tid] = p;
-    stok[tid] = v;
-    ssc[tid] = sel_score[(size_t)t * b + tid];
-    if (p < 0 || p >= n_live || v < 0 || v >= s.V) atomicOr(&err, 1);
+    p = sel_parent[(size_t)t * b + tid];
+    v = sel_token[(size_t)t * b + tid];
+    sc = sel_score[(size_t)t * b + tid];
   }
-  __syncthreads();
-  for (int idx = tid; idx < b * b; idx += kAppThreads) {
-    const int i = idx / b, j = idx % b;
-    if (i < j && sp[i] == sp[j] && stok[i] == stok[j]) atomicOr(&err, 1);
-  }
-  __syncthreads();
-  if (err) {
-    if (tid == 0) {
-      set_status(s.status, kDevEinval);
-      s.status[1] = 1;
-      s.n_moves[t] = 0;
-    }
-    return;
-  }
-
+  const int N = h.n_nodes, base = h.base, n_live = h.n_live;
   const int d_new = h.leaf_depth + 1;
   // window eviction: the leading run of slots with depth <= d_new - W (depth is sorted)
   const int e = s.W > 0 ? block_first_above(s.depth + off + base, N, d_new - s.W, wave_cnt) : 0;
@@ -121,9 +103,8 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
   const uint64_t full_b = (b == 64) ? ~0ull : ((1ull << b) - 1ull);
 
   if (N - r0 <= kAppThreads) {
-    // common case: the slots after the shared prefix fit one pass of the block; every
-    // field is loaded up front and new positions stay in LDS
-    __shared__ int lpos[kAppThreads];
+    // common case: the slots after the shared prefix fit one pass of the block.  Their
+    // fields load while the selection is checked; new positions stay in LDS.
     const int n = r0 + tid;
     const bool in = n < N;
     uint64_t m = 0;
@@ -135,13 +116,49 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
       dp = s.depth[off + base + n];
       pp = s.parent[off + base + n];
     }
+    if (tid == 0) err = 0;
+    if (tid < b) {
+      sp[tid] = p;
+      stok[tid] = v;
+      ssc[tid] = sc;
+    }
+    __syncthreads();
+    // invalid selections: a parent rank outside the live leaves, a token outside the
+    // vocabulary, the same (parent, token) twice
+    bool bad = tid < b && (p < 0 || p >= n_live || v < 0 || v >= s.V);
+    for (int idx = tid; idx < b * b; idx += kAppThreads) {
+      const int i = idx / b, j = idx % b;
+      bad |= i < j && sp[i] == sp[j] && stok[i] == stok[j];
+    }
+    if (bad) atomicOr(&err, 1);
+    // survivors (new mask != 0), the all-beam ones, and the first dead slot: one exchange
     const uint64_t nm = in ? remap_mask(m, sp, b) : 0ull;
     const bool alive = in && nm != 0ull;
-    int n_alive;
-    const int rank = block_rank(alive, wave_cnt, &n_alive);
-    const int n_full = block_count(alive && nm == full_b, wave_cnt2);
+    const int lane = tid & 63, wave = tid >> 6;
+    const uint64_t ba = __ballot(alive), bd = __ballot(in && !alive);
+    const uint64_t bf = __ballot(alive && nm == full_b);
+    if (lane == 0) {
+      wa[wave] = __popcll(ba);
+      wf[wave] = __popcll(bf);
+      wd[wave] = bd ? wave * 64 + __ffsll((unsigned long long)bd) - 1 : kAppThreads;
+    }
+    __syncthreads();
+    int rank = __popcll(ba & ((1ull << lane) - 1ull)), n_alive = 0, n_full = 0, first_dead = kAppThreads;
+    for (int w = 0; w < kAppWaves; ++w) {
+      rank += w < wave ? wa[w] : 0;
+      n_alive += wa[w];
+      n_full += wf[w];
+      first_dead = min(first_dead, wd[w]);
+    }
+    if (err) {
+      if (tid == 0) {
+        set_status(s.status, kDevEinval);
+        s.status[1] = 1;
+        s.n_moves[t] = 0;
+      }
+      return;
+    }
     const int np = alive ? (r0 - e) + rank : -1;
-    lpos[tid] = np;
     const int n_new = (r0 - e) + n_alive + b;
     if (base_new + n_new > s.cap) {
       if (tid == 0) {
@@ -151,6 +168,7 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
       }
       return;
     }
+    lpos[tid] = np;
     __syncthreads();
     auto new_phys = [&](int lp) -> int {  // new physical slot of old logical slot lp < N
       if (lp < e) return -1;
@@ -163,9 +181,12 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
       const int lp = pp - base;
       par = (lp >= 0 && lp < n) ? new_phys(lp) : -1;
     }
-    const bool moved = alive && (np + e != n);
-    int n_moved;
-    const int mrank = block_rank(moved, wave_cnt2, &n_moved);
+    // a survivor's physical slot changes (base + r0 + tid -> base_new + np = base + r0 +
+    // rank) iff a slot before it died; its rank among the moved ones is its survivor rank
+    // minus the survivors before the first dead slot (all the slots before it)
+    const bool moved = alive && tid > first_dead;
+    const int mrank = rank - first_dead;
+    const int n_moved = max(0, n_alive - first_dead);
     if (moved) s.moves[off + mrank] = make_int2(base + n, base_new + np);
     // all fields were read before the first barrier: rewrite in place
     if (alive) {
@@ -200,6 +221,33 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
       nh.pad0 = nh.pad1 = 0;
       s.hdr[t] = nh;
       s.n_moves[t] = n_moved;
+    }
+    return;
+  }
+
+  // general case (more than kAppThreads slots after the shared prefix)
+  if (tid == 0) {
+    err = 0;
+    full_cnt = 0;
+  }
+  __syncthreads();
+  if (tid < b) {
+    sp[tid] = p;
+    stok[tid] = v;
+    ssc[tid] = sc;
+    if (p < 0 || p >= n_live || v < 0 || v >= s.V) atomicOr(&err, 1);
+  }
+  __syncthreads();
+  for (int idx = tid; idx < b * b; idx += kAppThreads) {
+    const int i = idx / b, j = idx % b;
+    if (i < j && sp[i] == sp[j] && stok[i] == stok[j]) atomicOr(&err, 1);
+  }
+  __syncthreads();
+  if (err) {
+    if (tid == 0) {
+      set_status(s.status, kDevEinval);
+      s.status[1] = 1;
+      s.n_moves[t] = 0;
     }
     return;
   }
