@@ -134,6 +134,7 @@ td_status td_create(const td_desc* d, td_ctx** out) {
   s.k_pool = d->k_pool;
   s.v_pool = d->v_pool;
   s.lse_chunks = (s.V + td::kLseChunk - 1) / td::kLseChunk;
+  s.topk_half = (size_t)s.T * s.b * s.lse_chunks * 16;
   s.attn_pairs_max = 1024;
   s.attn_part_floats = s.attn_pairs_max * 32 * (s.D + 2);
   const size_t tc = (size_t)s.T * s.cap;
@@ -144,7 +145,7 @@ td_status td_create(const td_desc* d, td_ctx** out) {
       (e = alloc(c, &s.leaf_score, (size_t)s.T * s.b)) != hipSuccess ||
       (e = alloc(c, &s.status, 2)) != hipSuccess ||
       (e = alloc(c, &s.lse_part, (size_t)s.T * s.b * s.lse_chunks * 2)) != hipSuccess ||
-      (e = alloc(c, &s.topk_keys, (size_t)s.T * s.b * s.lse_chunks * 16)) != hipSuccess ||
+      (e = alloc(c, &s.topk_keys, 2 * (size_t)s.T * s.b * s.lse_chunks * 16)) != hipSuccess ||
       (e = alloc(c, &s.newpos, tc)) != hipSuccess || (e = alloc(c, &s.moves, tc)) != hipSuccess ||
       (e = alloc(c, &s.n_moves, (size_t)s.T)) != hipSuccess ||
       (e = alloc(c, &s.attn_part, (size_t)s.attn_part_floats)) != hipSuccess ||

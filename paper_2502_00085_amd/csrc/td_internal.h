@@ -36,7 +36,9 @@ struct DevState {
                          // was rejected (the trie kept its previous state)
   // workspace
   double* lse_part;      // [T][b][lse_chunks][2]  (chunk max, chunk sum of exp)
-  uint64_t* topk_keys;   // [T][b][lse_chunks][16]  largest logit (key) of each 256-logit sub-chunk
+  uint64_t* topk_keys;   // 2 x [T][b][lse_chunks][16]  largest / second largest logit key of
+                         //   each 256-logit sub-chunk (the second block at topk_half)
+  size_t topk_half;
   int32_t* newpos;       // [T][cap] new logical position of each old logical slot, -1 dead
   int2* moves;           // [T][cap] (src phys, dst phys) rows to move, ascending src
   int32_t* n_moves;      // [T]

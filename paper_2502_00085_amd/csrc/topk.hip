@@ -162,7 +162,8 @@ __device__ inline void rank_topb(const uint64_t* cand, const uint64_t* comp, int
   }
 }
 
-// One chunk of one row: max, fp64 sum of exp(x - max), largest logit key of each wave.
+// One chunk of one row: max, fp64 sum of exp(x - max), the two largest logit keys of each
+// wave (sub-chunk).
 __global__ __launch_bounds__(kChunkThreads) void k_topb_chunk(DevState s, const float* logits) {
   const int c = blockIdx.x, r = blockIdx.y, t = blockIdx.z;
   const int V = s.V, b = s.b;
@@ -181,21 +182,26 @@ __global__ __launch_bounds__(kChunkThreads) void k_topb_chunk(DevState s, const 
   }
   if (r >= s.hdr[t].n_live) return;
   float m = -INFINITY;
-  uint64_t km = 0;
+  uint64_t k1 = 0, k2 = 0;  // this lane's two largest keys
   const uint32_t flat0 = (uint32_t)r * (uint32_t)V + (uint32_t)v0 + threadIdx.x;
 #pragma unroll
   for (int i = 0; i < kChunkPer; ++i) {
     const int v = v0 + i * kChunkThreads + (int)threadIdx.x;
     m = fmaxf(m, x[i]);
     const uint64_t k = v < V ? x_key(x[i], flat0 + (uint32_t)(i * kChunkThreads)) : 0;
-    km = k > km ? k : km;
+    k2 = k > k1 ? k1 : (k > k2 ? k : k2);
+    k1 = k > k1 ? k : k1;
   }
   m = __ockl_wfred_max_f32(m);
-  km = wave_max_u64(km);
+  // the wave's largest key, and its second largest (the owner of the largest offers its
+  // own second; keys are unique)
+  const uint64_t km = wave_max_u64(k1);
+  const uint64_t km2 = wave_max_u64(k1 == km ? k2 : k1);
   const size_t list = ((size_t)t * b + r) * s.lse_chunks + c;
   if (lane == 0) {
     wm[wave] = m;
     s.topk_keys[list * kSub + wave] = km;  // 0 when the wave holds no logit
+    s.topk_keys[s.topk_half + list * kSub + wave] = km2;
   }
   __syncthreads();
   m = wm[0];
@@ -283,17 +289,22 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
 
   // Independent loads first: the sub-chunk maxima of every row (rows >= n_live are dropped
   // once n_live is known), pair logits, leaf scores, every row's lse, then n_live.
-  uint64_t km0[kSubPer];
+  const uint64_t* ssec = smax + s.topk_half;  // second largest keys, same layout
+  uint64_t km0[kSubPer], ks0[kSubPer];
 #pragma unroll
   for (int q = 0; q < kSubPer; ++q) {
     const int i = q * kFinalThreads + (int)threadIdx.x;
     km0[q] = i < b * per_row ? smax[i] : 0;
+    ks0[q] = i < b * per_row ? ssec[i] : 0;
   }
+  // pairs: the last b threads (their wave has no row below; the dependent logit load
+  // waits there)
+  const int pj = (int)threadIdx.x - (kFinalThreads - b);
   float pair_x = 0.0f;
   int pp = -1, pv = -1;
-  if (pair_parent != nullptr && (int)threadIdx.x < b) {
-    pp = pair_parent[(size_t)t * b + threadIdx.x];
-    pv = pair_token[(size_t)t * b + threadIdx.x];
+  if (pair_parent != nullptr && pj >= 0) {
+    pp = pair_parent[(size_t)t * b + pj];
+    pv = pair_token[(size_t)t * b + pj];
     if (pp >= 0 && pp < b && pv >= 0 && pv < V) pair_x = lrow[(size_t)pp * V + pv];
   }
   for (int r = threadIdx.x; r < b; r += kFinalThreads) row_score[r] = s.leaf_score[(size_t)t * b + r];
@@ -336,21 +347,30 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     L = 0;
     for (int w = 0; w < kFinalWaves; ++w) L = wt[w] > L ? wt[w] : L;
   }
-  // hot sub-chunks: largest score >= L (at least b of them)
+  // hot sub-chunks: largest score >= L (at least b of them).  A hot sub-chunk whose second
+  // largest logit also scores >= L is read again in full (its logits scoring >= L are the
+  // candidates); otherwise its largest logit is its only candidate.
   for (int i0 = 0; i0 < nsub; i0 += kSubPer * kFinalThreads) {
     int id[kSubPer];
-    bool take[kSubPer];
+    bool take[kSubPer], direct[kSubPer];
+    uint64_t ks[kSubPer], kx[kSubPer];
 #pragma unroll
     for (int q = 0; q < kSubPer; ++q) {
       const int i = i0 + q * kFinalThreads + (int)threadIdx.x;
-      // (o[] holds the last round of the bound loop: recompute from the keys)
       const uint64_t km = i >= nsub ? 0 : i0 == 0 ? km0[q] : smax[i];
+      const uint64_t k2 = i >= nsub ? 0 : i0 == 0 ? ks0[q] : ssec[i];
       const int r = div_small(i, inv_per_row);
-      const uint32_t oq = km != 0 ? ord_score(score_only(key_x(km), row_lse[r], row_score[r])) : 0u;
+      const float sc = km != 0 ? score_only(key_x(km), row_lse[r], row_score[r]) : 0.0f;
+      const bool hotq = i < nsub && km != 0 && ord_score(sc) >= L;
+      const bool again = hotq && k2 != 0 && ord_score(score_only(key_x(k2), row_lse[r], row_score[r])) >= L;
       id[q] = i;
-      take[q] = i < nsub && oq != 0 && oq >= L;
+      take[q] = again;
+      direct[q] = hotq && !again;
+      ks[q] = s_key(sc, key_flat(km));
+      kx[q] = km;
     }
     wave_append<kSubPer, int, int>(id, nullptr, take, hot, nullptr, kCandMax, &nhot);
+    wave_append<kSubPer, uint64_t, uint64_t>(ks, kx, direct, cand, cand_x, kCandMax, &ncand);
   }
   __syncthreads();
   const int n_hot = nhot;
@@ -441,10 +461,10 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     for (int r = threadIdx.x; r < b; r += kFinalThreads)
       lse_out[(size_t)t * b + r] = r < n_live ? row_lse[r] : 0.0f;
   }
-  if (pair_parent != nullptr && (int)threadIdx.x < b) {
+  if (pair_parent != nullptr && pj >= 0) {
     float sc = __uint_as_float(0x7fc00000u);  // NaN for an out-of-range pair
     if (pp >= 0 && pp < n_live && pv >= 0 && pv < V) sc = score_only(pair_x, row_lse[pp], row_score[pp]);
-    pair_score[(size_t)t * b + threadIdx.x] = sc;
+    pair_score[(size_t)t * b + pj] = sc;
   }
 }
 
