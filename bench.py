@@ -31,6 +31,28 @@ import synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
 
+# HBM traffic of the attention kernel measured by rocprofv3 (separate --pmc FETCH_SIZE and
+# --pmc WRITE_SIZE runs of `bench.py --profile-only --copy-ref-mib 512`, llama8b), scaled
+# by what the same counters read for a plain 512 MiB device copy (fetch x 2.0, write x 1.0),
+# as the mean bytes per launch over that run's launches.  Valid only for the kernel
+# sources it was measured on: reported as null once their digest differs.
+ATTN_TRAFFIC = {
+    "workload": "llama8b",
+    "sources_sha256": "25eef2fadad6839c893e2fc93df1544f35c1438271bc8505cc381405ee508e9a",
+    "bytes_per_launch": 286253422,             # 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE
+    "algorithmic_bytes_per_launch": 286847941,  # KV rows, q, new leaves, moved rows, out
+}
+ATTN_SOURCES = ("attn_mfma.hip", "attn_common.h", "td_internal.h")
+
+
+def attn_sources_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        with open(os.path.join(ROOT, "paper_2502_00085_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
 
 def parse():
     p = argparse.ArgumentParser()
@@ -306,6 +328,10 @@ def main():
     attn_s = r["attn_ms"] / 1e3
     graph_bytes = float(sum(r["attn_graph_nodes"])) * w.node_bytes
     achieved = graph_bytes / (r["attn_graph_ms"] / 1e3) / 1e9
+    traffic = None
+    if (ATTN_TRAFFIC["workload"] == w.name and ATTN_TRAFFIC["bytes_per_launch"] is not None
+            and ATTN_TRAFFIC["sources_sha256"] == attn_sources_digest()):
+        traffic = ATTN_TRAFFIC["bytes_per_launch"]
     out = {
         "metric": "trie-decode steps/s and achieved HBM GB/s (% of peak) at Llama-8B GQA shape, b=8",
         "value": round(K / r["seconds"], 2),
@@ -320,7 +346,7 @@ def main():
                    "vocab": w.vocab, "window": w.window, "growth": f"scripted, parent rank ~ "
                    f"(r+1)^-{w.alpha}", "launch": r["mode"]},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": "k_attn_mfma (trie_attn_decode, all layers, one launch)",
                      "attn_us_per_launch": round(r["attn_graph_ms"] * 1e3, 2),
                      "unique_kv_bytes_per_launch": int(graph_bytes),
