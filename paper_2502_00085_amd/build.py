@@ -39,9 +39,9 @@ def _flags():
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
     cmd = [hipcc(), *_flags(), "-c", src, "-o", obj]
-    if src.endswith(".cpp"):
-        cmd = [hipcc(), "-O3", "-std=c++17", "-fPIC", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-               "-Wall", "-c", src, "-o", obj]
+    if src.endswith(".cpp"):  # host code only: no device pass
+        cmd = [hipcc(), "-O3", "-std=c++17", "-fPIC", "--cuda-host-only", f"--offload-arch={ARCH}",
+               "-I", os.path.join(ROOT, "include"), "-I", CSRC, "-Wall", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

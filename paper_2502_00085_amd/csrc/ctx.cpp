@@ -162,8 +162,8 @@ td_status td_create(const td_desc* d, td_ctx** out) {
 
 td_status td_destroy(td_ctx* c) {
   if (!c) return TD_EINVAL;
-  hipDeviceSynchronize();
-  for (void* p : c->allocs) hipFree(p);
+  (void)hipDeviceSynchronize();
+  for (void* p : c->allocs) (void)hipFree(p);
   delete c;
   return TD_OK;
 }
