@@ -37,6 +37,7 @@ constexpr int kFinalWaves = kFinalThreads / 64;
 constexpr int kCandMax = 4096;
 constexpr int kSub = kChunkWaves;                     // sub-chunks (waves) per chunk
 constexpr int kSubPer = 4;                            // sub-chunk maxima per thread
+static_assert(kSub == kFinalThreads / 64, "the final merge maps sub-chunk w of a chunk to wave w");
 
 // Order-preserving maps of floats to unsigned integers: raw (-0 below +0) for logits, so
 // a key keeps the logit's exact bits; merged zeros for scores (equal scores tie).
@@ -290,10 +291,14 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
   // Independent loads first: the sub-chunk maxima of every row (rows >= n_live are dropped
   // once n_live is known), pair logits, leaf scores, every row's lse, then n_live.
   const uint64_t* ssec = smax + s.topk_half;  // second largest keys, same layout
+  // Sub-chunk i of a round is read by wave i % 16 (kSub = kFinalWaves): every wave sees
+  // sub-chunk w of every chunk of every row, so each wave's maximum is drawn from all
+  // rows and the bound below stays tight however the beams' scores differ.
+  auto sub_index = [&](int i0, int q) { return i0 + (q * 64 + lane) * kSub + wave; };
   uint64_t km0[kSubPer], ks0[kSubPer];
 #pragma unroll
   for (int q = 0; q < kSubPer; ++q) {
-    const int i = q * kFinalThreads + (int)threadIdx.x;
+    const int i = sub_index(0, q);
     km0[q] = i < b * per_row ? smax[i] : 0;
     ks0[q] = i < b * per_row ? ssec[i] : 0;
   }
@@ -319,7 +324,8 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
   const float inv_per_row = 1.0f / (float)per_row;
 
   // Bound L (ord of a score): with b <= 16, the b-th largest of the 16 waves' maxima of
-  // the sub-chunk maximum scores (16 distinct sub-chunks reach their wave's maximum);
+  // the sub-chunk maximum scores (16 distinct sub-chunks reach their wave's maximum, and
+  // each wave covers every row);
   // otherwise the largest of the waves' exact b-th largest.  Rounds of kSubPer *
   // kFinalThreads sub-chunks.
   uint32_t o[kSubPer];
@@ -327,7 +333,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
   for (int i0 = 0; i0 < nsub; i0 += kSubPer * kFinalThreads) {
 #pragma unroll
     for (int q = 0; q < kSubPer; ++q) {
-      const int i = i0 + q * kFinalThreads + (int)threadIdx.x;
+      const int i = sub_index(i0, q);
       const uint64_t km = i >= nsub ? 0 : i0 == 0 ? km0[q] : smax[i];
       const int r = div_small(i, inv_per_row);
       o[q] = km != 0 ? ord_score(score_only(key_x(km), row_lse[r], row_score[r])) : 0u;
@@ -356,7 +362,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     uint64_t ks[kSubPer], kx[kSubPer];
 #pragma unroll
     for (int q = 0; q < kSubPer; ++q) {
-      const int i = i0 + q * kFinalThreads + (int)threadIdx.x;
+      const int i = sub_index(i0, q);
       const uint64_t km = i >= nsub ? 0 : i0 == 0 ? km0[q] : smax[i];
       const uint64_t k2 = i >= nsub ? 0 : i0 == 0 ? ks0[q] : ssec[i];
       const int r = div_small(i, inv_per_row);
