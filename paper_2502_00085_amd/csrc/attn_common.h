@@ -5,18 +5,32 @@
 
 namespace td {
 
-// Work unit of one attention WG: (trie, layer of the call, KV head, row block, split).
+// Work unit of one attention WG: (trie, layer of the call, KV head, row block, split);
+// `unit` numbers (trie, layer, KV head, row block) for the split partials.
 struct AttnUnit {
-  int t, li, g, rb, split;
+  int t, li, g, rb, split, unit;
 };
 
+// WGs are dispatched round-robin over the 8 XCDs (each with its own L2).  With several
+// row blocks, the WGs that stream the same node range (the row blocks of one trie, layer,
+// KV head and split) are placed 8 apart in the grid when a.xcd_group is set: on the same
+// XCD, one after the other, so the later ones read that range from L2.
 __device__ inline AttnUnit attn_unit(const DevState& s, const AttnArgs& a) {
   int x = blockIdx.x;
   AttnUnit u;
-  u.split = x % a.splits;
-  x /= a.splits;
-  u.rb = x % a.row_blocks;
-  x /= a.row_blocks;
+  if (a.xcd_group) {
+    const int xcd = x % 8, k = x / 8;
+    u.rb = k % a.row_blocks;
+    x = (k / a.row_blocks) * 8 + xcd;  // ((t * nl + li) * Hkv + g) * splits + split
+    u.split = x % a.splits;
+    x /= a.splits;
+  } else {
+    u.split = x % a.splits;
+    x /= a.splits;
+    u.rb = x % a.row_blocks;
+    x /= a.row_blocks;
+  }
+  u.unit = x * a.row_blocks + u.rb;
   u.g = x % s.Hkv;
   x /= s.Hkv;
   u.li = x % a.n_layers;

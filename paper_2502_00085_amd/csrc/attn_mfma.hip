@@ -313,7 +313,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
 
   // 8 consecutive output elements per thread: 16-byte LDS reads, one 16-byte store
   __bf16* outp = static_cast<__bf16*>(a.out);
-  const int unit = blockIdx.x / a.splits;
+  const int unit = u.unit;
   float* part = s.attn_part + (size_t)unit * a.splits * kRows * (D + 2);
   for (int idx = threadIdx.x; idx < kRows * (D / 8); idx += NW * 64) {
     const int i = idx / (D / 8), c = idx % (D / 8) * 8;
@@ -374,6 +374,8 @@ int attn_choose_splits(const DevState& s, int n_layers, int row_blocks) {
 
 hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
                             hipEvent_t ev1) {
+  // (4-wave WGs, two per CU, measured slower than 8-wave WGs one per CU on every shape
+  // here, also for launches of several WG rounds)
   const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * a.splits), block(kNW * 64);
   switch (s.D) {
     case 64: hipExtLaunchKernelGGL((k_attn_mfma<64, kNW>), grid, block, 0, st, ev0, ev1, 0, s, a); break;

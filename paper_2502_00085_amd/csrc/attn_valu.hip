@@ -161,7 +161,7 @@ __global__ __launch_bounds__(kValuThreads) void k_attn_valu(DevState s, AttnArgs
   __syncthreads();
 
   T* outp = static_cast<T*>(a.out);
-  const int unit = blockIdx.x / a.splits;
+  const int unit = u.unit;
   float* part = s.attn_part + (size_t)unit * a.splits * R * (DD + 2);
   for (int idx = threadIdx.x; idx < R * DD; idx += kValuThreads) {
     const int i = idx / DD, c = idx % DD;

@@ -222,6 +222,7 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   a.splits = c->splits_override > 0 ? c->splits_override : td::attn_choose_splits(s, n_layers, a.row_blocks);
   const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;
+  a.xcd_group = a.row_blocks > 1 && ((long)s.T * n_layers * s.Hkv * a.splits) % 8 == 0 ? 1 : 0;
   // Rows moved by the last compaction are copied before the layer's first attention: by
   // the attention WGs themselves when each owns a whole (layer, KV head) and every layer
   // of the call is still due, else by a copy launch per due layer range.

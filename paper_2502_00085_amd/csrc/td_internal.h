@@ -66,6 +66,7 @@ struct AttnArgs {
                          //    trie, layer and KV head: splits == row_blocks == 1)
   int splits;            // WGs per (trie, layer, kv head, row block) along the node axis
   int row_blocks;        // ceil(b * G / rows_per_block)
+  int xcd_group;         // place the row blocks of a node range on one XCD (see attn_unit)
 };
 
 hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const int32_t* d_tokens,
