@@ -7,8 +7,10 @@ Per step s (s = 1, 2, ...):
 2. every live leaf attends over its ancestor path (Section 3.3);
 3. row log-softmax and the global top-b over the n_live x V candidates
    (``argsort_b`` of Alg 2);
-4. the b chosen continuations are appended (``update_trie``), then the trie is
-   garbage-collected (Section 3.5) - here at every step, i.e. interval g = 1.
+4. the b chosen continuations are appended (``update_trie``, ``update_mask``),
+   then, when the collection interval g says so (``Trie.gc_due``: the position
+   predicted next is a multiple of g), the trie is garbage-collected (Section 3.5);
+   g = 1 collects at every step.
 
 Two ways to choose what is appended:
 
@@ -50,6 +52,7 @@ def decode_step(trie: Trie, step: int, q: Optional[np.ndarray], k_new, v_new, lo
         out["pair_score"] = sc
         out["pair_logprob"] = lp
     trie.append(par, tok, sc)
-    trie.garbage_collect()
+    if trie.gc_due():
+        trie.garbage_collect()
     out["state"] = trie.state()
     return out

@@ -12,6 +12,15 @@ Follows the paper's Methodology section:
   from the live leaves, removes the unmarked nodes from the pointer structure
   and keeps the survivors in their previous relative order (the
   ``index_select`` compaction of the KV cache).
+* Alg 2 / Section 3.5, deferred collection: with interval g the collection runs
+  at the top of the iteration that predicts position i whenever i mod g = 0.
+  After the append that brings the leaves to depth D_new, the next position is
+  D_new + 1, so ``gc_due`` tests (D_new + 1) mod g.  Until then a dead node
+  stays in ``order`` with an all-zero mask (its ancestor bits remap to nothing)
+  and is never attended.  The collection Alg 2 would run before the first
+  prediction (when P mod g = 0) is not modelled: right after the prompt no node
+  is dead, and with a window it could only drop prompt nodes the first query
+  cannot see.
 * Alg 3: the causal mask has one row per live leaf; walking from each leaf to
   the root opens that leaf's path.  ``alg3_mask`` returns it as one bit per
   (slot, leaf) instead of a dense b x N matrix of 0 / -inf.
@@ -46,10 +55,14 @@ class Node:
 
 
 class Trie:
-    def __init__(self, prompt_tokens, prompt_k, prompt_v, beam_width: int, window: int = 0):
+    def __init__(self, prompt_tokens, prompt_k, prompt_v, beam_width: int, window: int = 0,
+                 gc_interval: int = 1):
         """prompt_k / prompt_v: [L'][Hkv][P][d] exact fp32 values of the prefill K/V."""
         self.b = int(beam_width)
         self.window = int(window)
+        self.gc_interval = int(gc_interval)
+        if self.gc_interval < 1:
+            raise ValueError("gc_interval must be >= 1")
         self.prompt_len = len(prompt_tokens)
         self.order: List[Node] = []
         prev = None
@@ -67,6 +80,9 @@ class Trie:
         self.step = 0           # completed appends
         self.pruned = 0         # nodes removed because no live leaf reaches them
         self.evicted = 0        # nodes removed because they left every beam's window
+        self.collections = 0    # garbage collections run
+        self.collected_at = 0   # step of the last collection (0: none yet)
+        self.n_after_collection = len(self.order)
         # incremental mask (Alg 2 update_mask), cross-checked against Alg 3: every prompt
         # node lies on the single leaf's path (bit 0)
         self.masks = {id(n): 1 for n in self.order}
@@ -126,8 +142,15 @@ class Trie:
         self.scores = np.asarray(score, dtype=np.float32).copy()
         self.step = s
 
+    def gc_due(self) -> bool:
+        """Alg 2: collect before predicting position i when i mod g = 0; the next position
+        after the leaves at depth D is D + 1."""
+        return (self.leaf_depth + 1) % self.gc_interval == 0
+
     def garbage_collect(self):
         """Section 3.5: mark (walk up from the leaves), prune, compact (stable)."""
+        self.collections += 1
+        self.collected_at = self.step
         marked = set()
         for leaf in self.leaves:
             n = leaf
@@ -154,6 +177,7 @@ class Trie:
             if id(n) in alive and n.parent is not None and id(n.parent) not in alive:
                 n.parent = None
         self.order = [n for n in self.order if id(n) in alive]
+        self.n_after_collection = len(self.order)
 
     # ---- views ---------------------------------------------------------------------------
     def alg3_mask(self) -> np.ndarray:

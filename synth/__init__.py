@@ -60,6 +60,7 @@ class Workload:
     alpha: float            # parent-rank exponent: P(rank r) ~ (r+1)^-alpha
     qkv_std: float
     logit_std: float
+    gc_interval: int = 1    # garbage-collection interval g (Alg 2); 1 = collect every step
 
     @property
     def group(self) -> int:

@@ -30,11 +30,11 @@ import synth
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
-def small_workload(b=3, V=20, P=5, steps=8, W=0, L=2, Hq=4, Hkv=2, d=8, alpha=1.0):
+def small_workload(b=3, V=20, P=5, steps=8, W=0, L=2, Hq=4, Hkv=2, d=8, alpha=1.0, g=1):
     return synth.WORKLOADS["tiny"].replace(
         name="small", cfg_id=100, n_layers=L, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d, dtype="f32",
         n_tries=1, prompt_min=P, prompt_max=P, beam_width=b, steps=steps, vocab=V, window=W,
-        alpha=alpha)
+        alpha=alpha, gc_interval=g)
 
 
 def _prompt(w, seed):
@@ -53,7 +53,7 @@ def _step_inputs(w, s, seed):
 # --------------------------------------------------------------------------------------------
 def pin_batch_equivalence(w, seed, scripted=False, check_invariants=True):
     tok, pk, pv = _prompt(w, seed)
-    trie = otrie.Trie(tok, pk, pv, w.beam_width, w.window)
+    trie = otrie.Trie(tok, pk, pv, w.beam_width, w.window, w.gc_interval)
     bb = obb.BatchBeamSearch(tok, pk, pv, w.beam_width, w.window)
     scale = 1.0 / np.sqrt(w.head_dim)
     for s in range(1, w.steps + 1):
@@ -83,11 +83,61 @@ def pin_batch_equivalence(w, seed, scripted=False, check_invariants=True):
             seq = bb.beams[j]
             last = len(seq.ids) - 1
             keep = [i for i in range(len(seq.ids)) if w.window == 0 or last - i < w.window]
-            assert [n.id for n in trie.path(leaf)] == [seq.ids[i] for i in keep], f"step {s}: path ids"
-            assert [n.token for n in trie.path(leaf)] == [seq.tokens[i] for i in keep], "path tokens"
+            # the visible path always; the stored path too right after a collection (nodes that
+            # left the window stay stored until the next one)
+            paths = [trie.visible_path(leaf)] + ([trie.path(leaf)] if trie.collected_at == s else [])
+            for pth in paths:
+                assert [n.id for n in pth] == [seq.ids[i] for i in keep], f"step {s}: path ids"
+                assert [n.token for n in pth] == [seq.tokens[i] for i in keep], "path tokens"
         if check_invariants:
             oinv.check(trie)
     return trie, bb
+
+
+# --------------------------------------------------------------------------------------------
+# deferred garbage collection (interval g) against collection at every step
+# --------------------------------------------------------------------------------------------
+def pin_gc_deferral(w, seed, scripted=True):
+    """With interval g (w.gc_interval) the decode results are those of g = 1 (a dead node
+    is on no path, so it is never attended) and the stored state is the g = 1 state plus
+    the nodes a collection would drop, in creation order: dead ones (mask 0) and, with a
+    window, those at depth <= D - W.  Collections run exactly after the appends whose next
+    position P + s is a multiple of g (Alg 2), and there the two states are identical."""
+    g = w.gc_interval
+    tok, pk, pv = _prompt(w, seed)
+    t1 = otrie.Trie(tok, pk, pv, w.beam_width, w.window, 1)
+    tg = otrie.Trie(tok, pk, pv, w.beam_width, w.window, g)
+    scale = 1.0 / np.sqrt(w.head_dim)
+    P = w.prompt_min
+    gcs = 0
+    for s in range(1, w.steps + 1):
+        q, kn, vn, logits = _step_inputs(w, s, seed)
+        script = None
+        if scripted:
+            par, tk = synth.step_script(w, s, seed)
+            script = (par[0], tk[0])
+        r1 = odec.decode_step(t1, s, q, kn, vn, logits, scale, script)
+        rg = odec.decode_step(tg, s, q, kn, vn, logits, scale, script)
+        assert np.array_equal(r1["o"], rg["o"]), f"step {s}: attention depends on g"
+        for key in ("sel_parent", "sel_token", "sel_score", "sel_logprob", "lse"):
+            assert np.array_equal(r1[key], rg[key]), f"step {s}: {key} depends on g"
+        due = (P + s) % g == 0
+        gcs += due
+        assert (tg.collected_at == s) == due and tg.collections == gcs, f"step {s}: schedule"
+        a, c = r1["state"], rg["state"]
+        D = int(c["depth"][c["n_nodes"] - 1])
+        keep = np.nonzero((c["mask"] != 0) & ((w.window == 0) | (D - c["depth"] < w.window)))[0]
+        for key in ("node_id", "token", "depth", "mask"):
+            assert np.array_equal(c[key][keep], a[key]), f"step {s}: stored {key}"
+        kept = set(c["node_id"][keep].tolist())
+        pid = np.array([p if p in kept else -1 for p in c["parent_id"][keep].tolist()], dtype=np.int32)
+        assert np.array_equal(pid, a["parent_id"]), f"step {s}: parents"
+        assert np.array_equal(c["leaf_score"], a["leaf_score"])
+        if due:
+            for key in ("node_id", "parent_slot", "token", "depth", "mask", "leaf_slot"):
+                assert np.array_equal(c[key], a[key]), f"step {s}: state {key} after a collection"
+        oinv.check(tg)
+    return tg
 
 
 # --------------------------------------------------------------------------------------------

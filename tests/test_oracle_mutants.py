@@ -3,7 +3,9 @@
 Every mutant is a plausible slip in code of this kind - a dropped scale, a wrong
 GQA head mapping, an off-by-one window, reversed tie order, a float32 log-sum-exp,
 a missing prune, a wrong mask remap, a wrong parent, a swapped query row, a
-missing window eviction, a wrong row in the pair score.  The pins run on a
+missing window eviction, a wrong row in the pair score, a collection schedule
+counted in steps or ignoring the interval, dead nodes keeping stale mask bits
+between collections.  The pins run on a
 monkeypatched copy of the oracle for the duration of one test.
 """
 import numpy as np
@@ -123,3 +125,28 @@ def test_mutant_pair_score_row(monkeypatch):
         return (np.asarray(scores, np.float32)[parent] + lp).astype(np.float32), lp
     monkeypatch.setattr(obeam, "pair_scores", bad)
     _fails(pins.pin_pair_scores, 9)
+
+
+def test_mutant_gc_phase_counts_steps(monkeypatch):
+    # collection every g decode steps instead of at positions that are multiples of g
+    monkeypatch.setattr(otrie.Trie, "gc_due", lambda self: self.step % self.gc_interval == 0)
+    _fails(pins.pin_gc_deferral, pins.small_workload(b=3, V=30, P=5, steps=10, g=4), 5)
+
+
+def test_mutant_gc_ignores_interval(monkeypatch):
+    monkeypatch.setattr(otrie.Trie, "gc_due", lambda self: True)
+    _fails(pins.pin_batch_equivalence, pins.small_workload(b=3, V=30, P=5, steps=10, g=4), 6)
+
+
+def test_mutant_deferred_gc_keeps_old_masks(monkeypatch):
+    # a node that is on no new path keeps its old bits until the collection
+    orig = otrie.Trie.append
+
+    def bad(self, parent_rank, token, score):
+        old = {id(n): self.masks[id(n)] for n in self.order}
+        orig(self, parent_rank, token, score)
+        for n in self.order[:-self.b]:
+            if self.masks[id(n)] == 0:
+                self.masks[id(n)] = old[id(n)]
+    monkeypatch.setattr(otrie.Trie, "append", bad)
+    _fails(pins.pin_gc_deferral, pins.small_workload(b=4, V=30, P=5, steps=10, g=5), 7)

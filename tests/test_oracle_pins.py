@@ -24,6 +24,19 @@ def test_trie_equals_batch_beam_search_scripted(b, W, alpha, seed):
     pins.pin_batch_equivalence(w, seed, scripted=True)
 
 
+@pytest.mark.parametrize("b,W,g,seed", [(3, 0, 3, 30), (4, 3, 4, 31), (5, 0, 15, 32), (2, 2, 2, 33)])
+def test_deferred_gc_trie_equals_batch_beam_search(b, W, g, seed):
+    pins.pin_batch_equivalence(pins.small_workload(b=b, V=25, W=W, steps=14, g=g), seed)
+
+
+@pytest.mark.parametrize("b,W,g,alpha,P,seed", [(3, 0, 3, 1.0, 5, 40), (4, 4, 5, 0.0, 7, 41),
+                                                (8, 0, 15, 1.0, 6, 42), (1, 3, 4, 1.0, 5, 43),
+                                                (6, 2, 2, 0.0, 4, 44)])
+def test_deferred_gc_equals_collection_every_step(b, W, g, alpha, P, seed):
+    tg = pins.pin_gc_deferral(pins.small_workload(b=b, V=40, P=P, W=W, steps=20, alpha=alpha, g=g), seed)
+    assert tg.collections == sum((P + s) % g == 0 for s in range(1, 21))
+
+
 @pytest.mark.parametrize("W,seed", [(0, 20), (3, 21)])
 def test_path_attention_equals_alg3_masked_dense_sdpa(W, seed):
     pins.pin_dense_mask(pins.small_workload(b=4, V=30, W=W, steps=6), seed)
