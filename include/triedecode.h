@@ -10,8 +10,8 @@
  *   beam_logsoftmax_topk  row log-softmax and the global top-b over the b x V
  *                         continuations (the argsort_b of Alg 1 / Alg 2)
  *   trie_append_prune     append the b chosen children (update_trie / update_mask of
- *                         Alg 2), then garbage-collect: mark, prune, compact
- *                         (Section 3.5)
+ *                         Alg 2), then, every g-th position, garbage-collect: mark,
+ *                         prune, compact (Section 3.5)
  *
  * Memory.  The caller owns every tensor (K/V pools, queries, outputs, logits and
  * selections) as device memory; PyTorch tensors are the intended source.  The library
@@ -30,9 +30,12 @@
  *
  * Slots.  Node metadata and K/V rows live at physical slots base .. base+n_nodes-1 of a
  * trie (base advances when a sliding window evicts the oldest nodes, so evicted rows are
- * never moved).  Survivors keep their relative order (the paper's index_select
+ * never moved; a collection that would leave too little room after the trie re-packs it
+ * at slot 0).  Survivors keep their relative order (the paper's index_select
  * compaction), so node ids and depths never decrease along the slots, and the live
- * leaves are always the last n_live slots, in rank order.
+ * leaves are always the last n_live slots, in rank order.  Between collections
+ * (gc_interval > 1) a node that no live leaf reaches keeps its slot with mask 0; it is
+ * never attended.
  *
  * Errors.  Argument checks run on the host before any HIP call and return TD_EINVAL
  * with nothing changed.  A failed HIP launch returns TD_EHIP.  Conditions only the
@@ -80,6 +83,9 @@ typedef struct {
   int32_t window;       /* sliding window W (0 = dense): key visible iff D - depth < W    */
   int32_t dtype;        /* td_dtype of pools, q, out, k_new, v_new                        */
   int32_t attn_impl;    /* td_attn_impl                                                   */
+  int32_t gc_interval;  /* g >= 1: garbage is collected after the appends whose next      */
+                        /*   position (leaf depth + 1) is a multiple of g (Alg 2); 1 =    */
+                        /*   after every append                                           */
   void* k_pool;         /* caller-owned device [T][L][Hkv][capacity][d]; valid until      */
   void* v_pool;         /*   td_destroy                                                   */
 } td_desc;
@@ -88,7 +94,7 @@ typedef struct {
  * Arrays are caller-allocated host memory with room for capacity (node arrays) and
  * beam_width (leaf arrays) entries. */
 typedef struct {
-  int32_t n_nodes;      /* N: stored (live) nodes                                         */
+  int32_t n_nodes;      /* N: stored nodes (dead ones included until the next collection) */
   int32_t n_live;       /* live leaves (1 after the prompt, b afterwards)                 */
   int32_t base;         /* physical slot of logical slot 0 (read only)                    */
   int32_t n_shared;     /* leading slots on every live beam's path (read only)            */
@@ -99,7 +105,8 @@ typedef struct {
   int32_t* parent_slot; /* [N] logical slot of the parent, -1 for a root                 */
   int32_t* token;       /* [N]                                                            */
   int32_t* depth;       /* [N] position in the equivalent per-beam sequence (Section 3.4) */
-  uint64_t* mask;       /* [N] bit i set <=> slot lies on live leaf i's path (Alg 3)      */
+  uint64_t* mask;       /* [N] bit i set <=> slot lies on live leaf i's path (Alg 3);     */
+                        /*     0 for a dead node awaiting collection                      */
   int32_t* leaf_slot;   /* [n_live] logical slots of the live leaves, rank order          */
   float* leaf_score;    /* [n_live] cumulative log-probability of each live leaf          */
 } td_state;
@@ -154,18 +161,24 @@ td_status beam_logsoftmax_topk(td_ctx* ctx, const float* d_logits, int32_t* d_se
                                const int32_t* d_pair_token, float* d_pair_score,
                                hipStream_t stream);
 
-/* Alg 2 update_trie + update_mask, then Section 3.5 garbage collection (every call).
+/* Alg 2 update_trie + update_mask, then, when due, Section 3.5 garbage collection.
  * New node j (j < b) is a child of live leaf sel_parent[j] with token sel_token[j],
  * score sel_score[j], depth D+1 and id next_id+j; every stored node's mask is remapped
- * (new bit j = old bit sel_parent[j]).  A node dies when its new mask is 0 (no live leaf
- * reaches it) or, with a window, when depth <= D+1-W.  Survivors are compacted stably
- * (parent slots remapped, -1 if the parent died).  The K/V rows of moved survivors are
- * copied to their new slots by the next trie_attn_decode call of each layer, before it
- * reads them (until then the pools hold those rows at their old slots; td_init_prompt and
- * td_load_state drop copies still due).  The new leaves become the last b slots in rank
- * j order; their K/V rows are pending until the next trie_attn_decode.
- * Inputs [T][b] device.  Invalid selections / capacity overflow: sticky device status,
- * trie unchanged. */
+ * (new bit j = old bit sel_parent[j]; a node whose new mask is 0 is dead: no live leaf
+ * reaches it).  The collection runs in this call when D+2, the position predicted next,
+ * is a multiple of desc.gc_interval (Alg 2 collects at the top of such an iteration; with
+ * g = 1 every call collects).  It drops the dead nodes and, with a window, those with
+ * depth <= D+1-W, and compacts the survivors stably (parent slots remapped, -1 if the
+ * parent died).  If the room after the compacted trie is smaller than the (g-1)*b slots
+ * the appends before the next collection need, the trie is re-packed at slot 0.  The
+ * K/V rows of moved survivors are copied to their new slots by the next trie_attn_decode
+ * call of each layer, before it reads them (until then the pools hold those rows at their
+ * old slots; td_init_prompt and td_load_state drop copies still due).  The new leaves
+ * become the last b slots in rank j order; their K/V rows are pending until the next
+ * trie_attn_decode.
+ * Inputs [T][b] device.  Invalid selections / capacity overflow (a trie without room for
+ * its next b nodes after any collection of this call): sticky device status, trie
+ * unchanged. */
 td_status trie_append_prune(td_ctx* ctx, const int32_t* d_sel_parent, const int32_t* d_sel_token,
                             const float* d_sel_score, hipStream_t stream);
 
@@ -174,8 +187,9 @@ td_status td_read_state(td_ctx* ctx, int32_t trie, td_state* host_out);
 /* Replace trie t by a host state (synchronous).  Slots are placed at base 0.  The state
  * must be one the method can produce: depth non-decreasing along slots, parents before
  * children with depth + 1, leaves = last n_live slots in rank order with one-hot masks,
- * the all-beam (shared) slots a prefix.  The pools must hold the K/V rows of every slot
- * (except the leaves' when kv_pending = 1). */
+ * no all-beam slot after a slot on only some paths (dead slots, mask 0, may lie anywhere
+ * before the leaves).  The pools must hold the K/V rows of every slot (except the leaves'
+ * when kv_pending = 1). */
 td_status td_load_state(td_ctx* ctx, int32_t trie, const td_state* host_in);
 /* Read and clear the sticky device status (synchronises the device).  When the status
  * comes from a rejected trie_append_prune of a one-trie context, the context is returned

@@ -27,7 +27,7 @@ class TdDesc(ctypes.Structure):
                 ("n_layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("window", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("attn_impl", ctypes.c_int32),
+                ("attn_impl", ctypes.c_int32), ("gc_interval", ctypes.c_int32),
                 ("k_pool", ctypes.c_void_p), ("v_pool", ctypes.c_void_p)]
 
 
@@ -268,7 +268,7 @@ class TrieDecoder:
     """One context plus its caller-owned K/V pools, allocated as torch tensors on the device."""
 
     def __init__(self, n_tries, beam_width, capacity, vocab, n_layers, n_q_heads, n_kv_heads,
-                 head_dim, window=0, dtype="bf16", attn_impl=TD_ATTN_AUTO, device="cuda"):
+                 head_dim, window=0, dtype="bf16", attn_impl=TD_ATTN_AUTO, device="cuda", gc_interval=1):
         import torch
         self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
         shape = (n_tries, n_layers, n_kv_heads, capacity, head_dim)
@@ -276,7 +276,7 @@ class TrieDecoder:
         self.v_pool = torch.zeros(shape, dtype=self.tdtype, device=device)
         self.desc = TdDesc(n_tries, beam_width, capacity, vocab, n_layers, n_q_heads, n_kv_heads,
                            head_dim, window, TD_BF16 if dtype == "bf16" else TD_F32, attn_impl,
-                           self.k_pool.data_ptr(), self.v_pool.data_ptr())
+                           gc_interval, self.k_pool.data_ptr(), self.v_pool.data_ptr())
         self.dims = Dims(self.desc)
         self.ctx = td_create(self.desc)
 

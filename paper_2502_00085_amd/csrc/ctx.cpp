@@ -19,6 +19,8 @@ struct td_ctx {
   std::vector<uint8_t> layer_written;  // per layer, while pending
   bool moves_pending = false;          // rows moved by the last compaction not yet copied
                                        //   (for the layers not yet written)
+  std::vector<int32_t> leaf_depth;     // per trie: depth of its live leaves (mirrors the
+                                       //   device header; tells which appends collect)
   int32_t* d_plen = nullptr;
   int splits_override = 0;             // TD_ATTN_SPLITS (tuning): WGs per attention unit
   hipEvent_t attn_ev0 = nullptr;       // td_set_attn_events: kernel-timestamp events of the
@@ -105,6 +107,8 @@ td_status td_create(const td_desc* d, td_ctx** out) {
   if (d->capacity < d->beam_width + 1 || d->capacity > (1 << 30))
     return fail(nullptr, TD_EINVAL, "capacity must be in [beam_width + 1, 2^30]");
   if (d->window < 0) return fail(nullptr, TD_EINVAL, "window must be >= 0");
+  if (d->gc_interval < 1 || d->gc_interval > (1 << 20))
+    return fail(nullptr, TD_EINVAL, "gc_interval must be in [1, 2^20]");
   if (d->dtype != TD_F32 && d->dtype != TD_BF16) return fail(nullptr, TD_EINVAL, "bad dtype");
   if (d->attn_impl < TD_ATTN_AUTO || d->attn_impl > TD_ATTN_MFMA)
     return fail(nullptr, TD_EINVAL, "bad attn_impl");
@@ -130,6 +134,7 @@ td_status td_create(const td_desc* d, td_ctx** out) {
   s.Hkv = d->n_kv_heads;
   s.D = d->head_dim;
   s.W = d->window;
+  s.G = d->gc_interval;
   s.dtype = d->dtype;
   s.k_pool = d->k_pool;
   s.v_pool = d->v_pool;
@@ -154,6 +159,7 @@ td_status td_create(const td_desc* d, td_ctx** out) {
     return hip_fail(nullptr, e, "allocating trie metadata / workspace");
   }
   c->inited.assign(s.T, 0);
+  c->leaf_depth.assign(s.T, 0);
   c->layer_written.assign(s.L, 0);
   if (const char* sp = getenv("TD_ATTN_SPLITS")) c->splits_override = atoi(sp) > 0 ? (atoi(sp) < 64 ? atoi(sp) : 64) : 0;
   *out = c;
@@ -185,6 +191,7 @@ td_status td_init_prompt(td_ctx* c, const int32_t* h_plen, const int32_t* d_toke
   if (e == hipSuccess) e = td::launch_init_prompt(c->dev, c->d_plen, d_tokens, stride, st);
   if (e != hipSuccess) return hip_fail(c, e, "td_init_prompt");
   c->inited.assign(c->dev.T, 1);
+  for (int t = 0; t < c->dev.T; ++t) c->leaf_depth[t] = h_plen[t] - 1;
   c->pending = c->moves_pending = false;
   c->layer_written.assign(c->dev.L, 0);
   return TD_OK;
@@ -299,8 +306,14 @@ td_status trie_append_prune(td_ctx* c, const int32_t* d_sel_parent, const int32_
     return fail(c, TD_ESTATE, "trie_attn_decode has not stored the leaves' K/V for every layer");
   hipError_t e = td::launch_append_prune(c->dev, d_sel_parent, d_sel_token, d_sel_score, st);
   if (e != hipSuccess) return hip_fail(c, e, "trie_append_prune launch");
+  // rows move only where this append collects (Alg 2: the next position is a multiple of g)
+  bool collects = false;
+  for (int t = 0; t < c->dev.T; ++t) {
+    ++c->leaf_depth[t];
+    collects = collects || (c->leaf_depth[t] + 1) % c->dev.G == 0;
+  }
   c->pending = true;
-  c->moves_pending = true;
+  c->moves_pending = collects;
   c->layer_written.assign(c->dev.L, 0);
   return TD_OK;
 }
@@ -337,6 +350,7 @@ td_status td_read_state(td_ctx* c, int32_t trie, td_state* o) {
   for (size_t i = 0; i < n; ++i)
     o->parent_slot[i] = o->parent_slot[i] >= 0 ? o->parent_slot[i] - h.base : -1;
   for (int j = 0; j < h.n_live; ++j) o->leaf_slot[j] = h.n_nodes - h.n_live + j;
+  c->leaf_depth[trie] = h.leaf_depth;
   o->n_nodes = h.n_nodes;
   o->n_live = h.n_live;
   o->base = h.base;
@@ -360,10 +374,12 @@ td_status td_load_state(td_ctx* c, int32_t trie, const td_state* in) {
   const uint64_t full = nl == 64 ? ~0ull : ((1ull << nl) - 1ull);
   int n_shared = 0;
   while (n_shared < N && in->mask[n_shared] == full) ++n_shared;
+  bool partial = false;
   for (int i = 0; i < N; ++i) {
     const uint64_t m = in->mask[i];
-    if (m == 0 || (m & ~full) != 0) return fail(c, TD_EINVAL, "slot %d: mask must be a non-empty subset of the live leaves", i);
-    if (i >= n_shared && m == full) return fail(c, TD_EINVAL, "slots on every beam's path must be a leading run");
+    if ((m & ~full) != 0) return fail(c, TD_EINVAL, "slot %d: mask must be a subset of the live leaves", i);
+    if (m == full && partial) return fail(c, TD_EINVAL, "slot %d: a slot on every beam's path follows one on only some", i);
+    partial = partial || (m != 0 && m != full);
     if (i > 0 && in->depth[i] < in->depth[i - 1]) return fail(c, TD_EINVAL, "depth must not decrease along the slots");
     const int p = in->parent_slot[i];
     if (p >= i || p < -1) return fail(c, TD_EINVAL, "slot %d: parent must precede its child", i);
@@ -400,6 +416,7 @@ td_status td_load_state(td_ctx* c, int32_t trie, const td_state* in) {
   if (e == hipSuccess) e = hipMemcpy(s.hdr + trie, &h, sizeof h, hipMemcpyHostToDevice);
   if (e != hipSuccess) return hip_fail(c, e, "td_load_state");
   c->inited[trie] = 1;
+  c->leaf_depth[trie] = h.leaf_depth;
   c->pending = in->kv_pending != 0;
   c->moves_pending = false;
   c->layer_written.assign(s.L, 0);
@@ -413,6 +430,13 @@ td_status td_get_status(td_ctx* c) {
   if (e == hipSuccess) e = hipMemcpy(v, c->dev.status, sizeof v, hipMemcpyDeviceToHost);
   if (e == hipSuccess) e = hipMemset(c->dev.status, 0, sizeof v);
   if (e != hipSuccess) return hip_fail(c, e, "td_get_status");
+  if (v[1]) {
+    // the rejected trie kept its leaves: take the leaf depths from the device again
+    std::vector<td::TrieHdr> h(c->dev.T);
+    e = hipMemcpy(h.data(), c->dev.hdr, sizeof(td::TrieHdr) * h.size(), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(c, e, "td_get_status");
+    for (int t = 0; t < c->dev.T; ++t) c->leaf_depth[t] = h[t].leaf_depth;
+  }
   if (v[1] && c->dev.T == 1) {
     // a rejected append left the trie as it was: the leaves' K/V are stored, not pending
     // (with several tries the others advanced; such a context needs td_load_state)

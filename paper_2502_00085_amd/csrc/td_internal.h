@@ -14,7 +14,8 @@ struct TrieHdr {
   int32_t n_nodes;     // stored nodes N
   int32_t base;        // physical slot of logical slot 0
   int32_t n_live;      // live leaves (last n_live logical slots, rank order)
-  int32_t n_shared;    // leading logical slots that lie on every live leaf's path
+  int32_t n_shared;    // leading logical slots that lie on every live leaf's path (a dead
+                       //   slot, kept until the next collection, ends the run)
   int32_t leaf_depth;  // depth D of every live leaf
   int32_t next_id;     // id given to the next appended node of rank 0
   int32_t pad0, pad1;
@@ -23,6 +24,7 @@ struct TrieHdr {
 // Device-side pointers of one context.  Node arrays are [T][cap], indexed by physical slot.
 struct DevState {
   int T, b, cap, V, L, Hq, Hkv, D, W, dtype;
+  int G;                 // garbage-collection interval g (>= 1)
   void* k_pool;
   void* v_pool;
   TrieHdr* hdr;          // [T]

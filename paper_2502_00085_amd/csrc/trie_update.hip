@@ -1,7 +1,7 @@
 // Trie initialisation, append + mask update, garbage collection and KV compaction (gfx950).
 //
-// Alg 2 (update_trie, update_mask) and Section 3.5 (mark, prune, compact) of the paper,
-// restated for a device-resident trie:
+// Alg 2 (update_trie, update_mask, collection every g steps) and Section 3.5 (mark, prune,
+// compact) of the paper, restated for a device-resident trie:
 //   * a node's ancestor mask holds one bit per live leaf (bit i <=> on leaf i's path);
 //     after the top-b, new bit j of every node is old bit sel_parent[j];
 //   * marking from the leaves is the same as "new mask != 0"; with a sliding window a
@@ -71,6 +71,43 @@ __device__ inline uint64_t remap_mask(uint64_t m, const int* sp, int b) {
   return r;
 }
 
+// Relocation of the shared run [e, r0) (logical slots of the old layout, all on every
+// beam's path) to new physical slots nb + (x - e), below the old ones, with its moves
+// (logical order, so ascending sources) at moves[0 .. r0 - e).  Reads of a chunk complete
+// before its writes and a later chunk reads only above every slot an earlier one wrote.
+// Block-wide; ends with a barrier.
+__device__ inline void relocate_shared_run(const DevState& s, size_t off, int base, int nb, int e,
+                                           int r0, uint64_t full_b) {
+  for (int c0 = e; c0 < r0; c0 += kAppThreads) {
+    const int x = c0 + (int)threadIdx.x;
+    int id = 0, tk = 0, dp = 0, pp = -1;
+    if (x < r0) {
+      id = s.node_id[off + base + x];
+      tk = s.token[off + base + x];
+      dp = s.depth[off + base + x];
+      pp = s.parent[off + base + x];
+    }
+    __syncthreads();
+    if (x < r0) {
+      const size_t dst = off + nb + (x - e);
+      s.node_id[dst] = id;
+      s.token[dst] = tk;
+      s.depth[dst] = dp;
+      s.parent[dst] = (pp >= 0 && pp - base >= e) ? nb + (pp - base - e) : -1;
+      s.mask[dst] = full_b;
+      s.moves[off + (x - e)] = make_int2(base + x, nb + (x - e));
+    }
+    __syncthreads();
+  }
+}
+
+// One WG per trie.  Appends the b selected children of the live leaves and remaps every
+// stored mask; when the collection is due (Alg 2: the position predicted next, D_new + 1,
+// is a multiple of g) it also drops the dead nodes (and, with a window, those no query can
+// see any more) and compacts the survivors stably.  Between collections a dead node keeps
+// its slot with mask 0.  A collection that leaves less room after the trie than the g - 1
+// appends before the next one needs moves the whole trie down to slot 0 (the pool is used
+// as a ring that is re-packed when it would run out; the moves carry the K/V rows).
 __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const int32_t* sel_parent,
                                                               const int32_t* sel_token,
                                                               const float* sel_score) {
@@ -81,8 +118,8 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
   __shared__ int sp[kMaxBeam], stok[kMaxBeam];
   __shared__ float ssc[kMaxBeam];
   __shared__ int err, wave_cnt[kAppWaves], wave_cnt2[kAppWaves];
-  __shared__ int full_cnt;
-  __shared__ int wa[kAppWaves], wf[kAppWaves], wd[kAppWaves];
+  __shared__ int full_cnt, first_nf;
+  __shared__ int wa[kAppWaves], wf[kAppWaves], wd[kAppWaves], wp[kAppWaves];
   __shared__ int lpos[kAppThreads];
 
   // the header and the selection go out together
@@ -96,8 +133,9 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
   }
   const int N = h.n_nodes, base = h.base, n_live = h.n_live;
   const int d_new = h.leaf_depth + 1;
+  const bool gc = (d_new + 1) % s.G == 0;
   // window eviction: the leading run of slots with depth <= d_new - W (depth is sorted)
-  const int e = s.W > 0 ? block_first_above(s.depth + off + base, N, d_new - s.W, wave_cnt) : 0;
+  const int e = (gc && s.W > 0) ? block_first_above(s.depth + off + base, N, d_new - s.W, wave_cnt) : 0;
   const int r0 = max(e, h.n_shared);
   const int base_new = base + e;
   const uint64_t full_b = (b == 64) ? ~0ull : ((1ull << b) - 1ull);
@@ -131,78 +169,112 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
       bad |= i < j && sp[i] == sp[j] && stok[i] == stok[j];
     }
     if (bad) atomicOr(&err, 1);
-    // survivors (new mask != 0), the all-beam ones, and the first dead slot: one exchange
+    // survivors (new mask != 0), the all-beam ones, the first dead and the first
+    // not-all-beam slot: one exchange
     const uint64_t nm = in ? remap_mask(m, sp, b) : 0ull;
     const bool alive = in && nm != 0ull;
     const int lane = tid & 63, wave = tid >> 6;
     const uint64_t ba = __ballot(alive), bd = __ballot(in && !alive);
-    const uint64_t bf = __ballot(alive && nm == full_b);
+    const uint64_t bf = __ballot(alive && nm == full_b), bp = __ballot(in && nm != full_b);
     if (lane == 0) {
       wa[wave] = __popcll(ba);
       wf[wave] = __popcll(bf);
       wd[wave] = bd ? wave * 64 + __ffsll((unsigned long long)bd) - 1 : kAppThreads;
+      wp[wave] = bp ? wave * 64 + __ffsll((unsigned long long)bp) - 1 : kAppThreads;
     }
     __syncthreads();
     int rank = __popcll(ba & ((1ull << lane) - 1ull)), n_alive = 0, n_full = 0, first_dead = kAppThreads;
+    int first_part = kAppThreads;
     for (int w = 0; w < kAppWaves; ++w) {
       rank += w < wave ? wa[w] : 0;
       n_alive += wa[w];
       n_full += wf[w];
       first_dead = min(first_dead, wd[w]);
+      first_part = min(first_part, wp[w]);
     }
-    if (err) {
+    const int n_new = gc ? (r0 - e) + n_alive + b : N + b;
+    // a collection re-packs at slot 0 when the room after the trie is short of the appends
+    // before the next one
+    const bool rebase = gc && base_new > 0 && base_new + n_new + (s.G - 1) * b > s.cap;
+    const int nb = rebase ? 0 : base_new;  // base after this step
+    if (err || nb + n_new > s.cap) {
       if (tid == 0) {
-        set_status(s.status, kDevEinval);
+        set_status(s.status, err ? kDevEinval : kDevEcapacity);
         s.status[1] = 1;
+        s.n_moves[t] = 0;
+      }
+      return;
+    }
+    if (!gc) {
+      // no collection: every node keeps its slot, a dead one with mask 0
+      if (in) s.mask[off + base + n] = nm;
+      if (n_live != b) {
+        for (int x = tid; x < r0; x += kAppThreads) s.mask[off + base + x] = full_b;
+      }
+      if (tid < b) {
+        const size_t dst = off + base + N + tid;
+        s.node_id[dst] = h.next_id + tid;
+        s.token[dst] = stok[tid];
+        s.depth[dst] = d_new;
+        s.parent[dst] = base + N - n_live + sp[tid];
+        s.mask[dst] = 1ull << tid;
+        s.leaf_score[(size_t)t * b + tid] = ssc[tid];
+      }
+      if (tid == 0) {
+        TrieHdr nh;
+        nh.n_nodes = n_new;
+        nh.base = base;
+        nh.n_live = b;
+        // the all-beam run continues through the new leaves only when b == 1
+        nh.n_shared = first_part < kAppThreads ? r0 + first_part : N + (b == 1 ? 1 : 0);
+        nh.leaf_depth = d_new;
+        nh.next_id = h.next_id + b;
+        nh.pad0 = nh.pad1 = 0;
+        s.hdr[t] = nh;
         s.n_moves[t] = 0;
       }
       return;
     }
     const int np = alive ? (r0 - e) + rank : -1;
-    const int n_new = (r0 - e) + n_alive + b;
-    if (base_new + n_new > s.cap) {
-      if (tid == 0) {
-        set_status(s.status, kDevEcapacity);
-        s.status[1] = 1;
-        s.n_moves[t] = 0;
-      }
-      return;
-    }
     lpos[tid] = np;
+    if (rebase) relocate_shared_run(s, off, base, nb, e, r0, full_b);
     __syncthreads();
     auto new_phys = [&](int lp) -> int {  // new physical slot of old logical slot lp < N
       if (lp < e) return -1;
-      if (lp < r0) return base + lp;
+      if (lp < r0) return nb + (lp - e);
       const int q = lpos[lp - r0];
-      return q >= 0 ? base_new + q : -1;
+      return q >= 0 ? nb + q : -1;
     };
     int par = -1;
     if (alive && pp >= 0) {
       const int lp = pp - base;
       par = (lp >= 0 && lp < n) ? new_phys(lp) : -1;
     }
-    // a survivor's physical slot changes (base + r0 + tid -> base_new + np = base + r0 +
-    // rank) iff a slot before it died; its rank among the moved ones is its survivor rank
-    // minus the survivors before the first dead slot (all the slots before it)
-    const bool moved = alive && tid > first_dead;
-    const int mrank = rank - first_dead;
-    const int n_moved = max(0, n_alive - first_dead);
-    if (moved) s.moves[off + mrank] = make_int2(base + n, base_new + np);
-    // all fields were read before the first barrier: rewrite in place
+    // Without a re-pack a survivor's physical slot changes (base + r0 + tid -> base_new +
+    // np = base + r0 + rank) iff a slot before it died; its rank among the moved ones is
+    // its survivor rank minus the survivors before the first dead slot (all the slots
+    // before it).  A re-pack moves every survivor, after the shared run.
+    const bool moved = alive && (rebase || tid > first_dead);
+    const int mrank = rebase ? (r0 - e) + rank : rank - first_dead;
+    const int n_moved = rebase ? (r0 - e) + n_alive : max(0, n_alive - first_dead);
+    if (moved) s.moves[off + mrank] = make_int2(base + n, nb + np);
+    // all fields were read before the first barrier, the shared run's before its writes
     if (alive) {
-      const size_t dst = off + base_new + np;
+      const size_t dst = off + nb + np;
       s.node_id[dst] = id;
       s.token[dst] = tk;
       s.depth[dst] = dp;
       s.parent[dst] = par;
       s.mask[dst] = nm;
     }
-    if (n_live != b) {
-      for (int x = e + tid; x < r0; x += kAppThreads) s.mask[off + base + x] = full_b;
+    if (!rebase) {
+      if (n_live != b) {
+        for (int x = e + tid; x < r0; x += kAppThreads) s.mask[off + base + x] = full_b;
+      }
+      if (tid == 0 && e > 0 && e < r0) s.parent[off + base + e] = -1;
     }
-    if (tid == 0 && e > 0 && e < r0) s.parent[off + base + e] = -1;
     if (tid < b) {
-      const size_t dst = off + base_new + (r0 - e) + n_alive + tid;
+      const size_t dst = off + nb + (r0 - e) + n_alive + tid;
       s.node_id[dst] = h.next_id + tid;
       s.token[dst] = stok[tid];
       s.depth[dst] = d_new;
@@ -213,7 +285,7 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
     if (tid == 0) {
       TrieHdr nh;
       nh.n_nodes = n_new;
-      nh.base = base_new;
+      nh.base = nb;
       nh.n_live = b;
       nh.n_shared = (r0 - e) + n_full + (b == 1 ? 1 : 0);
       nh.leaf_depth = d_new;
@@ -229,6 +301,7 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
   if (tid == 0) {
     err = 0;
     full_cnt = 0;
+    first_nf = N;
   }
   __syncthreads();
   if (tid < b) {
@@ -243,10 +316,49 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
     if (i < j && sp[i] == sp[j] && stok[i] == stok[j]) atomicOr(&err, 1);
   }
   __syncthreads();
-  if (err) {
+  if (err || (!gc && base + N + b > s.cap)) {
     if (tid == 0) {
-      set_status(s.status, kDevEinval);
+      set_status(s.status, err ? kDevEinval : kDevEcapacity);
       s.status[1] = 1;
+      s.n_moves[t] = 0;
+    }
+    return;
+  }
+
+  if (!gc) {
+    // no collection: remap the masks in place (dead slots get 0) and find the first slot
+    // that is not on every path
+    for (int c0 = r0; c0 < N; c0 += kAppThreads) {
+      const int n = c0 + tid;
+      if (n < N) {
+        const uint64_t nm = remap_mask(s.mask[off + base + n], sp, b);
+        s.mask[off + base + n] = nm;
+        if (nm != full_b) atomicMin(&first_nf, n);
+      }
+    }
+    if (n_live != b) {
+      for (int x = tid; x < r0; x += kAppThreads) s.mask[off + base + x] = full_b;
+    }
+    if (tid < b) {
+      const size_t dst = off + base + N + tid;
+      s.node_id[dst] = h.next_id + tid;
+      s.token[dst] = stok[tid];
+      s.depth[dst] = d_new;
+      s.parent[dst] = base + N - n_live + sp[tid];
+      s.mask[dst] = 1ull << tid;
+      s.leaf_score[(size_t)t * b + tid] = ssc[tid];
+    }
+    __syncthreads();
+    if (tid == 0) {
+      TrieHdr nh;
+      nh.n_nodes = N + b;
+      nh.base = base;
+      nh.n_live = b;
+      nh.n_shared = first_nf < N ? first_nf : N + (b == 1 ? 1 : 0);
+      nh.leaf_depth = d_new;
+      nh.next_id = h.next_id + b;
+      nh.pad0 = nh.pad1 = 0;
+      s.hdr[t] = nh;
       s.n_moves[t] = 0;
     }
     return;
@@ -269,7 +381,9 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
     alive_run += tot;
   }
   const int n_new = (r0 - e) + alive_run + b;
-  if (base_new + n_new > s.cap) {
+  const bool rebase = base_new > 0 && base_new + n_new + (s.G - 1) * b > s.cap;
+  const int nb = rebase ? 0 : base_new;
+  if (nb + n_new > s.cap) {
     if (tid == 0) {
       set_status(s.status, kDevEcapacity);
       s.status[1] = 1;
@@ -278,10 +392,11 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
     return;
   }
   __syncthreads();
+  if (rebase) relocate_shared_run(s, off, base, nb, e, r0, full_b);
 
   // pass 2: rewrite the survivors after the shared prefix at their new slots (in place:
   // destinations never exceed sources and chunks go in ascending order), collect moves
-  int mv_run = 0;
+  int mv_run = rebase ? r0 - e : 0;
   for (int c0 = r0; c0 < N; c0 += kAppThreads) {
     const int n = c0 + tid;
     int np = -1, id = 0, tk = 0, dp = 0, par = -1;
@@ -297,21 +412,21 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
         if (pp >= 0) {
           const int lp = pp - base;
           if (lp < e || lp >= n) par = -1;  // evicted (a parent always precedes its child)
-          else if (lp < r0) par = pp;
+          else if (lp < r0) par = nb + (lp - e);
           else {
             const int q = s.newpos[off + lp];
-            par = q >= 0 ? base_new + q : -1;
+            par = q >= 0 ? nb + q : -1;
           }
         }
       }
     }
-    const bool moved = np >= 0 && (np + e != n);
+    const bool moved = np >= 0 && (nb + np != base + n);
     int mtot;
     const int mrank = block_rank(moved, wave_cnt2, &mtot);
-    if (moved) s.moves[off + mv_run + mrank] = make_int2(base + n, base_new + np);
+    if (moved) s.moves[off + mv_run + mrank] = make_int2(base + n, nb + np);
     __syncthreads();  // every read of this chunk precedes its writes
     if (np >= 0) {
-      const size_t dst = off + base_new + np;
+      const size_t dst = off + nb + np;
       s.node_id[dst] = id;
       s.token[dst] = tk;
       s.depth[dst] = dp;
@@ -322,23 +437,26 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
     mv_run += mtot;
   }
 
-  // the shared run [e, r0): masks become full(b); its first survivor loses an evicted parent
-  if (n_live != b) {
-    for (int n = e + tid; n < r0; n += kAppThreads) s.mask[off + base + n] = full_b;
+  if (!rebase) {
+    // the shared run [e, r0) stays: masks become full(b); its first survivor loses an
+    // evicted parent
+    if (n_live != b) {
+      for (int n = e + tid; n < r0; n += kAppThreads) s.mask[off + base + n] = full_b;
+    }
+    if (tid == 0 && e > 0 && e < r0) s.parent[off + base + e] = -1;
   }
-  if (tid == 0 && e > 0 && e < r0) s.parent[off + base + e] = -1;
 
   // new leaves: rank j at logical (r0 - e) + alive_run + j
   if (tid < b) {
     const int lp = N - n_live + sp[tid];  // old logical slot of the parent leaf
     int par;
     if (lp < e) par = -1;
-    else if (lp < r0) par = base + lp;
+    else if (lp < r0) par = nb + (lp - e);
     else {
       const int q = s.newpos[off + lp];
-      par = q >= 0 ? base_new + q : -1;
+      par = q >= 0 ? nb + q : -1;
     }
-    const size_t dst = off + base_new + (r0 - e) + alive_run + tid;
+    const size_t dst = off + nb + (r0 - e) + alive_run + tid;
     s.node_id[dst] = h.next_id + tid;
     s.token[dst] = stok[tid];
     s.depth[dst] = d_new;
@@ -350,7 +468,7 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
   if (tid == 0) {
     TrieHdr nh;
     nh.n_nodes = n_new;
-    nh.base = base_new;
+    nh.base = nb;
     nh.n_live = b;
     nh.n_shared = (r0 - e) + full_cnt + (b == 1 ? 1 : 0);
     nh.leaf_depth = d_new;

@@ -48,7 +48,8 @@ class Run:
         self.cap = capacity or w.capacity
         self.scale = 1.0 / float(np.sqrt(w.head_dim))
         self.dec = B.TrieDecoder(w.n_tries, w.beam_width, self.cap, w.vocab, w.n_layers, w.n_q_heads,
-                                 w.n_kv_heads, w.head_dim, w.window, w.dtype, attn_impl)
+                                 w.n_kv_heads, w.head_dim, w.window, w.dtype, attn_impl,
+                                 gc_interval=w.gc_interval)
         self.plens = synth.prompt_lengths(w, seed)
         tokens = np.zeros((w.n_tries, int(self.plens.max())), np.int32)
         self.tries = []
@@ -60,7 +61,8 @@ class Run:
             self.dec.v_pool[t, :, :, :P] = to_dev(w, pv)
             if oracle:
                 self.tries.append(otrie.Trie(tok, synth.as_f32(w, pk[self.layers]),
-                                             synth.as_f32(w, pv[self.layers]), w.beam_width, w.window))
+                                             synth.as_f32(w, pv[self.layers]), w.beam_width, w.window,
+                                             w.gc_interval))
         self.dec.init_prompt(self.plens.tolist(), torch.from_numpy(tokens).cuda())
         self.pending = False
         self.step_no = 0

@@ -39,7 +39,7 @@ def test_library_exports_every_declared_symbol():
 
 def _desc(**kw):
     d = dict(n_tries=1, beam_width=8, capacity=4096, vocab=1000, n_layers=2, n_q_heads=8,
-             n_kv_heads=2, head_dim=128, window=0, dtype=B.TD_BF16, attn_impl=0, k_pool=0x10000,
+             n_kv_heads=2, head_dim=128, window=0, dtype=B.TD_BF16, attn_impl=0, gc_interval=1, k_pool=0x10000,
              v_pool=0x20000)
     d.update(kw)
     return B.TdDesc(**d)
@@ -51,6 +51,7 @@ def _desc(**kw):
     (dict(head_dim=80), "head_dim"), (dict(capacity=8), "capacity"), (dict(window=-1), "window"),
     (dict(dtype=7), "dtype"), (dict(k_pool=0), "k_pool"), (dict(v_pool=0x20004), "aligned"),
     (dict(attn_impl=2, dtype=B.TD_F32), "bf16"), (dict(vocab=2 ** 28, beam_width=16), "vocab"),
+    (dict(gc_interval=0), "gc_interval"), (dict(gc_interval=-3), "gc_interval"),
 ])
 def test_create_rejects_bad_descriptors(kw, frag):
     L = B.lib()

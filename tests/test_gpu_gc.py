@@ -1,0 +1,105 @@
+"""GPU parity with deferred garbage collection (interval g > 1, Alg 2) and pool re-packing.
+
+Between collections dead nodes keep their slots with mask 0 and must never be attended;
+collections run after the appends whose next position is a multiple of g, per trie.  A
+collection that leaves less room after the trie than the g - 1 appends before the next
+one needs re-packs the trie at slot 0 (all survivors and their K/V rows move down).  The
+expected states, selections and attention outputs come from the oracle run with the same
+g; the cases below reach both code paths of the append kernel (up to 1024 slots after the
+shared run, and more) with and without a collection, and re-packs with and without a
+shared run to relocate.  The steps at which re-packs happen were worked out from the
+oracle's node counts and are asserted through the state's base.
+"""
+import numpy as np
+import pytest
+
+import paper_2502_00085_amd.binding as B
+import synth
+from gpu_harness import Run, log
+
+pytestmark = pytest.mark.gpu
+
+
+def small(**kw):
+    base = dict(name="small", cfg_id=210, n_layers=2, n_q_heads=16, n_kv_heads=4, head_dim=128,
+                dtype="bf16", n_tries=1, prompt_min=100, prompt_max=100, beam_width=8, steps=20,
+                vocab=3000, window=0, alpha=1.0, qkv_std=1.0, logit_std=3.0, gc_interval=3)
+    base.update(kw)
+    return synth.Workload(**base)
+
+
+def run_case(w, seed=0, mode="scripted", impl=B.TD_ATTN_AUTO, capacity=None, repack_steps=()):
+    log(f"gc case T={w.n_tries} L={w.n_layers} Hq={w.n_q_heads} Hkv={w.n_kv_heads} d={w.head_dim} "
+        f"{w.dtype} P={w.prompt_min}-{w.prompt_max} b={w.beam_width} W={w.window} g={w.gc_interval} "
+        f"cap={capacity} mode={mode} impl={impl} seed={seed}")
+    r = Run(w, seed, attn_impl=impl, mode=mode, capacity=capacity)
+    prev_base = 0
+    repacks, dead_seen = [], 0
+    for s in range(1, w.steps + 1):
+        evicted = r.tries[0].evicted
+        errs, g = r.step()
+        assert not errs, "\n".join(errs[:10])
+        st = g["state"][0]
+        # base advances by the evicted slots, unless the trie was re-packed at slot 0
+        if st["base"] != prev_base + (r.tries[0].evicted - evicted):
+            assert st["base"] == 0, (s, st["base"], prev_base)
+            repacks.append(s)
+        prev_base = st["base"]
+        dead_seen = max(dead_seen, int(np.count_nonzero(st["mask"][:st["n_nodes"]] == 0)))
+    assert r.dec.status() == B.TD_OK
+    r.dec.close()
+    assert repacks == list(repack_steps), repacks
+    return dead_seen
+
+
+@pytest.mark.parametrize("impl", [B.TD_ATTN_MFMA, B.TD_ATTN_VALU])
+@pytest.mark.parametrize("mode", ["driven", "scripted"])
+def test_interval_three(impl, mode):
+    assert run_case(small(), seed=1, mode=mode, impl=impl) > 0
+
+
+def test_interval_fifteen_long_run():
+    assert run_case(small(gc_interval=15, steps=40), seed=2) > 0
+
+
+def test_fp32_interval_two():
+    run_case(synth.WORKLOADS["tiny"].replace(gc_interval=2), seed=3)
+
+
+def test_several_tries_collect_at_different_steps():
+    # ragged prompts: each trie's collections follow its own positions
+    run_case(small(n_tries=3, prompt_min=17, prompt_max=90, beam_width=4, steps=12, gc_interval=4), seed=4)
+
+
+def test_greedy_chain_has_nothing_to_collect():
+    assert run_case(small(beam_width=1, steps=10, gc_interval=5), seed=5, mode="driven") == 0
+
+
+def test_window_repack_with_shared_run_every_step():
+    # g = 1, window 40: base advances by the evicted slots until, at step 34, the trie is
+    # re-packed at slot 0 (36 shared slots relocated)
+    run_case(small(n_layers=1, n_q_heads=4, n_kv_heads=4, head_dim=64, beam_width=4, steps=40,
+                   window=40, gc_interval=1), seed=0, capacity=140, repack_steps=[34])
+
+
+def test_window_repack_deferred():
+    # g = 4, window 24: the first collection (step 4) evicts most of the prompt and
+    # re-packs, relocating a 20-slot shared run
+    run_case(small(n_layers=1, n_q_heads=4, n_kv_heads=4, head_dim=64, beam_width=8, steps=40,
+                   window=24, gc_interval=4), seed=0, capacity=130, repack_steps=[4])
+
+
+def test_more_than_a_block_of_slots_between_collections():
+    # b = 16, flat parents, g = 128: more than 1024 slots pile up after the shared run
+    # before the first collection (step 78), which then runs the chunked path
+    assert run_case(small(n_layers=1, n_q_heads=4, n_kv_heads=4, head_dim=64, beam_width=16,
+                          prompt_min=50, prompt_max=50, steps=80, alpha=0.0, gc_interval=128),
+                    seed=0, capacity=50 + 80 * 16) > 0
+
+
+def test_chunked_collection_repacks_shared_run():
+    # b = 32, window 100, g = 48: the collection at step 40 takes the chunked path, evicts
+    # 140 prompt slots, relocates the 60 shared ones and re-packs at slot 0
+    run_case(small(n_layers=1, n_q_heads=4, n_kv_heads=4, head_dim=64, beam_width=32,
+                   prompt_min=200, prompt_max=200, steps=60, window=100, alpha=0.0, gc_interval=48),
+             seed=0, capacity=1900, repack_steps=[40])
