@@ -69,6 +69,11 @@ def parse():
     p.add_argument("--attn-reps", type=int, default=32, help="launches in the attention timing graph")
     p.add_argument("--copy-ref-mib", type=int, default=0,
                    help="also run one plain device copy of this many MiB (reference for HBM counters)")
+    p.add_argument("--gc-interval", type=int, default=0,
+                   help="garbage-collection interval g (0: the workload's)")
+    p.add_argument("--input-period", type=int, default=0,
+                   help="draw q / k_new / v_new / logits for this many steps and reuse them in turn "
+                        "(0: fresh inputs every step); the trie growth is drawn for every step")
     return p.parse_args()
 
 
@@ -77,7 +82,7 @@ def log(*a):
 
 
 class Bench:
-    def __init__(self, w, steps, seed):
+    def __init__(self, w, steps, seed, input_period=0):
         import torch
         import paper_2502_00085_amd.binding as B
         self.B, self.torch, self.w, self.seed = B, torch, w, seed
@@ -86,7 +91,7 @@ class Bench:
         self.scale = 1.0 / float(np.sqrt(w.head_dim))
         t0 = time.time()
         self.dec = B.TrieDecoder(w.n_tries, w.beam_width, self.cap, w.vocab, w.n_layers, w.n_q_heads,
-                                 w.n_kv_heads, w.head_dim, w.window, w.dtype)
+                                 w.n_kv_heads, w.head_dim, w.window, w.dtype, gc_interval=w.gc_interval)
         self.plens = synth.prompt_lengths(w, seed)
         tokens = np.zeros((w.n_tries, int(self.plens.max())), np.int32)
         for t in range(w.n_tries):
@@ -99,11 +104,18 @@ class Bench:
         # per-step inputs, resident in HBM
         self.q, self.kn, self.vn, self.logits, self.par, self.tok = [], [], [], [], [], []
         for s in range(1, steps + 1):
-            q, kn, vn = synth.step_qkv(w, s, seed)
-            self.q.append(self.dev(q))
-            self.kn.append(self.dev(kn))
-            self.vn.append(self.dev(vn))
-            self.logits.append(torch.from_numpy(synth.step_logits(w, s, seed)).cuda())
+            if input_period > 0 and s > input_period:
+                j = (s - 1) % input_period
+                for a in (self.q, self.kn, self.vn, self.logits):
+                    a.append(a[j])
+            else:
+                q, kn, vn = synth.step_qkv(w, s, seed)
+                self.q.append(self.dev(q))
+                self.kn.append(self.dev(kn))
+                self.vn.append(self.dev(vn))
+                self.logits.append(torch.from_numpy(synth.step_logits(w, s, seed)).cuda())
+            if s % 100 == 0:
+                log(f"[bench] inputs of {s} steps drawn")
             par, tok = synth.step_script(w, s, seed)
             self.par.append(torch.from_numpy(par).cuda())
             self.tok.append(torch.from_numpy(tok).cuda())
@@ -125,12 +137,15 @@ class Bench:
         self.dec.init_prompt(self.plens.tolist(), self.tokens)
         self.torch.cuda.synchronize()
 
-    def step(self, i, stream, ev=None):
-        """Decode step i (0-based) through the C ABI with raw device pointers."""
+    def step(self, i, stream, ev=None, phases=None):
+        """Decode step i (0-based) through the C ABI with raw device pointers.  ev: kernel
+        events of the attention; phases: kernel events of every td_phase (index = phase)."""
         L, ctx = self.B.lib(), self.dec.ctx
         pend = i > 0
         if ev is not None:
-            self.B.td_set_attn_events(ctx, ev.start, ev.stop)
+            self.B.td_set_kernel_events(ctx, self.B.TD_PHASE_ATTN, ev.start, ev.stop)
+        for ph, e in enumerate(phases or ()):
+            self.B.td_set_kernel_events(ctx, ph, e.start, e.stop)
         st = L.trie_attn_decode(ctx, 0, self.w.n_layers, self.q[i].data_ptr(),
                                 self.kn[i].data_ptr() if pend else None,
                                 self.vn[i].data_ptr() if pend else None, self.out.data_ptr(),
@@ -156,12 +171,19 @@ class Bench:
         return np.array(n)
 
     def attended(self, t):
+        """Nodes the leaves attend to: on a live path (mask != 0; dead nodes awaiting a
+        collection are stored but never read for any beam) and inside the window."""
         st = self.dec.read_state(t)
         N, W = st["n_nodes"], self.w.window
-        if W <= 0:
-            return N
-        D = int(st["depth"][N - 1])
-        return int(np.count_nonzero(D - st["depth"][:N] < W))
+        live = st["mask"][:N] != 0
+        if W > 0:
+            live &= int(st["depth"][N - 1]) - st["depth"][:N] < W
+        return int(np.count_nonzero(live))
+
+    def collects(self, i):
+        """Whether the append of step i (0-based) collects garbage in any trie (Alg 2: the
+        position after the new leaves, P + i + 1, is a multiple of g)."""
+        return any((int(P) + i + 1) % self.w.gc_interval == 0 for P in self.plens)
 
 
 def gpu_bench(args, w, K):
@@ -174,7 +196,7 @@ def gpu_bench(args, w, K):
         torch.cuda.synchronize()
         log(f"[bench] reference copy: {args.copy_ref_mib} MiB read + {args.copy_ref_mib} MiB written")
         del src, dst
-    bench = Bench(w, K, args.seed)
+    bench = Bench(w, K, args.seed, args.input_period)
     stream = torch.cuda.current_stream().cuda_stream
     # warmup (eager)
     bench.init()
@@ -228,10 +250,61 @@ def gpu_bench(args, w, K):
     if status != 0:
         raise RuntimeError(f"device status {status} after the timed run")
     attn_graph_ms, attn_graph_nodes = attn_graph_time(bench, K, args.attn_reps)
+    phase_ms = phase_times(bench, K)
     nodes = bench.nodes_per_step(K)
+    collects = np.array([bench.collects(i) for i in range(K)])
     bench.dec.close()
     return dict(mode=mode, seconds=t1 - t0, eager_seconds=eager_s, attn_ms=attn_ms, nodes=nodes,
-                attn_graph_ms=attn_graph_ms, attn_graph_nodes=attn_graph_nodes)
+                attn_graph_ms=attn_graph_ms, attn_graph_nodes=attn_graph_nodes, phase_ms=phase_ms,
+                collects=collects)
+
+
+def phase_times(bench, K):
+    """[K][4] device ms of every td_phase at every step of an eager pass (kernel-timestamp
+    events; the row copy runs as a launch of its own here, so it can be timed)."""
+    import torch
+    stream = torch.cuda.current_stream().cuda_stream
+    evs = [[bench.B.KernelEvents() for _ in range(4)] for _ in range(K)]
+    bench.init()
+    for i in range(K):
+        bench.step(i, stream, phases=evs[i])
+    torch.cuda.synchronize()
+    t = np.array([[e.elapsed_ms() for e in row] for row in evs])
+    for row in evs:
+        for e in row:
+            e.close()
+    return t
+
+
+def gc_summary(w, ph, collects):
+    """Garbage-collection cost against the decode pass (the paper's Figure 4 comparison):
+    the decode pass is attention + top-b; a collection is the append kernel of a collecting
+    step (append, mask update and the collection itself) plus the copy of the moved rows
+    in the next step's attention call."""
+    K = len(ph)
+    us = ph * 1e3
+    dec = us[:, 0] + us[:, 2]
+    idx = np.nonzero(collects)[0]
+    gc = np.array([us[i, 3] + (us[i + 1, 1] if i + 1 < K else 0.0) for i in idx])
+    other = ~collects
+    tenth = max(1, K // 10)
+    out = {"interval": w.gc_interval, "collections": int(len(idx)), "steps": K,
+           "decode_pass_us": round(float(dec.mean()), 2),
+           "decode_pass_us_first_tenth": round(float(dec[:tenth].mean()), 2),
+           "decode_pass_us_last_tenth": round(float(dec[-tenth:].mean()), 2),
+           "append_us_without_collection": round(float(us[other, 3].mean()), 2) if other.any() else None,
+           "append_us_with_collection": round(float(us[idx, 3].mean()), 2) if len(idx) else None,
+           "row_copy_us_after_collection": round(float(np.mean([us[i + 1, 1] for i in idx if i + 1 < K])), 2)
+           if len(idx) and idx[0] + 1 < K else None}
+    if len(idx):
+        out["collection_us"] = round(float(gc.mean()), 2)
+        out["collection_us_first_tenth"] = round(float(gc[:max(1, len(gc) // 10)].mean()), 2)
+        out["collection_us_last_tenth"] = round(float(gc[-max(1, len(gc) // 10):].mean()), 2)
+        out["collection_over_decode_pass"] = round(float(gc.mean() / dec.mean()), 4)
+        out["collection_per_step_over_decode_pass"] = round(float(gc.sum() / K / dec.mean()), 4)
+    out["timing"] = ("kernel-timestamp events per phase over one eager pass of the timed steps "
+                     "(the row copy as a launch of its own)")
+    return out
 
 
 def attn_graph_time(bench, K, reps):
@@ -319,6 +392,8 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     w = synth.WORKLOADS[args.workload]
+    if args.gc_interval > 0:
+        w = w.replace(gc_interval=args.gc_interval)
     K = args.steps or w.steps
     if K > w.steps:
         raise SystemExit(f"--steps must be <= {w.steps} for {w.name}")
@@ -343,8 +418,8 @@ def main():
         "config": {"workload": w.name, "layers": w.n_layers, "q_heads": w.n_q_heads,
                    "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "tries": w.n_tries,
                    "prompt": [w.prompt_min, w.prompt_max], "beam_width": w.beam_width,
-                   "vocab": w.vocab, "window": w.window, "growth": f"scripted, parent rank ~ "
-                   f"(r+1)^-{w.alpha}", "launch": r["mode"]},
+                   "vocab": w.vocab, "window": w.window, "gc_interval": w.gc_interval,
+                   "growth": f"scripted, parent rank ~ (r+1)^-{w.alpha}", "launch": r["mode"]},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": "k_attn_mfma (trie_attn_decode, all layers, one launch)",
@@ -356,7 +431,10 @@ def main():
         "hbm_gbps_unique_kv_whole_step": round(float(kv_bytes.mean() / (ms_per_step / 1e3) / 1e9), 1),
         "eager_ms_per_step": round(r["eager_seconds"] * 1e3 / K, 5),
         "nodes_per_step_mean": round(float(r["nodes"].sum(axis=1).mean()), 1),
+        "gc": gc_summary(w, r["phase_ms"], r["collects"]),
     }
+    if args.input_period > 0:
+        out["data"] = f"synthetic, inputs of {args.input_period} steps reused in turn"
     if not args.no_cpu_baseline and not args.profile_only:
         out["cpu_baseline"] = cpu_baseline(w, args.seed, args.cpu_seconds)
     print(json.dumps(out), flush=True)

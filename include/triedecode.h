@@ -137,14 +137,25 @@ td_status trie_attn_decode(td_ctx* ctx, int32_t layer_begin, int32_t n_layers, c
                            const void* d_k_new, const void* d_v_new, void* d_out, float scale,
                            hipStream_t stream);
 
-/* Measurement hook, not part of the method: the next trie_attn_decode call (only that
- * one) launches its kernels with kernel-timestamp events (hipExtLaunchKernel): `start`
- * takes the dispatch time of its first kernel and `stop` the completion time of its last,
- * so hipEventElapsedTime(start, stop) is the call's device time as a kernel profiler
- * reports it, without the fences that hipEventRecord adds between launches.  Both events
- * are created by the caller (hipEventCreate) and must outlive that call; both NULL clears
- * a pending request.  One NULL and one non-NULL: TD_EINVAL. */
-td_status td_set_attn_events(td_ctx* ctx, hipEvent_t start, hipEvent_t stop);
+/* Phases of a decode step that td_set_kernel_events can time. */
+typedef enum {
+  TD_PHASE_ATTN = 0,    /* trie_attn_decode: the attention kernel (and its split combine)   */
+  TD_PHASE_MOVES = 1,   /* trie_attn_decode: the copy of the K/V rows a compaction moved     */
+  TD_PHASE_TOPB = 2,    /* beam_logsoftmax_topk: both of its kernels                          */
+  TD_PHASE_APPEND = 3   /* trie_append_prune: append, mask update and any collection         */
+} td_phase;
+
+/* Measurement hook, not part of the method: the next call that runs `phase` launches that
+ * phase's kernels with kernel-timestamp events (hipExtLaunchKernel): `start` takes the
+ * dispatch time of its first kernel and `stop` the completion time of its last, so
+ * hipEventElapsedTime(start, stop) is the phase's device time as a kernel profiler
+ * reports it, without the fences that hipEventRecord adds between launches.  Timing
+ * TD_PHASE_MOVES makes that trie_attn_decode copy the moved rows in launches of their own
+ * (otherwise the attention kernel may copy them itself); when the call has no rows to
+ * copy, both events are recorded on the stream at the same point (elapsed time 0).  Both
+ * events are created by the caller (hipEventCreate) and must outlive the call; both NULL
+ * clears a pending request.  A bad phase, or one NULL and one non-NULL event: TD_EINVAL. */
+td_status td_set_kernel_events(td_ctx* ctx, int32_t phase, hipEvent_t start, hipEvent_t stop);
 
 /* Alg 1 / Alg 2 top-b with cumulative log-probability scores.  For every trie, row r <
  * n_live:  lse_r = fp32 rounding of the fp64 log-sum-exp of the row;  per candidate

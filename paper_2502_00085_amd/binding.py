@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtriedeco
 TD_OK, TD_EINVAL, TD_ECAPACITY, TD_EHIP, TD_ESTATE, TD_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 TD_F32, TD_BF16 = 0, 1
 TD_ATTN_AUTO, TD_ATTN_VALU, TD_ATTN_MFMA = 0, 1, 2
+TD_PHASE_ATTN, TD_PHASE_MOVES, TD_PHASE_TOPB, TD_PHASE_APPEND = 0, 1, 2, 3
 
 
 class TdDesc(ctypes.Structure):
@@ -70,14 +71,14 @@ def lib() -> ctypes.CDLL:
         L.td_read_state.argtypes = [vp, i32, ctypes.POINTER(TdState)]
         L.td_load_state.argtypes = [vp, i32, ctypes.POINTER(TdState)]
         L.td_get_status.argtypes = [vp]
-        L.td_set_attn_events.argtypes = [vp, vp, vp]
+        L.td_set_kernel_events.argtypes = [vp, i32, vp, vp]
         L.td_error_string.argtypes = [vp]
         L.td_error_string.restype = ctypes.c_char_p
         L.td_status_name.argtypes = [i32]
         L.td_status_name.restype = ctypes.c_char_p
         for name in ("td_create", "td_destroy", "td_init_prompt", "trie_attn_decode",
                      "beam_logsoftmax_topk", "trie_append_prune", "td_read_state", "td_load_state",
-                     "td_get_status", "td_set_attn_events"):
+                     "td_get_status", "td_set_kernel_events"):
             getattr(L, name).restype = ctypes.c_int32
         _lib = L
     return _lib
@@ -157,14 +158,14 @@ def trie_attn_decode(ctx, dims: Dims, layer_begin: int, n_layers: int, q, k_new,
         _ptr(v_new, tdt, nk, "v_new"), _ptr(out, tdt, nq, "out"), float(scale), _stream(stream)))
 
 
-def td_set_attn_events(ctx, start, stop):
-    """Kernel-timestamp events for the next trie_attn_decode call (raw hipEvent_t handles,
-    e.g. KernelEvents.start / .stop; None, None clears)."""
-    _check(ctx, lib().td_set_attn_events(ctx, start, stop))
+def td_set_kernel_events(ctx, phase, start, stop):
+    """Kernel-timestamp events for the next run of `phase` (TD_PHASE_*; raw hipEvent_t
+    handles, e.g. KernelEvents.start / .stop; None, None clears)."""
+    _check(ctx, lib().td_set_kernel_events(ctx, int(phase), start, stop))
 
 
 class KernelEvents:
-    """A pair of plain HIP events (hipEventCreate) for td_set_attn_events; elapsed_ms()
+    """A pair of plain HIP events (hipEventCreate) for td_set_kernel_events; elapsed_ms()
     synchronises on the stop event."""
 
     _hip = None

@@ -23,8 +23,8 @@ struct td_ctx {
                                        //   device header; tells which appends collect)
   int32_t* d_plen = nullptr;
   int splits_override = 0;             // TD_ATTN_SPLITS (tuning): WGs per attention unit
-  hipEvent_t attn_ev0 = nullptr;       // td_set_attn_events: kernel-timestamp events of the
-  hipEvent_t attn_ev1 = nullptr;       //   next trie_attn_decode launch
+  hipEvent_t ev[4][2] = {};             // td_set_kernel_events: per td_phase, the
+                                       //   kernel-timestamp events of its next run
   std::vector<void*> allocs;
   std::string err;
 };
@@ -230,9 +230,14 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;
   a.xcd_group = a.row_blocks > 1 && ((long)s.T * n_layers * s.Hkv * a.splits) % 8 == 0 ? 1 : 0;
+  hipEvent_t ev0 = c->ev[TD_PHASE_ATTN][0], ev1 = c->ev[TD_PHASE_ATTN][1];
+  hipEvent_t mv0 = c->ev[TD_PHASE_MOVES][0], mv1 = c->ev[TD_PHASE_MOVES][1];
+  c->ev[TD_PHASE_ATTN][0] = c->ev[TD_PHASE_ATTN][1] = nullptr;
+  c->ev[TD_PHASE_MOVES][0] = c->ev[TD_PHASE_MOVES][1] = nullptr;
   // Rows moved by the last compaction are copied before the layer's first attention: by
   // the attention WGs themselves when each owns a whole (layer, KV head) and every layer
-  // of the call is still due, else by a copy launch per due layer range.
+  // of the call is still due (unless the copy is being timed), else by a copy launch per
+  // due layer range.
   a.moves = 0;
   std::vector<std::pair<int, int>> due;
   if (c->pending && c->moves_pending) {
@@ -246,17 +251,21 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
       due.emplace_back(l, j - l);
       l = j;
     }
-    if (due.size() == 1 && due[0].second == n_layers && a.splits == 1 && a.row_blocks == 1) {
+    if (due.size() == 1 && due[0].second == n_layers && a.splits == 1 && a.row_blocks == 1 && !mv0) {
       a.moves = 1;
       due.clear();
     }
   }
-  hipEvent_t ev0 = c->attn_ev0, ev1 = c->attn_ev1;
-  c->attn_ev0 = c->attn_ev1 = nullptr;
   hipEvent_t main_ev1 = a.splits > 1 ? nullptr : ev1;
   hipError_t e = hipSuccess;
-  for (const auto& d : due)
-    if (e == hipSuccess) e = td::launch_move_rows(s, d.first, d.second, st);
+  for (size_t i = 0; i < due.size(); ++i)
+    if (e == hipSuccess)
+      e = td::launch_move_rows(s, due[i].first, due[i].second, st, i == 0 ? mv0 : nullptr,
+                               i + 1 == due.size() ? mv1 : nullptr);
+  if (mv0 && due.empty()) {
+    if (e == hipSuccess) e = hipEventRecord(mv0, st);
+    if (e == hipSuccess) e = hipEventRecord(mv1, st);
+  }
   if (e == hipSuccess) e = mfma ? td::launch_attn_mfma(s, a, st, ev0, main_ev1) : td::launch_attn_valu(s, a, st, ev0, main_ev1);
   if (e == hipSuccess && a.splits > 1) e = td::launch_attn_combine(s, a, rpb, st, nullptr, ev1);
   if (e != hipSuccess) return hip_fail(c, e, "trie_attn_decode launch");
@@ -269,12 +278,13 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   return TD_OK;
 }
 
-td_status td_set_attn_events(td_ctx* c, hipEvent_t start, hipEvent_t stop) {
+td_status td_set_kernel_events(td_ctx* c, int32_t phase, hipEvent_t start, hipEvent_t stop) {
   if (!c) return TD_EINVAL;
   c->err.clear();
+  if (phase < TD_PHASE_ATTN || phase > TD_PHASE_APPEND) return fail(c, TD_EINVAL, "bad phase %d", phase);
   if ((start == nullptr) != (stop == nullptr)) return fail(c, TD_EINVAL, "pass both events or neither");
-  c->attn_ev0 = start;
-  c->attn_ev1 = stop;
+  c->ev[phase][0] = start;
+  c->ev[phase][1] = stop;
   return TD_OK;
 }
 
@@ -291,7 +301,9 @@ td_status beam_logsoftmax_topk(td_ctx* c, const float* d_logits, int32_t* d_sel_
     return fail(c, TD_EINVAL, "pair_parent / pair_token / pair_score must be given together");
   hipError_t e = td::launch_logsoftmax_topk(c->dev, d_logits, d_sel_parent, d_sel_token, d_sel_score,
                                             d_sel_logprob, d_lse, d_pair_parent, d_pair_token,
-                                            d_pair_score, st);
+                                            d_pair_score, st, c->ev[TD_PHASE_TOPB][0],
+                                            c->ev[TD_PHASE_TOPB][1]);
+  c->ev[TD_PHASE_TOPB][0] = c->ev[TD_PHASE_TOPB][1] = nullptr;
   if (e != hipSuccess) return hip_fail(c, e, "beam_logsoftmax_topk launch");
   return TD_OK;
 }
@@ -304,7 +316,9 @@ td_status trie_append_prune(td_ctx* c, const int32_t* d_sel_parent, const int32_
     return fail(c, TD_EINVAL, "sel_parent / sel_token / sel_score are required");
   if (c->pending)
     return fail(c, TD_ESTATE, "trie_attn_decode has not stored the leaves' K/V for every layer");
-  hipError_t e = td::launch_append_prune(c->dev, d_sel_parent, d_sel_token, d_sel_score, st);
+  hipError_t e = td::launch_append_prune(c->dev, d_sel_parent, d_sel_token, d_sel_score, st,
+                                         c->ev[TD_PHASE_APPEND][0], c->ev[TD_PHASE_APPEND][1]);
+  c->ev[TD_PHASE_APPEND][0] = c->ev[TD_PHASE_APPEND][1] = nullptr;
   if (e != hipSuccess) return hip_fail(c, e, "trie_append_prune launch");
   // rows move only where this append collects (Alg 2: the next position is a multiple of g)
   bool collects = false;

@@ -73,8 +73,8 @@ struct AttnArgs {
 
 hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const int32_t* d_tokens,
                               int stride, hipStream_t st);
-// The attention launchers take optional kernel-timestamp events (hipExtLaunchKernel):
-// ev0 records the dispatch of the launched kernel, ev1 its completion (null = none).
+// The launchers take optional kernel-timestamp events (hipExtLaunchKernel): ev0 records
+// the dispatch of the first launched kernel, ev1 the completion of the last (null = none).
 hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
                             hipEvent_t ev1);
 hipError_t launch_attn_valu(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
@@ -87,12 +87,14 @@ int attn_choose_splits(const DevState& s, int n_layers, int row_blocks);
 hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_t* sel_parent,
                                   int32_t* sel_token, float* sel_score, float* sel_logprob,
                                   float* lse, const int32_t* pair_parent, const int32_t* pair_token,
-                                  float* pair_score, hipStream_t st);
+                                  float* pair_score, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1);
 int topb_max_chunk_lists();  // limit of b * lse_chunks per trie
 hipError_t launch_append_prune(const DevState& s, const int32_t* sel_parent,
-                               const int32_t* sel_token, const float* sel_score, hipStream_t st);
+                               const int32_t* sel_token, const float* sel_score, hipStream_t st,
+                               hipEvent_t ev0, hipEvent_t ev1);
 // Copies the K/V rows moved by the last compaction for layers [layer_begin, +n_layers).
-hipError_t launch_move_rows(const DevState& s, int layer_begin, int n_layers, hipStream_t st);
+hipError_t launch_move_rows(const DevState& s, int layer_begin, int n_layers, hipStream_t st,
+                            hipEvent_t ev0, hipEvent_t ev1);
 
 // ---------------------------------------------------------------------------------------
 // small device helpers

@@ -479,12 +479,14 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
 hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_t* sel_parent,
                                   int32_t* sel_token, float* sel_score, float* sel_logprob,
                                   float* lse, const int32_t* pair_parent, const int32_t* pair_token,
-                                  float* pair_score, hipStream_t st) {
-  hipLaunchKernelGGL(k_topb_chunk, dim3(s.lse_chunks, s.b, s.T), dim3(kChunkThreads), 0, st, s, logits);
+                                  float* pair_score, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+  hipExtLaunchKernelGGL(k_topb_chunk, dim3(s.lse_chunks, s.b, s.T), dim3(kChunkThreads), 0, st, ev0,
+                        nullptr, 0, s, logits);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_topb_final, dim3(s.T), dim3(kFinalThreads), 0, st, s, logits, sel_parent,
-                     sel_token, sel_score, sel_logprob, lse, pair_parent, pair_token, pair_score);
+  hipExtLaunchKernelGGL(k_topb_final, dim3(s.T), dim3(kFinalThreads), 0, st, nullptr, ev1, 0, s, logits,
+                        sel_parent, sel_token, sel_score, sel_logprob, lse, pair_parent, pair_token,
+                        pair_score);
   return hipGetLastError();
 }
 

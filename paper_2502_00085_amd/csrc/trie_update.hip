@@ -523,15 +523,17 @@ hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const in
 }
 
 hipError_t launch_append_prune(const DevState& s, const int32_t* sel_parent,
-                               const int32_t* sel_token, const float* sel_score, hipStream_t st) {
-  hipLaunchKernelGGL(k_append_prune, dim3(s.T), dim3(kAppThreads), 0, st, s, sel_parent, sel_token,
-                     sel_score);
+                               const int32_t* sel_token, const float* sel_score, hipStream_t st,
+                               hipEvent_t ev0, hipEvent_t ev1) {
+  hipExtLaunchKernelGGL(k_append_prune, dim3(s.T), dim3(kAppThreads), 0, st, ev0, ev1, 0, s, sel_parent,
+                        sel_token, sel_score);
   return hipGetLastError();
 }
 
-hipError_t launch_move_rows(const DevState& s, int layer_begin, int n_layers, hipStream_t st) {
-  hipLaunchKernelGGL(k_move_rows, dim3(s.T * n_layers * s.Hkv * 2), dim3(kMoveThreads), kMoveLdsBytes, st,
-                     s, layer_begin, n_layers);
+hipError_t launch_move_rows(const DevState& s, int layer_begin, int n_layers, hipStream_t st,
+                            hipEvent_t ev0, hipEvent_t ev1) {
+  hipExtLaunchKernelGGL(k_move_rows, dim3(s.T * n_layers * s.Hkv * 2), dim3(kMoveThreads), kMoveLdsBytes,
+                        st, ev0, ev1, 0, s, layer_begin, n_layers);
   return hipGetLastError();
 }
 

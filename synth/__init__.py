@@ -94,6 +94,10 @@ WORKLOADS: Dict[str, Workload] = {
                            4096, 1.0, 1.0, 3.0),
     "stress": Workload("stress", 5, 32, 32, 8, 128, "bf16", 16, 256, 1024, 16, 512, 128256, 0, 0.0,
                        1.0, 3.0),
+    # the garbage-collection overhead experiment (Section 5.3, Figure 4): Llama-3.1-8B shape,
+    # 30 beams, 1000 decode steps, collection every 15 positions
+    "llama8b_b30": Workload("llama8b_b30", 6, 32, 32, 8, 128, "bf16", 1, 2048, 2048, 30, 1000,
+                                128256, 0, 1.0, 1.0, 3.0, 15),
 }
 
 

@@ -40,10 +40,10 @@ class Run:
     """One decode run of workload ``w`` on the GPU with a CPU oracle beside it."""
 
     def __init__(self, w, seed=0, layers=None, attn_impl=0, capacity=None, mode="scripted",
-                 oracle=True):
+                 oracle=True, phase_events=False):
         import torch
         import paper_2502_00085_amd.binding as B
-        self.w, self.seed, self.mode = w, seed, mode
+        self.w, self.seed, self.mode, self.phase_events = w, seed, mode, phase_events
         self.layers = list(range(w.n_layers)) if layers is None else list(layers)
         self.cap = capacity or w.capacity
         self.scale = 1.0 / float(np.sqrt(w.head_dim))
@@ -82,6 +82,12 @@ class Run:
         out = torch.full_like(qd, 7.0)  # garbage: every row must be written
         knd = to_dev(w, kn) if self.pending else None
         vnd = to_dev(w, vn) if self.pending else None
+        evs = []
+        if self.phase_events:
+            import paper_2502_00085_amd.binding as B
+            evs = [B.KernelEvents() for _ in range(4)]
+            for ph, e in enumerate(evs):
+                B.td_set_kernel_events(dec.ctx, ph, e.start, e.stop)
         dec.attn_decode(0, w.n_layers, qd, knd, vnd, out, self.scale)
         ld = torch.from_numpy(np.ascontiguousarray(logits)).cuda()
         i32 = dict(dtype=torch.int32, device="cuda")
@@ -104,6 +110,10 @@ class Run:
         if ps is not None:
             res["pair_score"] = ps.cpu().numpy()
         res["state"] = [dec.read_state(t) for t in range(T)]
+        if evs:
+            res["phase_ms"] = [e.elapsed_ms() for e in evs]
+            for e in evs:
+                e.close()
         return res
 
     def step(self, check=True, check_attn=True):

@@ -71,7 +71,7 @@ def test_null_context_is_rejected_by_every_call():
     assert L.td_get_status(None) == B.TD_EINVAL
     assert L.td_read_state(None, 0, None) == B.TD_EINVAL
     assert L.td_load_state(None, 0, None) == B.TD_EINVAL
-    assert L.td_set_attn_events(None, None, None) == B.TD_EINVAL
+    assert L.td_set_kernel_events(None, B.TD_PHASE_ATTN, None, None) == B.TD_EINVAL
     assert L.td_status_name(B.TD_ECAPACITY) == b"TD_ECAPACITY"
 
 

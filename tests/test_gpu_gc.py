@@ -103,3 +103,19 @@ def test_chunked_collection_repacks_shared_run():
     run_case(small(n_layers=1, n_q_heads=4, n_kv_heads=4, head_dim=64, beam_width=32,
                    prompt_min=200, prompt_max=200, steps=60, window=100, alpha=0.0, gc_interval=48),
              seed=0, capacity=1900, repack_steps=[40])
+
+
+def test_phase_events_keep_results():
+    """Timing every phase (td_set_kernel_events) moves the row copy out of the attention
+    kernel into launches of its own; results must not change, and every phase reports a
+    device time (0 for the copy when a step moved nothing)."""
+    w = small(gc_interval=1, steps=8)
+    log(f"phase events case b={w.beam_width} g={w.gc_interval}")
+    r = Run(w, seed=6, phase_events=True)
+    for _ in range(w.steps):
+        errs, g = r.step()
+        assert not errs, "\n".join(errs[:10])
+        attn, moves, topb, append = g["phase_ms"]
+        assert attn > 0 and topb > 0 and append > 0 and moves >= 0, g["phase_ms"]
+    assert r.dec.status() == B.TD_OK
+    r.dec.close()
