@@ -75,7 +75,7 @@ typedef struct {
   int32_t n_tries;      /* T >= 1: independent requests decoded together                 */
   int32_t beam_width;   /* b in [1, 64] (one bit per beam in a 64-bit ancestor mask)      */
   int32_t capacity;     /* node slots per trie (>= every prompt length + b)              */
-  int32_t vocab;        /* V >= b, b * ceil(V / 4096) <= 4096                             */
+  int32_t vocab;        /* V >= b, b * ceil(V / 4096) <= 2048                             */
   int32_t n_layers;     /* L >= 1                                                         */
   int32_t n_q_heads;    /* Hq, a multiple of Hkv                                          */
   int32_t n_kv_heads;   /* Hkv >= 1                                                       */

@@ -14,7 +14,8 @@
 //                 sum of exp(x - max), and the largest logit (key, with its index) of each
 //                 of its 16 sub-chunks (the 256 logits of one wave: 4 runs of 64);
 //   k_topb_final  grid (tries): every row's lse from its chunk partials; the score of each
-//                 sub-chunk's largest logit; a bound L at most the b-th largest of those;
+//                 sub-chunk's largest logit; a bound L at most the b-th largest of those
+//                 (the b-th largest of the maxima of disjoint groups of sub-chunks);
 //                 the "hot" sub-chunks whose largest score reaches L, read again; the exact
 //                 top-b of their logits scoring at or above L.
 // Exactness: within a row s is a non-decreasing function of x (fl32 subtraction and
@@ -36,7 +37,8 @@ constexpr int kFinalThreads = 1024;
 constexpr int kFinalWaves = kFinalThreads / 64;
 constexpr int kCandMax = 4096;
 constexpr int kSub = kChunkWaves;                     // sub-chunks (waves) per chunk
-constexpr int kSubPer = 4;                            // sub-chunk maxima per thread
+constexpr int kPer = 16;                              // entries per lane held in registers
+constexpr int kMaxEntries = 2048;                     // entries per wave (b * chunks per row)
 static_assert(kSub == kFinalThreads / 64, "the final merge maps sub-chunk w of a chunk to wave w");
 
 // Order-preserving maps of floats to unsigned integers: raw (-0 below +0) for logits, so
@@ -199,10 +201,11 @@ __global__ __launch_bounds__(kChunkThreads) void k_topb_chunk(DevState s, const 
   const uint64_t km = wave_max_u64(k1);
   const uint64_t km2 = wave_max_u64(k1 == km ? k2 : k1);
   const size_t list = ((size_t)t * b + r) * s.lse_chunks + c;
+  const size_t lists = (size_t)s.T * b * s.lse_chunks;
   if (lane == 0) {
     wm[wave] = m;
-    s.topk_keys[list * kSub + wave] = km;  // 0 when the wave holds no logit
-    s.topk_keys[s.topk_half + list * kSub + wave] = km2;
+    s.topk_keys[wave * lists + list] = km;  // 0 when the wave holds no logit
+    s.topk_keys[s.topk_half + wave * lists + list] = km2;
   }
   __syncthreads();
   m = wm[0];
@@ -279,28 +282,27 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __shared__ uint64_t cand[kCandMax], cand_x[kCandMax];
   __shared__ __align__(16) uint32_t wt[kFinalWaves];
+  __shared__ uint32_t tmax[kFinalThreads];
   __shared__ int wsum[kFinalWaves];
   __shared__ uint64_t best_k[kMaxBeam], best_c[kMaxBeam];
   __shared__ float row_lse[kMaxBeam], row_score[kMaxBeam];
   __shared__ int ncand, nhot;
   __shared__ int hot[kCandMax];
   const float* lrow = logits + (size_t)t * b * V;
-  const uint64_t* smax = s.topk_keys + (size_t)t * b * nch * kSub;  // [row][chunk][sub]
-  const int per_row = nch * kSub;
+  // Entry j of wave w is sub-chunk w of (row j / nch, chunk j % nch): every wave covers
+  // every row, and its entries are contiguous (coalesced loads).
+  const size_t lists = (size_t)s.T * b * nch;
+  const uint64_t* ekey = s.topk_keys + wave * lists + (size_t)t * b * nch;  // largest keys
+  const uint64_t* ekey2 = ekey + s.topk_half;                                 // second largest
+  const int e_all = b * nch;
 
-  // Independent loads first: the sub-chunk maxima of every row (rows >= n_live are dropped
-  // once n_live is known), pair logits, leaf scores, every row's lse, then n_live.
-  const uint64_t* ssec = smax + s.topk_half;  // second largest keys, same layout
-  // Sub-chunk i of a round is read by wave i % 16 (kSub = kFinalWaves): every wave sees
-  // sub-chunk w of every chunk of every row, so each wave's maximum is drawn from all
-  // rows and the bound below stays tight however the beams' scores differ.
-  auto sub_index = [&](int i0, int q) { return i0 + (q * 64 + lane) * kSub + wave; };
-  uint64_t km0[kSubPer], ks0[kSubPer];
+  // Independent loads first: the first batch of this wave's entries (rows >= n_live are
+  // dropped once n_live is known), pair logits, leaf scores, every row's lse, then n_live.
+  uint64_t km0[kPer];
 #pragma unroll
-  for (int q = 0; q < kSubPer; ++q) {
-    const int i = sub_index(0, q);
-    km0[q] = i < b * per_row ? smax[i] : 0;
-    ks0[q] = i < b * per_row ? ssec[i] : 0;
+  for (int q = 0; q < kPer; ++q) {
+    const int j = q * 64 + lane;
+    km0[q] = j < e_all ? ekey[j] : 0;
   }
   // pairs: the last b threads (their wave has no row below; the dependent logit load
   // waits there)
@@ -320,63 +322,92 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
   const int n_live = s.hdr[t].n_live;
   if (threadIdx.x == 0) ncand = nhot = 0;
   __syncthreads();
-  const int nsub = n_live * per_row;
-  const float inv_per_row = 1.0f / (float)per_row;
+  const int e_live = n_live * nch;
+  const float inv_nch = 1.0f / (float)nch;
 
-  // Bound L (ord of a score): with b <= 16, the b-th largest of the 16 waves' maxima of
-  // the sub-chunk maximum scores (16 distinct sub-chunks reach their wave's maximum, and
-  // each wave covers every row);
-  // otherwise the largest of the waves' exact b-th largest.  Rounds of kSubPer *
-  // kFinalThreads sub-chunks.
-  uint32_t o[kSubPer];
-  uint32_t L = 0, lmax = 0;
-  for (int i0 = 0; i0 < nsub; i0 += kSubPer * kFinalThreads) {
+  // score ord of an entry's largest logit (0: no entry / no logit); the first batch is
+  // kept in registers, a second one (more than 1024 entries per wave) is read again later
+  auto entry_ord = [&](int j, uint64_t km) -> uint32_t {
+    const int r = div_small(j, inv_nch);
+    return km != 0 ? ord_score(score_only(key_x(km), row_lse[r], row_score[r])) : 0u;
+  };
+  uint32_t o0[kPer];
+  uint32_t lmax = 0;
 #pragma unroll
-    for (int q = 0; q < kSubPer; ++q) {
-      const int i = sub_index(i0, q);
-      const uint64_t km = i >= nsub ? 0 : i0 == 0 ? km0[q] : smax[i];
-      const int r = div_small(i, inv_per_row);
-      o[q] = km != 0 ? ord_score(score_only(key_x(km), row_lse[r], row_score[r])) : 0u;
-      lmax = o[q] > lmax ? o[q] : lmax;
-    }
-    if (b > kFinalWaves) {
-      const uint32_t tw = wave_bth32<kSubPer>(o, b);
-      L = tw > L ? tw : L;
-    }
+  for (int q = 0; q < kPer; ++q) {
+    const int j = q * 64 + lane;
+    o0[q] = entry_ord(j, j < e_live ? km0[q] : 0);
+    lmax = o0[q] > lmax ? o0[q] : lmax;
   }
-  if (b <= kFinalWaves) L = __ockl_wfred_max_u32(lmax);
-  if (lane == 0) wt[wave] = L;
-  __syncthreads();
+  for (int j = kPer * 64 + lane; j < e_live; j += 64) {
+    const uint32_t oj = entry_ord(j, ekey[j]);
+    lmax = oj > lmax ? oj : lmax;
+  }
+
+  // Bound L (ord of a score): the b-th largest of the maxima of disjoint groups of
+  // entries, so that at least b distinct sub-chunks score >= L.  With b <= 16 the groups
+  // are the 16 waves (each covers every row); otherwise the 1024 threads, whose maxima
+  // one wave selects from exactly.
+  uint32_t L;
   if (b <= kFinalWaves) {
+    L = __ockl_wfred_max_u32(lmax);
+    if (lane == 0) wt[wave] = L;
+    __syncthreads();
     L = wave_bth_of16(wt, b);
   } else {
-    L = 0;
-    for (int w = 0; w < kFinalWaves; ++w) L = wt[w] > L ? wt[w] : L;
-  }
-  // hot sub-chunks: largest score >= L (at least b of them).  A hot sub-chunk whose second
-  // largest logit also scores >= L is read again in full (its logits scoring >= L are the
-  // candidates); otherwise its largest logit is its only candidate.
-  for (int i0 = 0; i0 < nsub; i0 += kSubPer * kFinalThreads) {
-    int id[kSubPer];
-    bool take[kSubPer], direct[kSubPer];
-    uint64_t ks[kSubPer], kx[kSubPer];
+    tmax[threadIdx.x] = lmax;
+    __syncthreads();
+    if (wave == 0) {
+      uint32_t v[kFinalWaves];
 #pragma unroll
-    for (int q = 0; q < kSubPer; ++q) {
-      const int i = sub_index(i0, q);
-      const uint64_t km = i >= nsub ? 0 : i0 == 0 ? km0[q] : smax[i];
-      const uint64_t k2 = i >= nsub ? 0 : i0 == 0 ? ks0[q] : ssec[i];
-      const int r = div_small(i, inv_per_row);
-      const float sc = km != 0 ? score_only(key_x(km), row_lse[r], row_score[r]) : 0.0f;
-      const bool hotq = i < nsub && km != 0 && ord_score(sc) >= L;
+      for (int j = 0; j < kFinalWaves; ++j) v[j] = tmax[j * 64 + lane];
+      L = wave_bth32<kFinalWaves>(v, b);
+      if (lane == 0) wt[0] = L;
+    }
+    __syncthreads();
+    L = wt[0];
+  }
+  // hot entries: largest score >= L (at least b of them).  A hot sub-chunk whose second
+  // largest logit also scores >= L is read again in full (its logits scoring >= L are the
+  // candidates); otherwise its largest logit is its only candidate.  Groups of 4 entries
+  // per lane; a group without a hot entry in the wave is skipped.
+  for (int g0 = 0; g0 * 64 < e_live; g0 += 4) {
+    uint32_t og[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = (g0 + q) * 64 + lane;
+      uint32_t v = 0;
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) v = (g0 + q == u) ? o0[u] : v;
+      og[q] = g0 + q < kPer ? v : (j < e_live ? entry_ord(j, ekey[j]) : 0u);
+    }
+    bool any = false;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) any |= og[q] >= L && og[q] != 0u;
+    if (__ballot(any) == 0) continue;
+    int id[4];
+    bool take[4], direct[4];
+    uint64_t ks[4], kx[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = (g0 + q) * 64 + lane;
+      const bool hotq = og[q] >= L && og[q] != 0u;
+      uint64_t km = 0, k2 = 0;
+      if (hotq) {
+        km = ekey[j];
+        k2 = ekey2[j];
+      }
+      const int r = div_small(j, inv_nch);
+      const float sc = score_only(key_x(km), row_lse[r], row_score[r]);
       const bool again = hotq && k2 != 0 && ord_score(score_only(key_x(k2), row_lse[r], row_score[r])) >= L;
-      id[q] = i;
+      id[q] = j * kSub + wave;  // (row * nch + chunk) * 16 + sub-chunk
       take[q] = again;
       direct[q] = hotq && !again;
       ks[q] = s_key(sc, key_flat(km));
       kx[q] = km;
     }
-    wave_append<kSubPer, int, int>(id, nullptr, take, hot, nullptr, kCandMax, &nhot);
-    wave_append<kSubPer, uint64_t, uint64_t>(ks, kx, direct, cand, cand_x, kCandMax, &ncand);
+    wave_append<4, int, int>(id, nullptr, take, hot, nullptr, kCandMax, &nhot);
+    wave_append<4, uint64_t, uint64_t>(ks, kx, direct, cand, cand_x, kCandMax, &ncand);
   }
   __syncthreads();
   const int n_hot = nhot;
@@ -384,7 +415,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     // one wave per hot sub-chunk: its 4 runs of 64 logits; keep those scoring >= L
     for (int h = wave; h < n_hot; h += kFinalWaves) {
       const int i = hot[h];
-      const int r = i / per_row, c = (i / kSub) % nch, sw = i % kSub;
+      const int r = i / (nch * kSub), c = (i / kSub) % nch, sw = i % kSub;
       float xs[kChunkPer];
 #pragma unroll
       for (int q = 0; q < kChunkPer; ++q) {
@@ -490,6 +521,6 @@ hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_
   return hipGetLastError();
 }
 
-int topb_max_chunk_lists() { return kCandMax; }
+int topb_max_chunk_lists() { return kMaxEntries; }
 
 }  // namespace td
