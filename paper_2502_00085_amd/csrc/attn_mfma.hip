@@ -39,6 +39,7 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kRows = 32;
 constexpr float kNegBig = -1.0e30f;
+constexpr int kRegMoves = 128;  // moved rows whose sources each wave keeps in registers
 
 template <int D, int NW>
 struct MfmaCfg {
@@ -51,8 +52,11 @@ struct MfmaCfg {
   static constexpr int OS = D + 4;            // LDS row stride of the O merge buffer (floats)
   static constexpr int V_LDS = NW * 2 * TILE_BYTES;  // one K and one V tile per wave
   static constexpr int O_LDS = NW * kRows * OS * 4 + 3 * NW * kRows * 4 + 2 * kRows * 4;
-  static constexpr int MOVE_LDS = 8192;    // staging of compaction moves, past the tiles
-  static constexpr int LDS = V_LDS + MOVE_LDS > O_LDS ? V_LDS + MOVE_LDS : O_LDS;
+  // past both the tiles and the merge buffers: the moved rows' sources and staged copies
+  static constexpr int MOVE0 = V_LDS > O_LDS ? V_LDS : O_LDS;
+  static constexpr int LDS = 160 * 1024 - 256;  // (the rest: the window search's scratch)
+  static constexpr int MOVE_LDS = LDS - MOVE0;
+  static constexpr int ROW_BYTES = 4 * D;      // K + V of one node row
 };
 
 // Physical 16-byte chunk of logical chunk c of tile row r: rows are rotated by whole
@@ -83,13 +87,41 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   const int n0 = lo + u.split * per, n1 = min(N, n0 + per);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
-  // Rows moved by the last compaction (this WG is the only one of its layer and head) are
-  // copied by the whole block right after the first tile's loads are issued, so their
-  // round trips overlap that tile's (see the main loop).  A first tile that itself
-  // reaches a moved slot is issued after the copy instead.  The leaf store at the end,
-  // whose slots may be sources of moves, follows the merge's block barriers.
+  // Rows moved by the last compaction (this WG is the only one of its layer and head):
+  // their destinations are the consecutive slots first_moved, first_moved + 1, ...  This
+  // call reads them at their sources (still intact) and writes them to their destinations
+  // once every read of the call is done.  Up to kRegMoves rows: each wave keeps the source
+  // table in registers (lane j: rows j and j + 64) and the rows are staged in LDS by loads
+  // issued with the first tile, then written after the main loop.  More: the table goes to
+  // LDS (one block barrier) and the rows are copied at the end.  More than that table
+  // holds: copied first.  The leaf store, whose slots may be sources of moves, follows.
   const int nmoves = a.moves ? s.n_moves[u.t] : 0;
   const int first_moved = nmoves > 0 ? s.moves[(size_t)u.t * s.cap].y - base : INT_MAX;
+  // The pending leaves' rows of a WG whose range holds them are staged the same way (from
+  // k_new / v_new), ahead of the moved rows, unless the moved rows are copied through the
+  // same LDS at the start or the end.
+  const bool leaves_here = a.kv_pending && n0 < n1 && n1 > N - n_live;
+  const int leaf_chunks = n_live * 2 * C::CPR;
+  const int leaf_bytes = (leaf_chunks + 63) / 64 * 1024;
+  const int stage_chunks = nmoves * 2 * C::CPR;        // 16-byte chunks of the moved rows
+  const bool staged = nmoves > 0 && nmoves <= kRegMoves &&
+                      (leaves_here ? leaf_bytes : 0) + (stage_chunks + 63) / 64 * 1024 <= C::MOVE_LDS;
+  int* msrc = reinterpret_cast<int*>(lds + C::MOVE0);  // [nmoves] source slot - base (late)
+  const bool late_copy = nmoves > 0 && !staged && nmoves * 4 <= C::MOVE_LDS;
+  const bool leaves_staged = leaves_here && (nmoves == 0 || staged) && leaf_bytes <= C::MOVE_LDS;
+  unsigned char* lstage = lds + C::MOVE0;                                  // staged leaf rows
+  unsigned char* mstage = lds + C::MOVE0 + (leaves_staged ? leaf_bytes : 0);  // staged moved rows
+  int mt0 = 0, mt1 = 0;  // register source table (staged)
+  if (staged) {
+    const int2* mv = s.moves + (size_t)u.t * s.cap;
+    mt0 = lane < nmoves ? mv[lane].x - base : 0;
+    mt1 = lane + 64 < nmoves ? mv[lane + 64].x - base : 0;
+  }
+  auto table = [&](int k) -> int {  // source of moved row k < kRegMoves (all lanes active)
+    const int a0 = __builtin_amdgcn_ds_bpermute((k & 63) << 2, mt0);
+    const int a1 = __builtin_amdgcn_ds_bpermute((k & 63) << 2, mt1);
+    return k < 64 ? a0 : a1;
+  };
   // pending leaf rows are read from k_new / v_new by the main loop and stored into the
   // pool after it (by every WG whose node range holds them: identical data)
   const int leaf0 = a.kv_pending ? N - n_live : N;
@@ -140,16 +172,30 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   for (int t = 0; t < C::KSTEPS; ++t) kread[t] = col * (2 * D) + (hh * (C::CPR / 2) + t + col) % C::CPR * 16;
 
   // K and V rows of a tile -> the wave's LDS buffers (coalesced 16-byte direct loads; the
-  // pending leaves' rows come from k_new / v_new); in the range's last, partial tile, rows
-  // past the end are clamped to its last node and masked out later
+  // pending leaves' rows come from k_new / v_new, moved rows from their sources); in the
+  // range's last, partial tile, rows past the end are clamped to its last node and masked
+  // out later
+  const int moved_end = staged || late_copy ? first_moved + nmoves : INT_MIN;
   auto issue = [&](int tile) {
     const int tb = n0 + tile * 32;
     const bool full = tb + 32 <= n1;
+    const bool any_moved = tb + 32 > first_moved && tb < moved_end;  // wave-uniform
 #pragma unroll
     for (int i = 0; i < C::VINST; ++i) {
       const int nv = full ? tb + vrow[i] : min(tb + vrow[i], n1 - 1);
       const bool leaf = nv >= leaf0;
-      const size_t kr = leaf ? (size_t)(nv - leaf0) * leaf_stride : (size_t)nv * D;
+      int src = nv;
+      if (any_moved) {
+        const bool mvd = nv >= first_moved && nv < moved_end;
+        const int k = mvd ? nv - first_moved : 0;
+        if (staged) {
+          const int t = table(k);
+          src = mvd ? t : nv;
+        } else if (mvd) {
+          src = msrc[k];
+        }
+      }
+      const size_t kr = leaf ? (size_t)(nv - leaf0) * leaf_stride : (size_t)src * D;
       const __bf16* ks = (leaf ? knew : kpool) + kr + koff[i];
       const __bf16* vs = (leaf ? vnew : vpool) + kr + voff[i];
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)ks,
@@ -160,12 +206,33 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   };
 
   const float scale = a.scale_log2;
-  // first tile of every wave, unless it reaches a moved slot (then after the copy)
+  // first tile of every wave before the source table / the copy, unless it reaches a moved
+  // slot (the table and the copy's staging lie past the tile buffers)
   const bool early = my_tiles > 0 && min(n0 + wave * 32 + 32, n1) <= first_moved;
   if (early) issue(wave);
-  if (nmoves > 0) {
-    // staged past the tile buffers (the first tiles are landing in them)
-    move_rows_block<__bf16>(s, u.t, lab, u.g, reinterpret_cast<uint4*>(lds + C::V_LDS), C::MOVE_LDS / 16);
+  if (leaves_staged) {
+    for (int i = wave; i * 64 < leaf_chunks; i += NW) {
+      const int q = min(i * 64 + lane, leaf_chunks - 1);
+      const int j = q / (2 * C::CPR), c = q % (2 * C::CPR);
+      const __bf16* src = (c < C::CPR ? knew : vnew) + (size_t)j * leaf_stride + (c % C::CPR) * 8;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                       (__attribute__((address_space(3))) void*)(lstage + i * 1024), 16, 0, 0);
+    }
+  }
+  if (staged) {
+    // load i of the staging writes chunks 64 i .. 64 i + 63: row q / (2 CPR), K then V
+    for (int i = wave; i * 64 < stage_chunks; i += NW) {
+      const int q = min(i * 64 + lane, stage_chunks - 1);
+      const int k = q / (2 * C::CPR), c = q % (2 * C::CPR);
+      const __bf16* src = (c < C::CPR ? kpool : vpool) + (size_t)table(k) * D + (c % C::CPR) * 8;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                       (__attribute__((address_space(3))) void*)(mstage + i * 1024), 16, 0, 0);
+    }
+  } else if (late_copy) {
+    for (int k = threadIdx.x; k < nmoves; k += NW * 64) msrc[k] = s.moves[(size_t)u.t * s.cap + k].x - base;
+    __syncthreads();
+  } else if (nmoves > 0) {
+    move_rows_block<__bf16>(s, u.t, lab, u.g, reinterpret_cast<uint4*>(lds + C::MOVE0), C::MOVE_LDS / 16);
   }
   if (my_tiles > 0 && !early) issue(wave);
   // (the query rows load while the first tile is in flight)
@@ -277,7 +344,28 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
 
   // ---- merge the waves of this WG: every wave stores its state, one combine ----
   lsum += __shfl_xor(lsum, 32);
-  __syncthreads();  // the tile buffers are reused below
+  __builtin_amdgcn_s_waitcnt(kWaitVmAll);  // (staged moved rows of a wave without tiles)
+  __syncthreads();  // the tile buffers are reused below; every read of the pool is done
+  if (leaves_staged) {
+    // the staged leaf rows into the pool, for later calls (past the merge buffers)
+    __bf16* kdst = static_cast<__bf16*>(s.k_pool) + pool_row(s, u.t, lab, u.g, base + N - n_live);
+    __bf16* vdst = static_cast<__bf16*>(s.v_pool) + pool_row(s, u.t, lab, u.g, base + N - n_live);
+    for (int q = threadIdx.x; q < leaf_chunks; q += NW * 64) {
+      const int j = q / (2 * C::CPR), c = q % (2 * C::CPR);
+      __bf16* dst = (c < C::CPR ? kdst : vdst) + (size_t)j * D + (c % C::CPR) * 8;
+      *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(lstage + q * 16);
+    }
+  }
+  if (staged) {
+    // the staged moved rows to their destinations (past the merge buffers: no conflict)
+    __bf16* kdst = static_cast<__bf16*>(s.k_pool) + pool_row(s, u.t, lab, u.g, base + first_moved);
+    __bf16* vdst = static_cast<__bf16*>(s.v_pool) + pool_row(s, u.t, lab, u.g, base + first_moved);
+    for (int q = threadIdx.x; q < stage_chunks; q += NW * 64) {
+      const int k = q / (2 * C::CPR), c = q % (2 * C::CPR);
+      __bf16* dst = (c < C::CPR ? kdst : vdst) + (size_t)k * D + (c % C::CPR) * 8;
+      *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(mstage + q * 16);
+    }
+  }
   float* obuf = reinterpret_cast<float*>(lds);  // [NW][kRows][OS] unscaled O of each wave
   float* smx = obuf + NW * kRows * C::OS;        // [NW][kRows] running max
   float* ssum = smx + NW * kRows;                // [NW][kRows] weight sum
@@ -351,9 +439,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     }
   }
 
-  // the pending leaves' rows into the pool, for later calls (this call read them from
-  // k_new / v_new)
-  if (a.kv_pending && n0 < n1 && n1 > N - n_live) store_leaf_kv<__bf16>(s, a, u, base, N, n_live);
+  // the moved rows to their new slots (every read of this call is done), then the pending
+  // leaves' rows into the pool, for later calls (this call read them from k_new / v_new)
+  if (late_copy) {
+    __syncthreads();  // the merge buffers are free
+    move_rows_block<__bf16>(s, u.t, lab, u.g, reinterpret_cast<uint4*>(lds), C::LDS / 16);
+  }
+  if (leaves_here && !leaves_staged) store_leaf_kv<__bf16>(s, a, u, base, N, n_live);
 }
 
 constexpr int kNW = 8;

@@ -119,3 +119,36 @@ def test_phase_events_keep_results():
         assert attn > 0 and topb > 0 and append > 0 and moves >= 0, g["phase_ms"]
     assert r.dec.status() == B.TD_OK
     r.dec.close()
+
+
+@pytest.fixture
+def one_split(monkeypatch):
+    # one WG per (trie, layer, KV head): the attention kernel copies the moved rows itself
+    monkeypatch.setenv("TD_ATTN_SPLITS", "1")
+
+
+@pytest.mark.parametrize("impl", [B.TD_ATTN_MFMA, B.TD_ATTN_VALU])
+@pytest.mark.parametrize("g", [1, 3])
+def test_attention_copies_moved_rows(one_split, impl, g):
+    # 8 beams x 4 query heads per KV head = one 32-row block: the moved rows are read at
+    # their old slots, staged in LDS and written after the call's reads (matrix-core
+    # kernel; the vector-ALU kernel copies them first)
+    run_case(small(gc_interval=g, steps=12), seed=7, impl=impl)
+
+
+def test_attention_copies_a_large_repack_last(one_split):
+    # window 2100 over a 2500-token prompt in 2504 slots: the step-2 collection re-packs the
+    # trie at slot 0 and moves 2100 rows, more than fit staged in LDS, so the next call
+    # copies them at its end
+    run_case(small(n_layers=1, n_q_heads=4, n_kv_heads=4, head_dim=64, beam_width=4, prompt_min=2500,
+                   prompt_max=2500, steps=4, window=2100, gc_interval=1), seed=0, capacity=2504,
+             repack_steps=[2])
+
+
+def test_attention_copies_a_huge_repack_first(one_split):
+    # window 6400 over a 7000-token prompt in 7004 slots, head_dim 128: the step-2 re-pack
+    # moves about 6400 rows, more than the kernel's source table holds, so the next call
+    # copies them before its reads
+    run_case(small(n_layers=1, n_q_heads=4, n_kv_heads=4, head_dim=128, beam_width=4, prompt_min=7000,
+                   prompt_max=7000, steps=4, window=6400, gc_interval=1), seed=0, capacity=7004,
+             repack_steps=[2])
