@@ -32,6 +32,16 @@ class TdDesc(ctypes.Structure):
                 ("k_pool", ctypes.c_void_p), ("v_pool", ctypes.c_void_p)]
 
 
+class BbsDesc(ctypes.Structure):
+    _fields_ = [("n_requests", ctypes.c_int32), ("beam_width", ctypes.c_int32),
+                ("capacity", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("n_layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("window", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("attn_impl", ctypes.c_int32),
+                ("k_cache", ctypes.c_void_p * 2), ("v_cache", ctypes.c_void_p * 2)]
+
+
 class TdState(ctypes.Structure):
     _fields_ = [("n_nodes", ctypes.c_int32), ("n_live", ctypes.c_int32), ("base", ctypes.c_int32),
                 ("n_shared", ctypes.c_int32), ("next_id", ctypes.c_int32),
@@ -76,9 +86,22 @@ def lib() -> ctypes.CDLL:
         L.td_error_string.restype = ctypes.c_char_p
         L.td_status_name.argtypes = [i32]
         L.td_status_name.restype = ctypes.c_char_p
+        L.bbs_create.argtypes = [ctypes.POINTER(BbsDesc), ctypes.POINTER(vp)]
+        L.bbs_destroy.argtypes = [vp]
+        L.bbs_init_prompt.argtypes = [vp, ctypes.POINTER(i32), vp, i32, vp]
+        L.batch_beam_attn_decode.argtypes = [vp, i32, i32, vp, vp, vp, vp, f32, vp]
+        L.batch_beam_logsoftmax_topk.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.batch_beam_reorder.argtypes = [vp, vp, vp, vp, vp]
+        L.bbs_current_cache.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp)]
+        L.bbs_read_beams.argtypes = [vp, i32, vp, vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+        L.bbs_get_status.argtypes = [vp]
+        L.bbs_error_string.argtypes = [vp]
+        L.bbs_error_string.restype = ctypes.c_char_p
         for name in ("td_create", "td_destroy", "td_init_prompt", "trie_attn_decode",
                      "beam_logsoftmax_topk", "trie_append_prune", "td_read_state", "td_load_state",
-                     "td_get_status", "td_set_kernel_events"):
+                     "td_get_status", "td_set_kernel_events", "bbs_create", "bbs_destroy",
+                     "bbs_init_prompt", "batch_beam_attn_decode", "batch_beam_logsoftmax_topk",
+                     "batch_beam_reorder", "bbs_current_cache", "bbs_read_beams", "bbs_get_status"):
             getattr(L, name).restype = ctypes.c_int32
         _lib = L
     return _lib
@@ -314,3 +337,106 @@ class TrieDecoder:
 
     def status(self):
         return td_get_status(self.ctx)
+
+
+# ---------------------------------------------------------------------------------------------
+# batch-based beam search baseline (Alg 1): batchbeam.h
+# ---------------------------------------------------------------------------------------------
+def _bcheck(ctx, st: int):
+    if st != TD_OK:
+        raise TdError(st, lib().bbs_error_string(ctx).decode())
+
+
+class BatchBeamDecoder:
+    """One baseline context plus its two caller-owned cache buffers (torch tensors)."""
+
+    def __init__(self, n_requests, beam_width, capacity, vocab, n_layers, n_q_heads, n_kv_heads,
+                 head_dim, window=0, dtype="bf16", attn_impl=TD_ATTN_AUTO, device="cuda"):
+        import torch
+        self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
+        shape = (n_requests, beam_width, n_layers, n_kv_heads, capacity, head_dim)
+        self.k_cache = [torch.zeros(shape, dtype=self.tdtype, device=device) for _ in range(2)]
+        self.v_cache = [torch.zeros(shape, dtype=self.tdtype, device=device) for _ in range(2)]
+        d = BbsDesc()
+        d.n_requests, d.beam_width, d.capacity, d.vocab = n_requests, beam_width, capacity, vocab
+        d.n_layers, d.n_q_heads, d.n_kv_heads, d.head_dim = n_layers, n_q_heads, n_kv_heads, head_dim
+        d.window, d.dtype, d.attn_impl = window, TD_BF16 if dtype == "bf16" else TD_F32, attn_impl
+        for i in range(2):
+            d.k_cache[i] = self.k_cache[i].data_ptr()
+            d.v_cache[i] = self.v_cache[i].data_ptr()
+        self.desc = d
+        self.T, self.b, self.cap, self.V = n_requests, beam_width, capacity, vocab
+        self.L, self.Hq, self.Hkv, self.D = n_layers, n_q_heads, n_kv_heads, head_dim
+        self.ctx = ctypes.c_void_p()
+        st = lib().bbs_create(ctypes.byref(d), ctypes.byref(self.ctx))
+        if st != TD_OK:
+            raise TdError(st, lib().bbs_error_string(None).decode())
+
+    def close(self):
+        if self.ctx is not None and self.ctx.value is not None:
+            lib().bbs_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def prompt_cache(self):
+        """(k, v) views of buffer 0, where the prompt goes (beam 0 of each request)."""
+        return self.k_cache[0], self.v_cache[0]
+
+    def current_cache(self):
+        k, v = ctypes.c_void_p(), ctypes.c_void_p()
+        _bcheck(self.ctx, lib().bbs_current_cache(self.ctx, ctypes.byref(k), ctypes.byref(v)))
+        i = 0 if k.value == self.k_cache[0].data_ptr() else 1
+        return self.k_cache[i], self.v_cache[i]
+
+    def init_prompt(self, prompt_len, tokens, stream=None):
+        import torch
+        plen = np.ascontiguousarray(np.asarray(prompt_len, dtype=np.int32))
+        if tokens.dim() != 2 or tokens.shape[0] != plen.size:
+            raise ValueError("tokens must be [T][stride]")
+        _ptr(tokens, torch.int32, name="tokens")
+        _bcheck(self.ctx, lib().bbs_init_prompt(self.ctx, plen.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                                tokens.data_ptr(), int(tokens.shape[1]), _stream(stream)))
+
+    def attn_decode(self, layer_begin, n_layers, q, k_new, v_new, out, scale, stream=None):
+        nq = n_layers * self.T * self.b * self.Hq * self.D
+        nk = n_layers * self.T * self.b * self.Hkv * self.D
+        _bcheck(self.ctx, lib().batch_beam_attn_decode(
+            self.ctx, int(layer_begin), int(n_layers), _ptr(q, self.tdtype, nq, "q"),
+            _ptr(k_new, self.tdtype, nk, "k_new"), _ptr(v_new, self.tdtype, nk, "v_new"),
+            _ptr(out, self.tdtype, nq, "out"), float(scale), _stream(stream)))
+
+    def logsoftmax_topk(self, logits, sel_parent, sel_token, sel_score, sel_logprob, lse=None,
+                        pair_parent=None, pair_token=None, pair_score=None, stream=None):
+        import torch
+        tb = self.T * self.b
+        _bcheck(self.ctx, lib().batch_beam_logsoftmax_topk(
+            self.ctx, _ptr(logits, torch.float32, tb * self.V, "logits"),
+            _ptr(sel_parent, torch.int32, tb, "sel_parent"), _ptr(sel_token, torch.int32, tb, "sel_token"),
+            _ptr(sel_score, torch.float32, tb, "sel_score"), _ptr(sel_logprob, torch.float32, tb, "sel_logprob"),
+            _ptr(lse, torch.float32, tb, "lse"), _ptr(pair_parent, torch.int32, tb, "pair_parent"),
+            _ptr(pair_token, torch.int32, tb, "pair_token"), _ptr(pair_score, torch.float32, tb, "pair_score"),
+            _stream(stream)))
+
+    def reorder(self, sel_parent, sel_token, sel_score, stream=None):
+        import torch
+        tb = self.T * self.b
+        _bcheck(self.ctx, lib().batch_beam_reorder(
+            self.ctx, _ptr(sel_parent, torch.int32, tb, "sel_parent"), _ptr(sel_token, torch.int32, tb, "sel_token"),
+            _ptr(sel_score, torch.float32, tb, "sel_score"), _stream(stream)))
+
+    def read_beams(self, request=0) -> dict:
+        toks = np.zeros((self.b, self.cap), np.int32)
+        sc = np.zeros(self.b, np.float32)
+        length, n_live = ctypes.c_int32(), ctypes.c_int32()
+        _bcheck(self.ctx, lib().bbs_read_beams(self.ctx, int(request), toks.ctypes.data, sc.ctypes.data,
+                                                ctypes.byref(length), ctypes.byref(n_live)))
+        n, nl = length.value, n_live.value
+        return {"length": n, "n_live": nl, "tokens": toks[:nl, :n].copy(), "scores": sc[:nl].copy()}
+
+    def status(self):
+        return int(lib().bbs_get_status(self.ctx))

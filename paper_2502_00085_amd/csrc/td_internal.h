@@ -48,6 +48,26 @@ struct DevState {
   int lse_chunks, attn_part_floats, attn_pairs_max;
 };
 
+// Batch-based beam search baseline (Alg 1): state of the cache reorder.  `req` holds one
+// header per request (n_nodes = sequence length, n_live = live beams); `chain` one header
+// per beam (a single-chain trie with one leaf, read by the attention kernels).
+struct BbsState {
+  int T, b, cap, V, L, Hkv, D, esz;
+  TrieHdr* req;          // [T]
+  TrieHdr* chain;        // [T][b]
+  float* score;          // [T][b] beam scores
+  const int32_t* tok_src;  // [T][b][cap] token histories, current buffer
+  int32_t* tok_dst;        //   and the other one
+  const void* k_src;     // [T][b][L][Hkv][cap][d] current cache buffers
+  const void* v_src;
+  void* k_dst;           // the other buffers (gather destination)
+  void* v_dst;
+  int32_t* ok;           // [T] 1 if the request's selection is valid
+  int32_t* status;
+};
+hipError_t launch_bbs_reorder(const BbsState& s, const int32_t* sel_parent, const int32_t* sel_token,
+                              const float* sel_score, hipStream_t st);
+
 // selection / log-softmax geometry
 constexpr int kLseChunk = 4096;      // logits of one row per WG in the chunk pass
 constexpr int kMaxBeam = 64;

@@ -175,3 +175,107 @@ def compare(w, s, t, nl, layers, g, ref, check_attn=True):
         if not np.array_equal(gs["leaf_score"].view(np.uint32), rs["leaf_score"].view(np.uint32)):
             errs.append(f"{tag}: leaf_score bits differ")
     return errs
+
+
+class BatchRun:
+    """One decode run of workload ``w`` through the GPU batch beam search baseline with the
+    oracle's batch beam search (Alg 1) beside it."""
+
+    def __init__(self, w, seed=0, attn_impl=0, capacity=None, mode="scripted"):
+        import torch
+        import paper_2502_00085_amd.binding as B
+        import oracle.batch_beam as obb
+        self.w, self.seed, self.mode = w, seed, mode
+        self.cap = capacity or (w.prompt_max + w.steps + 1)
+        self.scale = 1.0 / float(np.sqrt(w.head_dim))
+        self.dec = B.BatchBeamDecoder(w.n_tries, w.beam_width, self.cap, w.vocab, w.n_layers, w.n_q_heads,
+                                      w.n_kv_heads, w.head_dim, w.window, w.dtype, attn_impl)
+        self.plens = synth.prompt_lengths(w, seed)
+        tokens = np.zeros((w.n_tries, int(self.plens.max())), np.int32)
+        kc, vc = self.dec.prompt_cache()
+        self.bbs = []
+        for t in range(w.n_tries):
+            P = int(self.plens[t])
+            tok, pk, pv = synth.prompt(w, t, P, seed)
+            tokens[t, :P] = tok
+            kc[t, 0, :, :, :P] = to_dev(w, pk)
+            vc[t, 0, :, :, :P] = to_dev(w, pv)
+            self.bbs.append(obb.BatchBeamSearch(tok, synth.as_f32(w, pk), synth.as_f32(w, pv), w.beam_width,
+                                                w.window))
+        self.dec.init_prompt(self.plens.tolist(), torch.from_numpy(tokens).cuda())
+        self.pending = False
+        self.step_no = 0
+
+    def step(self):
+        import torch
+        import oracle.beam as obeam
+        self.step_no += 1
+        s, w, dec = self.step_no, self.w, self.dec
+        T, b = w.n_tries, w.beam_width
+        q, kn, vn = synth.step_qkv(w, s, self.seed)
+        logits = synth.step_logits(w, s, self.seed)
+        par, tok = synth.step_script(w, s, self.seed) if self.mode == "scripted" else (None, None)
+        qd = to_dev(w, q)
+        out = torch.full_like(qd, 7.0)
+        dec.attn_decode(0, w.n_layers, qd, to_dev(w, kn) if self.pending else None,
+                        to_dev(w, vn) if self.pending else None, out, self.scale)
+        ld = torch.from_numpy(np.ascontiguousarray(logits)).cuda()
+        i32 = dict(dtype=torch.int32, device="cuda")
+        f32 = dict(dtype=torch.float32, device="cuda")
+        sp, st = torch.empty((T, b), **i32), torch.empty((T, b), **i32)
+        ss, sl, lse = (torch.empty((T, b), **f32) for _ in range(3))
+        if self.mode == "scripted":
+            pp, pt = torch.from_numpy(par).cuda(), torch.from_numpy(tok).cuda()
+            ps = torch.empty((T, b), **f32)
+            dec.logsoftmax_topk(ld, sp, st, ss, sl, lse, pp, pt, ps)
+            dec.reorder(pp, pt, ps)
+        else:
+            dec.logsoftmax_topk(ld, sp, st, ss, sl, lse)
+            dec.reorder(sp, st, ss)
+        torch.cuda.synchronize()
+        self.pending = True
+        og = from_dev(out)
+        g = {"sel_parent": sp.cpu().numpy(), "sel_token": st.cpu().numpy(), "sel_score": ss.cpu().numpy(),
+             "sel_logprob": sl.cpu().numpy(), "lse": lse.cpu().numpy(), "o": og}
+        errs = []
+        qf, knf, vnf = (synth.as_f32(w, a) for a in (q, kn, vn))
+        for t, bb in enumerate(self.bbs):
+            tag = f"step {s} request {t}"
+            nl = len(bb.beams)
+            if s > 1:
+                bb.write_kv(knf[:, t, :nl], vnf[:, t, :nl])
+            o_ref = bb.attention(qf[:, t, :nl], self.scale)
+            err = float(np.max(np.abs(og[:, t, :nl] - o_ref)))
+            mx = float(np.max(np.abs(o_ref)))
+            if w.dtype == "f32":
+                if not err <= ATTN_F32_TOL:
+                    errs.append(f"{tag}: attention max err {err:.3e}")
+            elif not (err <= ATTN_ABS_TOL and err <= ATTN_REL_TOL * mx + 1e-6):
+                errs.append(f"{tag}: attention max err {err:.3e} (max |o_ref| {mx:.3e})")
+            if nl < b and np.any(og[:, t, nl:] != 0):
+                errs.append(f"{tag}: output rows of beams >= n_live are not zero")
+            ref = obeam.select(logits[t, :nl], bb.scores, b)
+            for k in ("sel_parent", "sel_token"):
+                if not np.array_equal(g[k][t], ref[k]):
+                    errs.append(f"{tag}: {k} {g[k][t].tolist()} != {ref[k].tolist()}")
+            for k in ("sel_score", "sel_logprob"):
+                if not np.array_equal(g[k][t].view(np.uint32), ref[k].view(np.uint32)):
+                    errs.append(f"{tag}: {k} bits differ")
+            if not np.array_equal(g["lse"][t][:nl].view(np.uint32), ref["lse"].view(np.uint32)):
+                errs.append(f"{tag}: lse bits differ")
+            if self.mode == "scripted":
+                sc, _ = obeam.pair_scores(logits[t, :nl], ref["lse"], bb.scores, par[t], tok[t])
+                bb.advance(par[t], tok[t], sc)
+            else:
+                bb.advance(ref["sel_parent"], ref["sel_token"], ref["sel_score"])
+            gb = dec.read_beams(t)
+            if gb["n_live"] != len(bb.beams) or gb["length"] != len(bb.beams[0].tokens):
+                errs.append(f"{tag}: beams {gb['n_live']} x {gb['length']} != {len(bb.beams)} x "
+                            f"{len(bb.beams[0].tokens)}")
+            else:
+                want = np.array([seq.tokens for seq in bb.beams], dtype=np.int32)
+                if not np.array_equal(gb["tokens"], want):
+                    errs.append(f"{tag}: token histories differ")
+                if not np.array_equal(gb["scores"].view(np.uint32), bb.scores.view(np.uint32)):
+                    errs.append(f"{tag}: beam scores differ")
+        return errs, g

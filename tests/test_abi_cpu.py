@@ -10,13 +10,16 @@ import pytest
 import paper_2502_00085_amd.binding as B
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "triedecode.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if h.endswith(".h")]
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"^\s*(?:td_status|const char\*)\s+(\w+)\s*\(", text, flags=re.M)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names.update(re.findall(r"^\s*(?:td_status|const char\*)\s+(\w+)\s*\(", text, flags=re.M))
+    return sorted(names)
 
 
 def test_header_declares_the_three_hot_calls():
@@ -73,6 +76,55 @@ def test_null_context_is_rejected_by_every_call():
     assert L.td_load_state(None, 0, None) == B.TD_EINVAL
     assert L.td_set_kernel_events(None, B.TD_PHASE_ATTN, None, None) == B.TD_EINVAL
     assert L.td_status_name(B.TD_ECAPACITY) == b"TD_ECAPACITY"
+
+
+def test_header_declares_the_batch_beam_baseline():
+    names = declared_functions()
+    for n in ("bbs_create", "bbs_destroy", "bbs_init_prompt", "batch_beam_attn_decode",
+              "batch_beam_logsoftmax_topk", "batch_beam_reorder", "bbs_current_cache", "bbs_read_beams",
+              "bbs_get_status", "bbs_error_string"):
+        assert n in names
+
+
+def _bdesc(**kw):
+    d = B.BbsDesc()
+    vals = dict(n_requests=1, beam_width=8, capacity=4096, vocab=1000, n_layers=2, n_q_heads=8,
+                n_kv_heads=2, head_dim=128, window=0, dtype=B.TD_BF16, attn_impl=0)
+    vals.update({k: v for k, v in kw.items() if k not in ("k_cache", "v_cache")})
+    for k, v in vals.items():
+        setattr(d, k, v)
+    kc, vc = kw.get("k_cache", (0x10000, 0x30000)), kw.get("v_cache", (0x20000, 0x40000))
+    for i in range(2):
+        d.k_cache[i], d.v_cache[i] = kc[i], vc[i]
+    return d
+
+
+@pytest.mark.parametrize("kw,frag", [
+    (dict(n_requests=0), "n_requests"), (dict(beam_width=65), "beam_width"), (dict(vocab=4), "vocab"),
+    (dict(n_q_heads=6, n_kv_heads=4), "n_q_heads"), (dict(head_dim=80), "head_dim"),
+    (dict(capacity=1), "capacity"), (dict(window=-1), "window"), (dict(dtype=7), "dtype"),
+    (dict(k_cache=(0x10000, 0)), "k_cache"), (dict(v_cache=(0x20000, 0x40004)), "aligned"),
+    (dict(attn_impl=2, dtype=B.TD_F32), "bf16"),
+])
+def test_batch_beam_create_rejects_bad_descriptors(kw, frag):
+    L = B.lib()
+    ctx = ctypes.c_void_p()
+    st = L.bbs_create(ctypes.byref(_bdesc(**kw)), ctypes.byref(ctx))
+    assert st in (B.TD_EINVAL, B.TD_EUNSUPPORTED)
+    assert ctx.value is None
+    assert frag in L.bbs_error_string(None).decode()
+
+
+def test_batch_beam_null_context_is_rejected():
+    L = B.lib()
+    assert L.bbs_destroy(None) == B.TD_EINVAL
+    assert L.bbs_init_prompt(None, None, None, 0, None) == B.TD_EINVAL
+    assert L.batch_beam_attn_decode(None, 0, 1, None, None, None, None, 1.0, None) == B.TD_EINVAL
+    assert L.batch_beam_logsoftmax_topk(None, *([None] * 10)) == B.TD_EINVAL
+    assert L.batch_beam_reorder(None, None, None, None, None) == B.TD_EINVAL
+    assert L.bbs_current_cache(None, None, None) == B.TD_EINVAL
+    assert L.bbs_read_beams(None, 0, None, None, None, None) == B.TD_EINVAL
+    assert L.bbs_get_status(None) == B.TD_EINVAL
 
 
 def test_valid_descriptor_without_a_gpu_reports_a_hip_error():
