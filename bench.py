@@ -69,6 +69,8 @@ def parse():
     p.add_argument("--attn-reps", type=int, default=32, help="launches in the attention timing graph")
     p.add_argument("--copy-ref-mib", type=int, default=0,
                    help="also run one plain device copy of this many MiB (reference for HBM counters)")
+    p.add_argument("--no-batch-baseline", action="store_true",
+                   help="skip the batch-based beam search baseline on the same inputs")
     p.add_argument("--gc-interval", type=int, default=0,
                    help="garbage-collection interval g (0: the workload's)")
     p.add_argument("--input-period", type=int, default=0,
@@ -160,14 +162,17 @@ class Bench:
             raise RuntimeError(f"step {i}: {self.B.td_error_string(ctx)}")
 
     def nodes_per_step(self, K):
-        """Attended (live, in-window) nodes of every trie at each of the first K steps (untimed)."""
+        """Attended (live, in-window) and stored nodes of every trie at each of the first K
+        steps, before the step's append (untimed)."""
         self.init()
         stream = self.torch.cuda.current_stream().cuda_stream
-        n = []
+        n, stored = [], []
         for i in range(K):
             n.append([self.attended(t) for t in range(self.w.n_tries)])
+            stored.append([self.dec.read_state(t)["n_nodes"] for t in range(self.w.n_tries)])
             self.step(i, stream)
         self.torch.cuda.synchronize()
+        self.stored = np.array(stored)
         return np.array(n)
 
     def attended(self, t):
@@ -254,9 +259,77 @@ def gpu_bench(args, w, K):
     nodes = bench.nodes_per_step(K)
     collects = np.array([bench.collects(i) for i in range(K)])
     bench.dec.close()
+    batch = None if args.no_batch_baseline else batch_bench(bench, K, args.warmup)
     return dict(mode=mode, seconds=t1 - t0, eager_seconds=eager_s, attn_ms=attn_ms, nodes=nodes,
                 attn_graph_ms=attn_graph_ms, attn_graph_nodes=attn_graph_nodes, phase_ms=phase_ms,
-                collects=collects)
+                collects=collects, stored=bench.stored, batch=batch)
+
+
+def batch_bench(bench, K, warmup):
+    """The batch-based beam search baseline (Alg 1) on the same inputs: per-beam caches and a
+    full cache gather every step.  Steps/s of a graph replay of the K steps, and the KV bytes
+    its beams hold."""
+    import torch
+    B, w = bench.B, bench.w
+    cap = w.prompt_max + K + 2
+    dec = B.BatchBeamDecoder(w.n_tries, w.beam_width, cap, w.vocab, w.n_layers, w.n_q_heads, w.n_kv_heads,
+                             w.head_dim, w.window, w.dtype)
+    kc, vc = dec.prompt_cache()
+    for t in range(w.n_tries):
+        P = int(bench.plens[t])
+        _, pk, pv = synth.prompt(w, t, P, bench.seed)
+        kc[t, 0, :, :, :P] = bench.dev(pk)
+        vc[t, 0, :, :, :P] = bench.dev(pv)
+    L, ctx = B.lib(), dec.ctx
+
+    def init():
+        dec.init_prompt(bench.plens.tolist(), bench.tokens)
+        torch.cuda.synchronize()
+
+    def step(i, stream):
+        pend = i > 0
+        st = L.batch_beam_attn_decode(ctx, 0, w.n_layers, bench.q[i].data_ptr(),
+                                      bench.kn[i].data_ptr() if pend else None,
+                                      bench.vn[i].data_ptr() if pend else None, bench.out.data_ptr(),
+                                      ctypes.c_float(bench.scale), stream)
+        st |= L.batch_beam_logsoftmax_topk(ctx, bench.logits[i].data_ptr(), bench.sp.data_ptr(),
+                                           bench.st.data_ptr(), bench.ss.data_ptr(), bench.sl.data_ptr(),
+                                           bench.lse.data_ptr(), bench.par[i].data_ptr(), bench.tok[i].data_ptr(),
+                                           bench.ps.data_ptr(), stream)
+        st |= L.batch_beam_reorder(ctx, bench.par[i].data_ptr(), bench.tok[i].data_ptr(), bench.ps.data_ptr(),
+                                   stream)
+        if st != 0:
+            raise RuntimeError(f"batch step {i}: {L.bbs_error_string(ctx).decode()}")
+
+    stream = torch.cuda.current_stream().cuda_stream
+    init()
+    for i in range(min(warmup, K)):
+        step(i, stream)
+    torch.cuda.synchronize()
+    # the graph records the buffer of every step (the reorder alternates them), so K must be
+    # replayed from the initial state: re-initialised before each replay
+    init()
+    graph, cs = torch.cuda.CUDAGraph(), torch.cuda.Stream()
+    with torch.cuda.graph(graph, stream=cs):
+        s_ = torch.cuda.current_stream().cuda_stream
+        for i in range(K):
+            step(i, s_)
+    init()
+    graph.replay()
+    torch.cuda.synchronize()
+    init()
+    t0 = time.perf_counter()
+    graph.replay()
+    torch.cuda.synchronize()
+    sec = time.perf_counter() - t0
+    status = dec.status()
+    lens = np.array([[int(P) + i for P in bench.plens] for i in range(K)], dtype=np.float64)
+    n_beams = np.array([1] + [w.beam_width] * (K - 1), dtype=np.float64)
+    held = (lens.sum(axis=1) * n_beams).mean() * w.node_bytes  # KV the live beams hold, per step
+    dec.close()
+    if status != 0:
+        raise RuntimeError(f"batch baseline device status {status}")
+    return dict(seconds=sec, kv_bytes_mean=held)
 
 
 def phase_times(bench, K):
@@ -296,6 +369,16 @@ def gc_summary(w, ph, collects):
            "append_us_with_collection": round(float(us[idx, 3].mean()), 2) if len(idx) else None,
            "row_copy_us_after_collection": round(float(np.mean([us[i + 1, 1] for i in idx if i + 1 < K])), 2)
            if len(idx) and idx[0] + 1 < K else None}
+    # the Figure 4 series: per tenth of the run, mean decode pass and mean collection
+    series = []
+    for k in range(10):
+        lo, hi = k * K // 10, (k + 1) * K // 10
+        if hi <= lo:
+            continue
+        sel = [j for j, i in enumerate(idx) if lo <= i < hi]
+        series.append([lo + 1, round(float(dec[lo:hi].mean()), 2),
+                       round(float(gc[sel].mean()), 2) if sel else None])
+    out["series_first_step_decode_us_collection_us"] = series
     if len(idx):
         out["collection_us"] = round(float(gc.mean()), 2)
         out["collection_us_first_tenth"] = round(float(gc[:max(1, len(gc) // 10)].mean()), 2)
@@ -433,6 +516,19 @@ def main():
         "nodes_per_step_mean": round(float(r["nodes"].sum(axis=1).mean()), 1),
         "gc": gc_summary(w, r["phase_ms"], r["collects"]),
     }
+    if r["batch"] is not None:
+        trie_bytes = float(r["stored"].sum(axis=1).mean()) * w.node_bytes
+        bb = r["batch"]
+        out["batch_baseline"] = {
+            "value": round(K / bb["seconds"], 2), "unit": "steps/s",
+            "ms_per_step": round(bb["seconds"] * 1e3 / K, 5),
+            "trie_speedup": round((K / r["seconds"]) / (K / bb["seconds"]), 3),
+            "kv_bytes_mean": int(bb["kv_bytes_mean"]), "trie_kv_bytes_mean": int(trie_bytes),
+            "memory_ratio": round(bb["kv_bytes_mean"] / trie_bytes, 3),
+            "what": "Alg 1 on the same inputs: per-beam caches, a full cache gather (index_select) "
+                    "every step, the same attention and top-b kernels; KV bytes = what the live "
+                    "beams / the stored trie nodes hold, mean over the steps (the gather's second "
+                    "buffer not counted)"}
     if args.input_period > 0:
         out["data"] = f"synthetic, inputs of {args.input_period} steps reused in turn"
     if not args.no_cpu_baseline and not args.profile_only:

@@ -145,7 +145,7 @@ td_status bbs_create(const bbs_desc* d, bbs_ctx** out) {
       (e = balloc(c, &s.lse_part, (size_t)T * b * s.lse_chunks * 2)) != hipSuccess ||
       (e = balloc(c, &s.topk_keys, 2 * s.topk_half)) != hipSuccess ||
       (e = balloc(c, &c->tok[0], tbc)) != hipSuccess || (e = balloc(c, &c->tok[1], tbc)) != hipSuccess ||
-      (e = balloc(c, &c->rs.ok, (size_t)T)) != hipSuccess) {
+      (e = balloc(c, &c->rs.ok, 2 * (size_t)T)) != hipSuccess) {
     bbs_destroy(c);
     return bhip(nullptr, e, "allocating beam metadata / workspace");
   }

@@ -8,8 +8,8 @@
 //   k_bbs_copy   one WG per (request, new beam, layer, KV head): copies the parent's K and
 //                V rows of every stored position (a rejected request copies each beam onto
 //                itself, so both buffers stay consistent);
-//   k_bbs_meta   one WG per request: token histories, scores, lengths and the per-beam
-//                chain headers that the attention kernels read.
+//   k_bbs_meta   one WG per (request, new beam): token history, score and the chain
+//                header that the attention kernels read; the request's length.
 // The attention and the top-b are the trie decoder's kernels: a beam is a trie that is a
 // single chain with one leaf, and the requests' beams are the tries of one launch.
 #include "td_internal.h"
@@ -36,6 +36,7 @@ __global__ __launch_bounds__(64) void k_bbs_check(BbsState s, const int32_t* sel
   const bool full = len + 1 > s.cap;
   if (j == 0) {
     s.ok[t] = !(any_bad || full);
+    s.ok[s.T + t] = len;  // the length before this reorder, for the metadata launch
     if (any_bad || full) {
       atomicCAS(s.status, 0, any_bad ? kDevEinval : kDevEcapacity);
       s.status[1] = 1;
@@ -68,35 +69,30 @@ __global__ __launch_bounds__(256) void k_bbs_copy(BbsState s, const int32_t* sel
   }
 }
 
+// One WG per (request, new beam): the beam's token history, score and chain header; the
+// first beam's WG also updates the request's header (the old length comes from k_bbs_check).
 __global__ __launch_bounds__(256) void k_bbs_meta(BbsState s, const int32_t* sel_parent,
                                                   const int32_t* sel_token, const float* sel_score) {
-  const int t = blockIdx.x, b = s.b;
+  const int t = blockIdx.x / s.b, j = blockIdx.x % s.b, b = s.b;
   const bool ok = s.ok[t] != 0;
-  const int len = s.req[t].n_nodes;
-  const int32_t* ts = s.tok_src + (size_t)t * b * s.cap;
-  int32_t* td_ = s.tok_dst + (size_t)t * b * s.cap;
-  for (int idx = threadIdx.x; idx < b * len; idx += 256) {
-    const int j = idx / len, i = idx % len;
-    const int p = ok ? sel_parent[(size_t)t * b + j] : j;
-    td_[(size_t)j * s.cap + i] = ts[(size_t)p * s.cap + i];
-  }
-  __syncthreads();  // every thread has read the old length and live count
-  if (!ok) return;
-  if (threadIdx.x < b) {
-    const int j = threadIdx.x;
-    td_[(size_t)j * s.cap + len] = sel_token[(size_t)t * b + j];
-    s.score[(size_t)t * b + j] = sel_score[(size_t)t * b + j];
-    TrieHdr h;
-    h.n_nodes = len + 1;
-    h.base = 0;
-    h.n_live = 1;
-    h.n_shared = len + 1;
-    h.leaf_depth = len;
-    h.next_id = 0;
-    h.pad0 = h.pad1 = 0;
-    s.chain[(size_t)t * b + j] = h;
-  }
-  if (threadIdx.x == 0) {
+  const int len = s.ok[s.T + t];
+  const int p = ok ? sel_parent[(size_t)t * b + j] : j;
+  const int32_t* ts = s.tok_src + ((size_t)t * b + p) * s.cap;
+  int32_t* td_ = s.tok_dst + ((size_t)t * b + j) * s.cap;
+  for (int i = threadIdx.x; i < len; i += 256) td_[i] = ts[i];
+  if (!ok || threadIdx.x != 0) return;
+  td_[len] = sel_token[(size_t)t * b + j];
+  s.score[(size_t)t * b + j] = sel_score[(size_t)t * b + j];
+  TrieHdr h;
+  h.n_nodes = len + 1;
+  h.base = 0;
+  h.n_live = 1;
+  h.n_shared = len + 1;
+  h.leaf_depth = len;
+  h.next_id = 0;
+  h.pad0 = h.pad1 = 0;
+  s.chain[(size_t)t * b + j] = h;
+  if (j == 0) {
     TrieHdr r = s.req[t];
     r.n_nodes = len + 1;
     r.n_live = b;
@@ -114,7 +110,7 @@ hipError_t launch_bbs_reorder(const BbsState& s, const int32_t* sel_parent, cons
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_bbs_copy, dim3(s.T * s.b * s.L * s.Hkv), dim3(256), 0, st, s, sel_parent);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(k_bbs_meta, dim3(s.T), dim3(256), 0, st, s, sel_parent, sel_token, sel_score);
+  hipLaunchKernelGGL(k_bbs_meta, dim3(s.T * s.b), dim3(256), 0, st, s, sel_parent, sel_token, sel_score);
   return hipGetLastError();
 }
 

@@ -62,7 +62,7 @@ struct BbsState {
   const void* v_src;
   void* k_dst;           // the other buffers (gather destination)
   void* v_dst;
-  int32_t* ok;           // [T] 1 if the request's selection is valid
+  int32_t* ok;           // [2][T] 1 if the request's selection is valid; its old length
   int32_t* status;
 };
 hipError_t launch_bbs_reorder(const BbsState& s, const int32_t* sel_parent, const int32_t* sel_token,
