@@ -27,14 +27,17 @@ import numpy as np
 
 from .attention import path_attention
 from .beam import pair_scores, select
+from .finished import FinishedPool, select_with_eos
 from .trie import Trie
 
 
 def decode_step(trie: Trie, step: int, q: Optional[np.ndarray], k_new, v_new, logits: np.ndarray,
-                scale: float, script=None) -> dict:
+                scale: float, script=None, eos: int = -1, pool: Optional[FinishedPool] = None) -> dict:
     """q / k_new / v_new: [L'][b][..][d] (rows >= n_live unused) or None to skip attention.
 
     logits: [b][V] (rows >= n_live unused).  script: (parent_rank [b], token [b]) or None.
+    eos >= 0: the end-of-sequence token (the next beams are the best non-EOS candidates and
+    the finishing EOS candidates go to ``pool``, see ``finished``).
     """
     n_live = trie.n_live
     if step > 1 and k_new is not None:
@@ -42,7 +45,16 @@ def decode_step(trie: Trie, step: int, q: Optional[np.ndarray], k_new, v_new, lo
     out = {}
     if q is not None:
         out["o"] = path_attention(trie, q[:, :n_live], scale)
-    sel = select(logits[:n_live], trie.scores, trie.b)
+    if eos >= 0:
+        sel = select_with_eos(logits[:n_live], trie.scores, trie.b, eos)
+        if pool is not None:
+            tokens = None
+            if trie.window == 0:
+                leaves = list(trie.leaves)
+                tokens = lambda r: [n.token for n in trie.path(leaves[r])]  # noqa: E731
+            pool.process(sel, step, tokens, eos)
+    else:
+        sel = select(logits[:n_live], trie.scores, trie.b)
     out.update(sel)
     if script is None:
         par, tok, sc = sel["sel_parent"], sel["sel_token"], sel["sel_score"]

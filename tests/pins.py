@@ -399,3 +399,158 @@ def pin_fig1_counts():
     oinv.check(trie)
     ratio = len(trie.order) / sum(len(trie.path(leaf)) for leaf in trie.leaves)
     assert abs(ratio - 12.0 / 21.0) < 1e-15
+
+
+# --------------------------------------------------------------------------------------------
+# end of sequence, finished hypotheses, length penalty
+# --------------------------------------------------------------------------------------------
+def eos_logits(seed, rows, vocab, eos, boost):
+    """Logits where the EOS column is lifted by `boost` so that it often ranks near the top."""
+    g = np.random.default_rng(seed)
+    x = g.normal(0.0, 3.0, (rows, vocab)).astype(np.float32)
+    x[:, eos] += np.float32(boost)
+    return x
+
+
+def pin_eos_two_formulations(seed, cases=60):
+    """The ranking walk of ``select_with_eos`` against a second formulation written from the
+    definition: next beams = top-b of the score matrix with the EOS column removed; an EOS
+    candidate finishes iff fewer than b candidates (EOS or not) beat it in the key order."""
+    import oracle.finished as ofin
+    g = np.random.default_rng(seed)
+    for _ in range(cases):
+        n_live, vocab, b = int(g.integers(1, 7)), int(g.integers(8, 40)), int(g.integers(1, 7))
+        eos = int(g.integers(0, vocab))
+        logits = eos_logits(int(g.integers(1 << 30)), n_live, vocab, eos, float(g.uniform(0, 12)))
+        if g.random() < 0.3:  # ties: repeated values
+            logits = np.round(logits)
+        scores = -np.sort(g.uniform(0, 3, n_live)).astype(np.float32)
+        if g.random() < 0.3:
+            scores[:] = scores[0]
+        got = ofin.select_with_eos(logits, scores, b, eos)
+        lse = obeam.row_lse32(logits)
+        lp, s = obeam.candidate_scores(logits, lse, scores)
+        flat = np.arange(s.size).reshape(s.shape)
+        keys = [(-float(s[r, v]), int(flat[r, v])) for r in range(n_live) for v in range(vocab)]
+        non_eos = sorted(k for k in keys if k[1] % vocab != eos)[:b]
+        assert [k[1] // vocab for k in non_eos] == got["sel_parent"].tolist()
+        assert [k[1] % vocab for k in non_eos] == got["sel_token"].tolist()
+        fin = []
+        for r in range(n_live):
+            k = (-float(s[r, eos]), r * vocab + eos)
+            better = sum(1 for o in keys if o < k)
+            if better < b:
+                fin.append((better, r, np.float32(s[r, eos])))
+        fin.sort()
+        assert [(a, c, float(d)) for a, c, d in fin] == [(a, c, float(d)) for a, c, d in got["finished"]]
+
+
+def pin_eos_greedy(seed, steps=30):
+    """b = 1: every step the single best candidate; an EOS there finishes a hypothesis of
+    that step's length and the beam continues with the best non-EOS token.  With early
+    stopping the first EOS ends the request; with alpha = 0 the normalised score is the
+    score itself."""
+    import oracle.finished as ofin
+    g = np.random.default_rng(seed)
+    vocab, eos = 12, 3
+    pool = ofin.FinishedPool(1, 0.0, True)
+    score, first = np.float32(0.0), None
+    for s in range(1, steps + 1):
+        logits = eos_logits(int(g.integers(1 << 30)), 1, vocab, eos, 3.0)
+        sel = ofin.select_with_eos(logits, np.array([score], np.float32), 1, eos)
+        pool.process(sel, s)
+        lse = obeam.row_lse32(logits)
+        sc = (score + (logits[0] - lse[0])).astype(np.float32)
+        best = int(np.argmax(sc))  # greedy (the first maximum: lowest index on ties)
+        if best == eos and first is None:
+            first = (s, sc[eos])
+        nxt = int(np.argmax(np.where(np.arange(vocab) == eos, -np.inf, sc)))
+        assert sel["sel_token"].tolist() == [nxt]
+        score = sc[nxt]
+    assert first is not None, "the fixture must produce an EOS"
+    assert pool.done and len(pool.hyps) == 1
+    h = pool.hyps[0]
+    assert (h.step, float(h.score), float(h.norm)) == (first[0], float(first[1]), float(first[1]))
+
+
+def pin_eos_trie_equals_batch(w, seed, eos, boost, alpha, early):
+    """With an EOS the trie and batch beam search (Alg 1) still take the same steps, and
+    their finished pools hold the same hypotheses - the trie's read from root-to-leaf paths,
+    the batch's from its beams' token lists."""
+    import oracle.finished as ofin
+    tok, pk, pv = _prompt(w, seed)
+    trie = otrie.Trie(tok, pk, pv, w.beam_width, 0)
+    bb = obb.BatchBeamSearch(tok, pk, pv, w.beam_width, 0)
+    pt = ofin.FinishedPool(w.beam_width, alpha, early)
+    pb = ofin.FinishedPool(w.beam_width, alpha, early)
+    scale = 1.0 / np.sqrt(w.head_dim)
+    for s in range(1, w.steps + 1):
+        q, kn, vn, _ = _step_inputs(w, s, seed)
+        logits = eos_logits(seed * 1000 + s, w.beam_width, w.vocab, eos, boost)
+        n_live = trie.n_live
+        if s > 1:
+            bb.write_kv(kn[:, :n_live], vn[:, :n_live])
+        ob = bb.attention(q[:, :n_live], scale)
+        out = odec.decode_step(trie, s, q, kn, vn, logits, scale, None, eos, pt)
+        sel = ofin.select_with_eos(logits[:n_live], bb.scores, w.beam_width, eos)
+        pb.process(sel, s, lambda r: bb.beams[r].tokens, eos)
+        assert float(np.max(np.abs(out["o"] - ob))) <= 1e-12
+        for key in ("sel_parent", "sel_token", "sel_score"):
+            assert np.array_equal(out[key], sel[key]), (s, key)
+        bb.advance(sel["sel_parent"], sel["sel_token"], sel["sel_score"])
+        assert pt.done == pb.done
+        assert [(h.tokens, float(h.norm), h.step) for h in pt.hyps] == \
+               [(h.tokens, float(h.norm), h.step) for h in pb.hyps], s
+        oinv.check(trie)
+    return pt
+
+
+def pin_eos_greedy_length(seed, steps=30):
+    """b = 1, alpha = 1, early stopping: the first EOS ends the request with a hypothesis of
+    as many generated tokens as steps taken (the EOS counted), normalised by that count."""
+    import oracle.finished as ofin
+    g = np.random.default_rng(seed)
+    vocab, eos = 12, 3
+    pool = ofin.FinishedPool(1, 1.0, True)
+    score = np.float32(0.0)
+    for s in range(1, steps + 1):
+        logits = eos_logits(int(g.integers(1 << 30)), 1, vocab, eos, 3.0)
+        sel = ofin.select_with_eos(logits, np.array([score], np.float32), 1, eos)
+        had = pool.done
+        pool.process(sel, s)
+        if pool.done and not had:
+            _, _, sc = sel["finished"][0]
+            h = pool.hyps[0]
+            assert h.step == s and float(h.norm) == float(np.float32(float(sc) / s))
+            return
+        score = sel["sel_score"][0]
+    raise AssertionError("the fixture must produce an EOS")
+
+
+def pin_pool_is_best_of_events(seed, steps=40, b=4, alpha=0.8):
+    """The pool after a run equals the b best (normalised score, then arrival) of every
+    finishing event up to the step the request became done, and it became done at the first
+    step where b events had arrived and the worst of the b best reached the best next beam's
+    normalised score."""
+    import oracle.finished as ofin
+    g = np.random.default_rng(seed)
+    vocab, eos, n_live = 20, 5, 1
+    pool = ofin.FinishedPool(b, alpha, False)
+    scores = np.zeros(1, np.float32)
+    events, done_at = [], None
+    for s in range(1, steps + 1):
+        logits = eos_logits(int(g.integers(1 << 30)), n_live, vocab, eos, 5.0)
+        sel = ofin.select_with_eos(logits, scores, b, eos)
+        pool.process(sel, s)
+        if done_at is None:
+            for _rank, r, sc in sel["finished"]:
+                events.append((float(sc) / (float(s) ** alpha), len(events), s, r, float(sc)))
+            best = sorted(events, key=lambda e: (-float(np.float32(e[0])), e[1]))[:b]
+            if len(best) == b and float(np.float32(best[-1][0])) >= \
+                    float(np.float32(float(sel["sel_score"][0]) / (float(s) ** alpha))):
+                done_at = s
+        scores = sel["sel_score"]
+        n_live = len(scores)
+    best = sorted(events, key=lambda e: (-float(np.float32(e[0])), e[1]))[:b]
+    assert [(h.step, h.parent, float(h.score)) for h in pool.hyps] == [(e[2], e[3], e[4]) for e in best]
+    assert pool.done == (done_at is not None)

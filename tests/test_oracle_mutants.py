@@ -5,7 +5,8 @@ GQA head mapping, an off-by-one window, reversed tie order, a float32 log-sum-ex
 a missing prune, a wrong mask remap, a wrong parent, a swapped query row, a
 missing window eviction, a wrong row in the pair score, a collection schedule
 counted in steps or ignoring the interval, dead nodes keeping stale mask bits
-between collections.  The pins run on a
+between collections, an EOS finishing at rank b, a hypothesis length without its
+EOS, a pool that keeps the worst, a done test on raw scores.  The pins run on a
 monkeypatched copy of the oracle for the duration of one test.
 """
 import numpy as np
@@ -150,3 +151,58 @@ def test_mutant_deferred_gc_keeps_old_masks(monkeypatch):
                 self.masks[id(n)] = old[id(n)]
     monkeypatch.setattr(otrie.Trie, "append", bad)
     _fails(pins.pin_gc_deferral, pins.small_workload(b=4, V=30, P=5, steps=10, g=5), 7)
+
+
+def _select_rank_at_most_b(orig):
+    """select_with_eos, but an EOS candidate of rank b also finishes."""
+    def bad(logits, scores, b, eos):
+        out = orig(logits, scores, b, eos)
+        lse = obeam.row_lse32(logits)
+        _, sc = obeam.candidate_scores(logits, lse, scores)
+        flat = sc.ravel()
+        order = np.lexsort((np.arange(flat.size), -flat))
+        vocab = logits.shape[1]
+        out["finished"] = [(rk, int(f // vocab), np.float32(flat[f])) for rk, f in enumerate(order)
+                           if f % vocab == eos and rk <= b]
+        return out
+    return bad
+
+
+def test_mutant_eos_rank_threshold(monkeypatch):
+    import oracle.finished as ofin
+    monkeypatch.setattr(ofin, "select_with_eos", _select_rank_at_most_b(ofin.select_with_eos))
+    _fails(pins.pin_eos_two_formulations, 60)
+
+
+def test_mutant_eos_length_without_the_eos(monkeypatch):
+    import oracle.finished as ofin
+    orig = ofin.FinishedPool.add
+    monkeypatch.setattr(ofin.FinishedPool, "add",
+                        lambda self, score, step, parent, tokens=None: orig(self, score, step - 1 if step > 1 else 1,
+                                                                            parent, tokens))
+    _fails(pins.pin_eos_greedy_length, 61)
+
+
+def test_mutant_pool_keeps_the_worst(monkeypatch):
+    import oracle.finished as ofin
+
+    def bad(self, score, step, parent, tokens=None):
+        h = ofin.Hypothesis(ofin.normalized(score, step, self.alpha), np.float32(score), int(step), int(parent),
+                            tokens, self._arrivals)
+        self._arrivals += 1
+        self.hyps.append(h)
+        self.hyps.sort(key=lambda x: (float(x.norm), x.order))
+        del self.hyps[self.b:]
+    monkeypatch.setattr(ofin.FinishedPool, "add", bad)
+    _fails(pins.pin_pool_is_best_of_events, 62)
+
+
+def test_mutant_done_on_raw_scores(monkeypatch):
+    import oracle.finished as ofin
+
+    def bad(self, best_next_score, step):
+        if self.done or len(self.hyps) < self.b:
+            return
+        self.done = self.early or bool(self.worst() >= np.float32(best_next_score))
+    monkeypatch.setattr(ofin.FinishedPool, "update_done", bad)
+    _fails(pins.pin_pool_is_best_of_events, 63)

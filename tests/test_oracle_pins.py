@@ -89,3 +89,28 @@ def test_node_count_over_a_long_scripted_run():
         trie.garbage_collect()
         oinv.check(trie)
     assert trie.pruned > 0
+
+
+def test_eos_ranking_walk_equals_its_definition():
+    pins.pin_eos_two_formulations(50)
+
+
+def test_eos_greedy_closed_form():
+    pins.pin_eos_greedy(51)
+
+
+@pytest.mark.parametrize("b,alpha,early,boost,seed", [(3, 1.0, False, 4.0, 52), (4, 0.0, True, 6.0, 53),
+                                                      (5, 0.7, False, 5.0, 54), (2, 2.0, False, 8.0, 55)])
+def test_eos_trie_equals_batch_beam_search(b, alpha, early, boost, seed):
+    w = pins.small_workload(b=b, V=30, steps=14)
+    pool = pins.pin_eos_trie_equals_batch(w, seed, eos=7, boost=boost, alpha=alpha, early=early)
+    assert len(pool.hyps) > 0
+
+
+def test_eos_greedy_length_convention():
+    pins.pin_eos_greedy_length(56)
+
+
+@pytest.mark.parametrize("seed", [57, 58, 59])
+def test_finished_pool_is_the_best_of_its_events(seed):
+    pins.pin_pool_is_best_of_events(seed)
