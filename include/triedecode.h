@@ -86,6 +86,10 @@ typedef struct {
   int32_t gc_interval;  /* g >= 1: garbage is collected after the appends whose next      */
                         /*   position (leaf depth + 1) is a multiple of g (Alg 2); 1 =    */
                         /*   after every append                                           */
+  int32_t eos_token;    /* end-of-sequence token in [0, V), or -1 for none (then V >= b;   */
+                        /*   with one, V - 1 >= b): see beam_logsoftmax_topk              */
+  float length_penalty; /* alpha: a finished hypothesis ranks by score / length^alpha     */
+  int32_t early_stopping; /* 1: a trie is done once b hypotheses have finished            */
   void* k_pool;         /* caller-owned device [T][L][Hkv][capacity][d]; valid until      */
   void* v_pool;         /*   td_destroy                                                   */
 } td_desc;
@@ -101,6 +105,7 @@ typedef struct {
   int32_t next_id;      /* id of the next appended node (prompt P, then P + s*b)          */
   int32_t kv_pending;   /* 1: the leaves' K/V rows are not yet in the pools; the next     */
                         /*    trie_attn_decode call(s) must pass k_new/v_new              */
+  int32_t step;         /* appends so far (decode steps taken since the prompt)           */
   int32_t* node_id;     /* [N] prompt token j -> j; step s rank j -> P + (s-1)*b + j     */
   int32_t* parent_slot; /* [N] logical slot of the parent, -1 for a root                 */
   int32_t* token;       /* [N]                                                            */
@@ -165,7 +170,16 @@ td_status td_set_kernel_events(td_ctx* ctx, int32_t phase, hipEvent_t start, hip
  * sel_logprob = lp, each [T][b].  d_lse ([T][b], may be NULL) receives lse_r.
  * Optional scoring of caller-chosen pairs (d_pair_parent/d_pair_token [T][b], both
  * NULL or both set): d_pair_score receives s of each pair by the same formula.
- * Reads n_live and leaf scores from the context on the device. */
+ * Reads n_live and leaf scores from the context on the device.
+ * With an end-of-sequence token (desc.eos_token >= 0; the paper has none, this is the
+ * usual beam-search rule): an EOS candidate ranked better than b in the order above
+ * finishes a hypothesis, and the selection (the next beams) is the b best non-EOS
+ * candidates.  A hypothesis finished at decode step s (s = appends so far + 1) has s
+ * generated tokens, score = its candidate score, and ranks by norm = fl32(score /
+ * s^length_penalty) (fp64 division and power, one rounding).  Each trie keeps the b best
+ * by norm, earlier arrivals first among equals (td_read_finished); a trie is done once it
+ * holds b and early_stopping is set or its worst norm >= fl32(best next score /
+ * s^length_penalty); a done trie keeps decoding but finishes no more hypotheses. */
 td_status beam_logsoftmax_topk(td_ctx* ctx, const float* d_logits, int32_t* d_sel_parent,
                                int32_t* d_sel_token, float* d_sel_score, float* d_sel_logprob,
                                float* d_lse, const int32_t* d_pair_parent,
@@ -192,6 +206,13 @@ td_status beam_logsoftmax_topk(td_ctx* ctx, const float* d_logits, int32_t* d_se
  * unchanged. */
 td_status trie_append_prune(td_ctx* ctx, const int32_t* d_sel_parent, const int32_t* d_sel_token,
                             const float* d_sel_score, hipStream_t stream);
+
+/* The finished hypotheses of trie t (synchronises the device): *count (<= b) entries, best
+ * first - norm, score, step (its length), parent (rank of the live beam it extends at
+ * that step; with the selections of steps 1 .. step-1 this names its tokens) - and *done.
+ * Host arrays of beam_width entries.  Without an EOS token *count = *done = 0. */
+td_status td_read_finished(td_ctx* ctx, int32_t trie, float* h_norm, float* h_score, int32_t* h_step,
+                           int32_t* h_parent, int32_t* count, int32_t* done);
 
 /* Copy trie t to the host (synchronises the device). */
 td_status td_read_state(td_ctx* ctx, int32_t trie, td_state* host_out);

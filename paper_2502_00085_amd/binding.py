@@ -29,6 +29,8 @@ class TdDesc(ctypes.Structure):
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("window", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("attn_impl", ctypes.c_int32), ("gc_interval", ctypes.c_int32),
+                ("eos_token", ctypes.c_int32), ("length_penalty", ctypes.c_float),
+                ("early_stopping", ctypes.c_int32),
                 ("k_pool", ctypes.c_void_p), ("v_pool", ctypes.c_void_p)]
 
 
@@ -45,7 +47,7 @@ class BbsDesc(ctypes.Structure):
 class TdState(ctypes.Structure):
     _fields_ = [("n_nodes", ctypes.c_int32), ("n_live", ctypes.c_int32), ("base", ctypes.c_int32),
                 ("n_shared", ctypes.c_int32), ("next_id", ctypes.c_int32),
-                ("kv_pending", ctypes.c_int32),
+                ("kv_pending", ctypes.c_int32), ("step", ctypes.c_int32),
                 ("node_id", ctypes.POINTER(ctypes.c_int32)),
                 ("parent_slot", ctypes.POINTER(ctypes.c_int32)),
                 ("token", ctypes.POINTER(ctypes.c_int32)),
@@ -82,6 +84,7 @@ def lib() -> ctypes.CDLL:
         L.td_load_state.argtypes = [vp, i32, ctypes.POINTER(TdState)]
         L.td_get_status.argtypes = [vp]
         L.td_set_kernel_events.argtypes = [vp, i32, vp, vp]
+        L.td_read_finished.argtypes = [vp, i32, vp, vp, vp, vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
         L.td_error_string.argtypes = [vp]
         L.td_error_string.restype = ctypes.c_char_p
         L.td_status_name.argtypes = [i32]
@@ -99,7 +102,7 @@ def lib() -> ctypes.CDLL:
         L.bbs_error_string.restype = ctypes.c_char_p
         for name in ("td_create", "td_destroy", "td_init_prompt", "trie_attn_decode",
                      "beam_logsoftmax_topk", "trie_append_prune", "td_read_state", "td_load_state",
-                     "td_get_status", "td_set_kernel_events", "bbs_create", "bbs_destroy",
+                     "td_get_status", "td_set_kernel_events", "td_read_finished", "bbs_create", "bbs_destroy",
                      "bbs_init_prompt", "batch_beam_attn_decode", "batch_beam_logsoftmax_topk",
                      "batch_beam_reorder", "bbs_current_cache", "bbs_read_beams", "bbs_get_status"):
             getattr(L, name).restype = ctypes.c_int32
@@ -259,8 +262,20 @@ def td_read_state(ctx, dims: Dims, trie: int) -> dict:
     out["leaf_slot"] = arrs["leaf_slot"][:nl].copy()
     out["leaf_score"] = arrs["leaf_score"][:nl].copy()
     out.update(n_nodes=n, n_live=nl, base=st.base, n_shared=st.n_shared, next_id=st.next_id,
-               kv_pending=st.kv_pending)
+               kv_pending=st.kv_pending, step=st.step)
     return out
+
+
+def td_read_finished(ctx, dims: Dims, trie: int) -> dict:
+    b = dims.b
+    norm, score = np.zeros(b, np.float32), np.zeros(b, np.float32)
+    step, parent = np.zeros(b, np.int32), np.zeros(b, np.int32)
+    count, done = ctypes.c_int32(), ctypes.c_int32()
+    _check(ctx, lib().td_read_finished(ctx, int(trie), norm.ctypes.data, score.ctypes.data, step.ctypes.data,
+                                       parent.ctypes.data, ctypes.byref(count), ctypes.byref(done)))
+    n = count.value
+    return {"count": n, "done": bool(done.value), "norm": norm[:n].copy(), "score": score[:n].copy(),
+            "step": step[:n].copy(), "parent": parent[:n].copy()}
 
 
 def td_load_state(ctx, dims: Dims, trie: int, state: dict):
@@ -268,6 +283,7 @@ def td_load_state(ctx, dims: Dims, trie: int, state: dict):
     st = TdState()
     st.n_nodes, st.n_live = int(state["n_nodes"]), int(state["n_live"])
     st.next_id, st.kv_pending = int(state["next_id"]), int(state.get("kv_pending", 0))
+    st.step = int(state.get("step", 0))
     for k, dt in (("node_id", np.int32), ("parent_slot", np.int32), ("token", np.int32),
                   ("depth", np.int32), ("mask", np.uint64), ("leaf_slot", np.int32),
                   ("leaf_score", np.float32)):
@@ -292,7 +308,8 @@ class TrieDecoder:
     """One context plus its caller-owned K/V pools, allocated as torch tensors on the device."""
 
     def __init__(self, n_tries, beam_width, capacity, vocab, n_layers, n_q_heads, n_kv_heads,
-                 head_dim, window=0, dtype="bf16", attn_impl=TD_ATTN_AUTO, device="cuda", gc_interval=1):
+                 head_dim, window=0, dtype="bf16", attn_impl=TD_ATTN_AUTO, device="cuda", gc_interval=1,
+                 eos_token=-1, length_penalty=1.0, early_stopping=False):
         import torch
         self.tdtype = torch.bfloat16 if dtype == "bf16" else torch.float32
         shape = (n_tries, n_layers, n_kv_heads, capacity, head_dim)
@@ -300,7 +317,8 @@ class TrieDecoder:
         self.v_pool = torch.zeros(shape, dtype=self.tdtype, device=device)
         self.desc = TdDesc(n_tries, beam_width, capacity, vocab, n_layers, n_q_heads, n_kv_heads,
                            head_dim, window, TD_BF16 if dtype == "bf16" else TD_F32, attn_impl,
-                           gc_interval, self.k_pool.data_ptr(), self.v_pool.data_ptr())
+                           gc_interval, eos_token, length_penalty, int(bool(early_stopping)),
+                           self.k_pool.data_ptr(), self.v_pool.data_ptr())
         self.dims = Dims(self.desc)
         self.ctx = td_create(self.desc)
 
@@ -334,6 +352,9 @@ class TrieDecoder:
 
     def load_state(self, trie, state):
         td_load_state(self.ctx, self.dims, trie, state)
+
+    def read_finished(self, trie=0):
+        return td_read_finished(self.ctx, self.dims, trie)
 
     def status(self):
         return td_get_status(self.ctx)

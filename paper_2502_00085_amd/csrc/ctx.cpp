@@ -109,6 +109,11 @@ td_status td_create(const td_desc* d, td_ctx** out) {
   if (d->window < 0) return fail(nullptr, TD_EINVAL, "window must be >= 0");
   if (d->gc_interval < 1 || d->gc_interval > (1 << 20))
     return fail(nullptr, TD_EINVAL, "gc_interval must be in [1, 2^20]");
+  if (d->eos_token < -1 || d->eos_token >= d->vocab) return fail(nullptr, TD_EINVAL, "eos_token must be -1 or in [0, vocab)");
+  if (d->eos_token >= 0 && d->vocab - 1 < d->beam_width)
+    return fail(nullptr, TD_EINVAL, "with an eos_token, vocab - 1 must be >= beam_width");
+  if (!std::isfinite(d->length_penalty)) return fail(nullptr, TD_EINVAL, "length_penalty must be finite");
+  if (d->early_stopping != 0 && d->early_stopping != 1) return fail(nullptr, TD_EINVAL, "early_stopping must be 0 or 1");
   if (d->dtype != TD_F32 && d->dtype != TD_BF16) return fail(nullptr, TD_EINVAL, "bad dtype");
   if (d->attn_impl < TD_ATTN_AUTO || d->attn_impl > TD_ATTN_MFMA)
     return fail(nullptr, TD_EINVAL, "bad attn_impl");
@@ -135,6 +140,9 @@ td_status td_create(const td_desc* d, td_ctx** out) {
   s.D = d->head_dim;
   s.W = d->window;
   s.G = d->gc_interval;
+  s.eos = d->eos_token;
+  s.alpha = d->length_penalty;
+  s.early = d->early_stopping;
   s.dtype = d->dtype;
   s.k_pool = d->k_pool;
   s.v_pool = d->v_pool;
@@ -154,6 +162,12 @@ td_status td_create(const td_desc* d, td_ctx** out) {
       (e = alloc(c, &s.newpos, tc)) != hipSuccess || (e = alloc(c, &s.moves, tc)) != hipSuccess ||
       (e = alloc(c, &s.n_moves, (size_t)s.T)) != hipSuccess ||
       (e = alloc(c, &s.attn_part, (size_t)s.attn_part_floats)) != hipSuccess ||
+      (e = alloc(c, &s.fin_norm, (size_t)s.T * s.b)) != hipSuccess ||
+      (e = alloc(c, &s.fin_score, (size_t)s.T * s.b)) != hipSuccess ||
+      (e = alloc(c, &s.fin_step, (size_t)s.T * s.b)) != hipSuccess ||
+      (e = alloc(c, &s.fin_parent, (size_t)s.T * s.b)) != hipSuccess ||
+      (e = alloc(c, &s.fin_count, (size_t)s.T)) != hipSuccess ||
+      (e = alloc(c, &s.fin_done, (size_t)s.T)) != hipSuccess ||
       (e = alloc(c, &c->d_plen, (size_t)s.T)) != hipSuccess) {
     td_destroy(c);
     return hip_fail(nullptr, e, "allocating trie metadata / workspace");
@@ -189,6 +203,9 @@ td_status td_init_prompt(td_ctx* c, const int32_t* h_plen, const int32_t* d_toke
   hipError_t e = hipStreamSynchronize(st);
   if (e == hipSuccess) e = hipMemcpy(c->d_plen, h_plen, sizeof(int32_t) * c->dev.T, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = td::launch_init_prompt(c->dev, c->d_plen, d_tokens, stride, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = hipMemset(c->dev.fin_count, 0, sizeof(int32_t) * c->dev.T);
+  if (e == hipSuccess) e = hipMemset(c->dev.fin_done, 0, sizeof(int32_t) * c->dev.T);
   if (e != hipSuccess) return hip_fail(c, e, "td_init_prompt");
   c->inited.assign(c->dev.T, 1);
   for (int t = 0; t < c->dev.T; ++t) c->leaf_depth[t] = h_plen[t] - 1;
@@ -371,6 +388,7 @@ td_status td_read_state(td_ctx* c, int32_t trie, td_state* o) {
   o->n_shared = h.n_shared;
   o->next_id = h.next_id;
   o->kv_pending = c->pending ? 1 : 0;
+  o->step = h.step;
   return TD_OK;
 }
 
@@ -382,6 +400,7 @@ td_status td_load_state(td_ctx* c, int32_t trie, const td_state* in) {
   const int N = in->n_nodes, nl = in->n_live;
   if (N < 1 || N > s.cap || nl < 1 || nl > s.b || nl > N)
     return fail(c, TD_EINVAL, "need 1 <= n_live <= min(beam_width, n_nodes), n_nodes <= capacity");
+  if (in->step < 0) return fail(c, TD_EINVAL, "step must be >= 0");
   if (!in->node_id || !in->parent_slot || !in->token || !in->depth || !in->mask || !in->leaf_slot ||
       !in->leaf_score)
     return fail(c, TD_EINVAL, "all state arrays are required");
@@ -426,14 +445,36 @@ td_status td_load_state(td_ctx* c, int32_t trie, const td_state* in) {
   h.n_shared = n_shared;
   h.leaf_depth = in->depth[N - 1];
   h.next_id = in->next_id;
-  h.pad0 = h.pad1 = 0;
+  h.step = in->step;
+  h.pad1 = 0;
   if (e == hipSuccess) e = hipMemcpy(s.hdr + trie, &h, sizeof h, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemset(s.fin_count + trie, 0, sizeof(int32_t));
+  if (e == hipSuccess) e = hipMemset(s.fin_done + trie, 0, sizeof(int32_t));
   if (e != hipSuccess) return hip_fail(c, e, "td_load_state");
   c->inited[trie] = 1;
   c->leaf_depth[trie] = h.leaf_depth;
   c->pending = in->kv_pending != 0;
   c->moves_pending = false;
   c->layer_written.assign(s.L, 0);
+  return TD_OK;
+}
+
+td_status td_read_finished(td_ctx* c, int32_t trie, float* h_norm, float* h_score, int32_t* h_step,
+                           int32_t* h_parent, int32_t* count, int32_t* done) {
+  if (!c) return TD_EINVAL;
+  c->err.clear();
+  const td::DevState& s = c->dev;
+  if (trie < 0 || trie >= s.T || !h_norm || !h_score || !h_step || !h_parent || !count || !done)
+    return fail(c, TD_EINVAL, "bad trie index or null output");
+  const size_t off = (size_t)trie * s.b;
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = hipMemcpy(count, s.fin_count + trie, 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(done, s.fin_done + trie, 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(h_norm, s.fin_norm + off, (size_t)s.b * 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(h_score, s.fin_score + off, (size_t)s.b * 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(h_step, s.fin_step + off, (size_t)s.b * 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(h_parent, s.fin_parent + off, (size_t)s.b * 4, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(c, e, "td_read_finished");
   return TD_OK;
 }
 

@@ -18,13 +18,24 @@ struct TrieHdr {
                        //   slot, kept until the next collection, ends the run)
   int32_t leaf_depth;  // depth D of every live leaf
   int32_t next_id;     // id given to the next appended node of rank 0
-  int32_t pad0, pad1;
+  int32_t step;        // appends so far (the next selection is step + 1)
+  int32_t pad1;
 };
 
 // Device-side pointers of one context.  Node arrays are [T][cap], indexed by physical slot.
 struct DevState {
   int T, b, cap, V, L, Hq, Hkv, D, W, dtype;
   int G;                 // garbage-collection interval g (>= 1)
+  int eos;               // end-of-sequence token, -1 = none
+  float alpha;           // length penalty
+  int early;             // early stopping
+  // finished hypotheses (eos >= 0): [T][b], best first, and per trie the count and done flag
+  float* fin_norm;
+  float* fin_score;
+  int32_t* fin_step;
+  int32_t* fin_parent;
+  int32_t* fin_count;    // [T]
+  int32_t* fin_done;     // [T]
   void* k_pool;
   void* v_pool;
   TrieHdr* hdr;          // [T]

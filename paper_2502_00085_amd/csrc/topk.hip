@@ -191,7 +191,8 @@ __global__ __launch_bounds__(kChunkThreads) void k_topb_chunk(DevState s, const 
   for (int i = 0; i < kChunkPer; ++i) {
     const int v = v0 + i * kChunkThreads + (int)threadIdx.x;
     m = fmaxf(m, x[i]);
-    const uint64_t k = v < V ? x_key(x[i], flat0 + (uint32_t)(i * kChunkThreads)) : 0;
+    // (the end-of-sequence token, if any, is not a candidate for the next beams)
+    const uint64_t k = v < V && v != s.eos ? x_key(x[i], flat0 + (uint32_t)(i * kChunkThreads)) : 0;
     k2 = k > k1 ? k1 : (k > k2 ? k : k2);
     k1 = k > k1 ? k : k1;
   }
@@ -271,6 +272,49 @@ __device__ inline uint32_t wave_bth_of16(const uint32_t* w, int b) {
 // 0.5 / d away from an integer, and the float error, below (i / d) * 2^-22, is smaller.
 __device__ inline int div_small(int i, float inv) { return (int)(((float)i + 0.5f) * inv); }
 
+// fl32(score / length^alpha) in fp64 (one rounding).
+__device__ inline float length_norm(float score, int length, float alpha) {
+  return (float)((double)score / pow((double)length, (double)alpha));
+}
+
+// Adds the step's finishing EOS candidates (row r finishes iff rank[r] >= 0), in rank
+// order, to trie t's pool of the b best finished hypotheses (best first; a newcomer goes
+// after the entries it ties), then sets the done flag.  One thread; best_next = the score
+// of the best next beam.
+__device__ inline void finish_hypotheses(const DevState& s, int t, int n_live, const int* rank,
+                                         const float* val, float best_next) {
+  if (s.fin_done[t]) return;
+  const int b = s.b;
+  const int step = s.hdr[t].step + 1;
+  float* norm = s.fin_norm + (size_t)t * b;
+  float* score = s.fin_score + (size_t)t * b;
+  int32_t* stp = s.fin_step + (size_t)t * b;
+  int32_t* par = s.fin_parent + (size_t)t * b;
+  int count = s.fin_count[t];
+  for (int k = 0; k < b; ++k) {  // rank k of this step's ranking, if an EOS candidate holds it
+    int r = -1;
+    for (int i = 0; i < n_live; ++i) r = rank[i] == k ? i : r;
+    if (r < 0) continue;
+    const float nv = length_norm(val[r], step, s.alpha);
+    int p = count;
+    while (p > 0 && norm[p - 1] < nv) --p;
+    if (p >= b) continue;
+    for (int q = min(count, b - 1); q > p; --q) {
+      norm[q] = norm[q - 1];
+      score[q] = score[q - 1];
+      stp[q] = stp[q - 1];
+      par[q] = par[q - 1];
+    }
+    norm[p] = nv;
+    score[p] = val[r];
+    stp[p] = step;
+    par[p] = r;
+    count = min(count + 1, b);
+  }
+  s.fin_count[t] = count;
+  if (count == b && (s.early || norm[b - 1] >= length_norm(best_next, step, s.alpha))) s.fin_done[t] = 1;
+}
+
 // Merge of one trie's chunks into the final selection, then the outputs.
 __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const float* logits,
                                                               int32_t* sel_parent, int32_t* sel_token,
@@ -287,6 +331,9 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
   __shared__ uint64_t best_k[kMaxBeam], best_c[kMaxBeam];
   __shared__ float row_lse[kMaxBeam], row_score[kMaxBeam];
   __shared__ int ncand, nhot;
+  __shared__ uint64_t eos_key[kMaxBeam];
+  __shared__ int eos_at[kMaxBeam];
+  __shared__ float eos_val[kMaxBeam];
   __shared__ int hot[kCandMax];
   const float* lrow = logits + (size_t)t * b * V;
   // Entry j of wave w is sub-chunk w of (row j / nch, chunk j % nch): every wave covers
@@ -429,7 +476,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
         const int v = c * kLseChunk + q * kChunkThreads + sw * 64 + lane;
         const uint32_t flat = (uint32_t)r * (uint32_t)V + (uint32_t)v;
         const float sc = score_only(xs[q], row_lse[r], row_score[r]);
-        take[q] = v < V && ord_score(sc) >= L;
+        take[q] = v < V && v != s.eos && ord_score(sc) >= L;
         ks[q] = s_key(sc, flat);
         kx[q] = x_key(xs[q], flat);
       }
@@ -447,7 +494,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
       int cnt = 0;
       for (int f = threadIdx.x; f < total; f += kFinalThreads) {
         const int r = f / V;
-        cnt += s_key(score_only(lrow[f], row_lse[r], row_score[r]), (uint32_t)f) >= mid;
+        cnt += f - r * V != s.eos && s_key(score_only(lrow[f], row_lse[r], row_score[r]), (uint32_t)f) >= mid;
       }
       for (int sh = 32; sh > 0; sh >>= 1) cnt += __shfl_xor(cnt, sh);
       if (lane == 0) wsum[wave] = cnt;
@@ -464,7 +511,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
       const int r = f / V;
       const float x = lrow[f];
       const uint64_t ks = s_key(score_only(x, row_lse[r], row_score[r]), (uint32_t)f);
-      if (ks >= lo) {
+      if (ks >= lo && f - r * V != s.eos) {
         const int slot = atomicAdd(&ncand, 1);  // exactly b
         cand[slot] = ks;
         cand_x[slot] = x_key(x, (uint32_t)f);
@@ -475,6 +522,25 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
   for (int j = threadIdx.x; j < b; j += kFinalThreads) best_k[j] = best_c[j] = 0;
   __syncthreads();
   rank_topb(cand, cand_x, min(ncand, kCandMax), b, best_k, best_c);
+  // End of sequence: the EOS candidate of live row r finishes a hypothesis iff fewer than b
+  // candidates beat it: the selected non-EOS ones above it and the other rows' EOS above it.
+  int eos_rank = -1;
+  float eos_sc = 0.0f;
+  if (s.eos >= 0 && threadIdx.x < n_live) {
+    const int r = threadIdx.x;
+    eos_sc = score_only(lrow[(size_t)r * V + s.eos], row_lse[r], row_score[r]);
+    eos_key[r] = s_key(eos_sc, (uint32_t)(r * V + s.eos));
+  }
+  __syncthreads();
+  if (s.eos >= 0 && threadIdx.x < n_live) {
+    const uint64_t k = eos_key[threadIdx.x];
+    int better = 0;
+    for (int j = 0; j < b; ++j) better += best_k[j] > k;
+    for (int r = 0; r < n_live; ++r) better += eos_key[r] > k;
+    eos_rank = better < b ? better : -1;
+    eos_at[threadIdx.x] = eos_rank;
+    eos_val[threadIdx.x] = eos_sc;
+  }
   __syncthreads();
 
   for (int j = threadIdx.x; j < b; j += kFinalThreads) {
@@ -493,6 +559,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     sel_token[(size_t)t * b + j] = v;
     sel_score[(size_t)t * b + j] = sc;
     sel_logprob[(size_t)t * b + j] = lp;
+    if (j == 0 && s.eos >= 0) finish_hypotheses(s, t, n_live, eos_at, eos_val, sc);
   }
   if (lse_out != nullptr) {
     for (int r = threadIdx.x; r < b; r += kFinalThreads)

@@ -38,7 +38,8 @@ __global__ __launch_bounds__(256) void k_init_prompt(DevState s, const int32_t* 
     h.n_shared = P;
     h.leaf_depth = P - 1;
     h.next_id = P;
-    h.pad0 = h.pad1 = 0;
+    h.step = 0;
+    h.pad1 = 0;
     s.hdr[t] = h;
   }
 }
@@ -229,7 +230,8 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
         nh.n_shared = first_part < kAppThreads ? r0 + first_part : N + (b == 1 ? 1 : 0);
         nh.leaf_depth = d_new;
         nh.next_id = h.next_id + b;
-        nh.pad0 = nh.pad1 = 0;
+        nh.step = h.step + 1;
+        nh.pad1 = 0;
         s.hdr[t] = nh;
         s.n_moves[t] = 0;
       }
@@ -290,7 +292,8 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
       nh.n_shared = (r0 - e) + n_full + (b == 1 ? 1 : 0);
       nh.leaf_depth = d_new;
       nh.next_id = h.next_id + b;
-      nh.pad0 = nh.pad1 = 0;
+      nh.step = h.step + 1;
+      nh.pad1 = 0;
       s.hdr[t] = nh;
       s.n_moves[t] = n_moved;
     }
@@ -357,7 +360,8 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
       nh.n_shared = first_nf < N ? first_nf : N + (b == 1 ? 1 : 0);
       nh.leaf_depth = d_new;
       nh.next_id = h.next_id + b;
-      nh.pad0 = nh.pad1 = 0;
+      nh.step = h.step + 1;
+      nh.pad1 = 0;
       s.hdr[t] = nh;
       s.n_moves[t] = 0;
     }
@@ -473,7 +477,8 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
     nh.n_shared = (r0 - e) + full_cnt + (b == 1 ? 1 : 0);
     nh.leaf_depth = d_new;
     nh.next_id = h.next_id + b;
-    nh.pad0 = nh.pad1 = 0;
+    nh.step = h.step + 1;
+    nh.pad1 = 0;
     s.hdr[t] = nh;
     s.n_moves[t] = mv_run;
   }

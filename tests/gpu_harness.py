@@ -10,6 +10,7 @@ import sys
 import numpy as np
 
 import oracle.decode as odec
+import oracle.finished as ofin
 import oracle.trie as otrie
 import synth
 
@@ -40,19 +41,22 @@ class Run:
     """One decode run of workload ``w`` on the GPU with a CPU oracle beside it."""
 
     def __init__(self, w, seed=0, layers=None, attn_impl=0, capacity=None, mode="scripted",
-                 oracle=True, phase_events=False):
+                 oracle=True, phase_events=False, eos=-1, eos_boost=0.0, length_penalty=1.0,
+                 early_stopping=False):
         import torch
         import paper_2502_00085_amd.binding as B
         self.w, self.seed, self.mode, self.phase_events = w, seed, mode, phase_events
+        self.eos, self.eos_boost = eos, eos_boost
         self.layers = list(range(w.n_layers)) if layers is None else list(layers)
         self.cap = capacity or w.capacity
         self.scale = 1.0 / float(np.sqrt(w.head_dim))
         self.dec = B.TrieDecoder(w.n_tries, w.beam_width, self.cap, w.vocab, w.n_layers, w.n_q_heads,
                                  w.n_kv_heads, w.head_dim, w.window, w.dtype, attn_impl,
-                                 gc_interval=w.gc_interval)
+                                 gc_interval=w.gc_interval, eos_token=eos, length_penalty=length_penalty,
+                                 early_stopping=early_stopping)
         self.plens = synth.prompt_lengths(w, seed)
         tokens = np.zeros((w.n_tries, int(self.plens.max())), np.int32)
-        self.tries = []
+        self.tries, self.pools = [], []
         for t in range(w.n_tries):
             P = int(self.plens[t])
             tok, pk, pv = synth.prompt(w, t, P, seed)
@@ -63,6 +67,7 @@ class Run:
                 self.tries.append(otrie.Trie(tok, synth.as_f32(w, pk[self.layers]),
                                              synth.as_f32(w, pv[self.layers]), w.beam_width, w.window,
                                              w.gc_interval))
+                self.pools.append(ofin.FinishedPool(w.beam_width, length_penalty, early_stopping))
         self.dec.init_prompt(self.plens.tolist(), torch.from_numpy(tokens).cuda())
         self.pending = False
         self.step_no = 0
@@ -71,6 +76,8 @@ class Run:
         w = self.w
         q, kn, vn = synth.step_qkv(w, s, self.seed)
         logits = synth.step_logits(w, s, self.seed)
+        if self.eos >= 0 and self.eos_boost:
+            logits[:, :, self.eos] += np.float32(self.eos_boost)  # end-of-sequence candidates rank high
         par, tok = synth.step_script(w, s, self.seed) if self.mode == "scripted" else (None, None)
         return q, kn, vn, logits, par, tok
 
@@ -110,6 +117,8 @@ class Run:
         if ps is not None:
             res["pair_score"] = ps.cpu().numpy()
         res["state"] = [dec.read_state(t) for t in range(T)]
+        if self.eos >= 0:
+            res["finished"] = [dec.read_finished(t) for t in range(T)]
         if evs:
             res["phase_ms"] = [e.elapsed_ms() for e in evs]
             for e in evs:
@@ -132,8 +141,11 @@ class Run:
             nl = n_live[t]
             script = (par[t], tok[t]) if self.mode == "scripted" else None
             ref = odec.decode_step(tr, s, qf[:, t] if check_attn else None, knf[:, t], vnf[:, t],
-                                   logits[t], self.scale, script)
+                                   logits[t], self.scale, script, self.eos,
+                                   self.pools[t] if self.eos >= 0 else None)
             errs += compare(w, s, t, nl, self.layers, g, ref, check_attn)
+            if self.eos >= 0:
+                errs += compare_finished(s, t, g["finished"][t], self.pools[t])
         return errs, g
 
 
@@ -279,3 +291,18 @@ class BatchRun:
                 if not np.array_equal(gb["scores"].view(np.uint32), bb.scores.view(np.uint32)):
                     errs.append(f"{tag}: beam scores differ")
         return errs, g
+
+
+def compare_finished(s, t, got, pool):
+    tag = f"step {s} trie {t}"
+    errs = []
+    if got["count"] != len(pool.hyps) or got["done"] != pool.done:
+        return [f"{tag}: finished {got['count']} done {got['done']} != {len(pool.hyps)} done {pool.done}"]
+    for i, h in enumerate(pool.hyps):
+        if (int(got["step"][i]), int(got["parent"][i])) != (h.step, h.parent):
+            errs.append(f"{tag}: hypothesis {i} (step, parent) {(int(got['step'][i]), int(got['parent'][i]))} "
+                        f"!= {(h.step, h.parent)}")
+        if got["score"][i].view(np.uint32) != np.float32(h.score).view(np.uint32) or \
+                got["norm"][i].view(np.uint32) != np.float32(h.norm).view(np.uint32):
+            errs.append(f"{tag}: hypothesis {i} score/norm bits differ")
+    return errs

@@ -42,7 +42,8 @@ def test_library_exports_every_declared_symbol():
 
 def _desc(**kw):
     d = dict(n_tries=1, beam_width=8, capacity=4096, vocab=1000, n_layers=2, n_q_heads=8,
-             n_kv_heads=2, head_dim=128, window=0, dtype=B.TD_BF16, attn_impl=0, gc_interval=1, k_pool=0x10000,
+             n_kv_heads=2, head_dim=128, window=0, dtype=B.TD_BF16, attn_impl=0, gc_interval=1, eos_token=-1,
+             length_penalty=1.0, early_stopping=0, k_pool=0x10000,
              v_pool=0x20000)
     d.update(kw)
     return B.TdDesc(**d)
@@ -55,6 +56,9 @@ def _desc(**kw):
     (dict(dtype=7), "dtype"), (dict(k_pool=0), "k_pool"), (dict(v_pool=0x20004), "aligned"),
     (dict(attn_impl=2, dtype=B.TD_F32), "bf16"), (dict(vocab=2 ** 28, beam_width=16), "vocab"),
     (dict(gc_interval=0), "gc_interval"), (dict(gc_interval=-3), "gc_interval"),
+    (dict(eos_token=1000), "eos_token"), (dict(eos_token=-2), "eos_token"),
+    (dict(eos_token=3, vocab=8), "vocab - 1"), (dict(length_penalty=float("inf")), "length_penalty"),
+    (dict(early_stopping=2), "early_stopping"),
 ])
 def test_create_rejects_bad_descriptors(kw, frag):
     L = B.lib()
@@ -75,6 +79,7 @@ def test_null_context_is_rejected_by_every_call():
     assert L.td_read_state(None, 0, None) == B.TD_EINVAL
     assert L.td_load_state(None, 0, None) == B.TD_EINVAL
     assert L.td_set_kernel_events(None, B.TD_PHASE_ATTN, None, None) == B.TD_EINVAL
+    assert L.td_read_finished(None, 0, None, None, None, None, None, None) == B.TD_EINVAL
     assert L.td_status_name(B.TD_ECAPACITY) == b"TD_ECAPACITY"
 
 
