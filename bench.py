@@ -71,6 +71,9 @@ def parse():
                    help="also run one plain device copy of this many MiB (reference for HBM counters)")
     p.add_argument("--no-batch-baseline", action="store_true",
                    help="skip the batch-based beam search baseline on the same inputs")
+    p.add_argument("--eos", type=int, default=-1, help="end-of-sequence token (-1: none)")
+    p.add_argument("--eos-boost", type=float, default=0.0,
+                   help="added to every row's EOS logit, so that hypotheses finish")
     p.add_argument("--gc-interval", type=int, default=0,
                    help="garbage-collection interval g (0: the workload's)")
     p.add_argument("--input-period", type=int, default=0,
@@ -84,7 +87,7 @@ def log(*a):
 
 
 class Bench:
-    def __init__(self, w, steps, seed, input_period=0):
+    def __init__(self, w, steps, seed, input_period=0, eos=-1, eos_boost=0.0):
         import torch
         import paper_2502_00085_amd.binding as B
         self.B, self.torch, self.w, self.seed = B, torch, w, seed
@@ -93,7 +96,8 @@ class Bench:
         self.scale = 1.0 / float(np.sqrt(w.head_dim))
         t0 = time.time()
         self.dec = B.TrieDecoder(w.n_tries, w.beam_width, self.cap, w.vocab, w.n_layers, w.n_q_heads,
-                                 w.n_kv_heads, w.head_dim, w.window, w.dtype, gc_interval=w.gc_interval)
+                                 w.n_kv_heads, w.head_dim, w.window, w.dtype, gc_interval=w.gc_interval,
+                                 eos_token=eos)
         self.plens = synth.prompt_lengths(w, seed)
         tokens = np.zeros((w.n_tries, int(self.plens.max())), np.int32)
         for t in range(w.n_tries):
@@ -115,7 +119,10 @@ class Bench:
                 self.q.append(self.dev(q))
                 self.kn.append(self.dev(kn))
                 self.vn.append(self.dev(vn))
-                self.logits.append(torch.from_numpy(synth.step_logits(w, s, seed)).cuda())
+                lg = synth.step_logits(w, s, seed)
+                if eos >= 0 and eos_boost:
+                    lg[:, :, eos] += np.float32(eos_boost)
+                self.logits.append(torch.from_numpy(lg).cuda())
             if s % 100 == 0:
                 log(f"[bench] inputs of {s} steps drawn")
             par, tok = synth.step_script(w, s, seed)
@@ -201,7 +208,7 @@ def gpu_bench(args, w, K):
         torch.cuda.synchronize()
         log(f"[bench] reference copy: {args.copy_ref_mib} MiB read + {args.copy_ref_mib} MiB written")
         del src, dst
-    bench = Bench(w, K, args.seed, args.input_period)
+    bench = Bench(w, K, args.seed, args.input_period, args.eos, args.eos_boost)
     stream = torch.cuda.current_stream().cuda_stream
     # warmup (eager)
     bench.init()
@@ -254,6 +261,7 @@ def gpu_bench(args, w, K):
     status = bench.dec.status()
     if status != 0:
         raise RuntimeError(f"device status {status} after the timed run")
+    finished = [bench.dec.read_finished(t) for t in range(w.n_tries)] if args.eos >= 0 else None
     attn_graph_ms, attn_graph_nodes = attn_graph_time(bench, K, args.attn_reps)
     phase_ms = phase_times(bench, K)
     nodes = bench.nodes_per_step(K)
@@ -262,7 +270,7 @@ def gpu_bench(args, w, K):
     batch = None if args.no_batch_baseline else batch_bench(bench, K, args.warmup)
     return dict(mode=mode, seconds=t1 - t0, eager_seconds=eager_s, attn_ms=attn_ms, nodes=nodes,
                 attn_graph_ms=attn_graph_ms, attn_graph_nodes=attn_graph_nodes, phase_ms=phase_ms,
-                collects=collects, stored=bench.stored, batch=batch)
+                collects=collects, stored=bench.stored, batch=batch, finished=finished)
 
 
 def batch_bench(bench, K, warmup):
@@ -363,6 +371,7 @@ def gc_summary(w, ph, collects):
     tenth = max(1, K // 10)
     out = {"interval": w.gc_interval, "collections": int(len(idx)), "steps": K,
            "decode_pass_us": round(float(dec.mean()), 2),
+           "attention_us": round(float(us[:, 0].mean()), 2), "topb_us": round(float(us[:, 2].mean()), 2),
            "decode_pass_us_first_tenth": round(float(dec[:tenth].mean()), 2),
            "decode_pass_us_last_tenth": round(float(dec[-tenth:].mean()), 2),
            "append_us_without_collection": round(float(us[other, 3].mean()), 2) if other.any() else None,
@@ -502,6 +511,7 @@ def main():
                    "kv_heads": w.n_kv_heads, "head_dim": w.head_dim, "tries": w.n_tries,
                    "prompt": [w.prompt_min, w.prompt_max], "beam_width": w.beam_width,
                    "vocab": w.vocab, "window": w.window, "gc_interval": w.gc_interval,
+                   "eos_token": args.eos, "eos_boost": args.eos_boost,
                    "growth": f"scripted, parent rank ~ (r+1)^-{w.alpha}", "launch": r["mode"]},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
@@ -531,6 +541,10 @@ def main():
                     "buffer not counted)"}
     if args.input_period > 0:
         out["data"] = f"synthetic, inputs of {args.input_period} steps reused in turn"
+    if r["finished"] is not None:
+        out["eos"] = {"finished_per_trie": [f["count"] for f in r["finished"]],
+                      "done_per_trie": [f["done"] for f in r["finished"]],
+                      "best_norm": [float(f["norm"][0]) if f["count"] else None for f in r["finished"]]}
     if not args.no_cpu_baseline and not args.profile_only:
         out["cpu_baseline"] = cpu_baseline(w, args.seed, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -120,6 +120,7 @@ td_status bbs_create(const bbs_desc* d, bbs_ctx** out) {
   a.W = d->window;
   a.dtype = d->dtype;
   a.G = 1;
+  a.eos = -1;
   a.attn_pairs_max = 1024;
   a.attn_part_floats = a.attn_pairs_max * 32 * (a.D + 2);
   td::DevState& s = c->sel;
@@ -134,6 +135,7 @@ td_status bbs_create(const bbs_desc* d, bbs_ctx** out) {
   s.D = d->head_dim;
   s.dtype = d->dtype;
   s.G = 1;
+  s.eos = -1;  // the baseline has no end-of-sequence handling (no finished-hypothesis pool)
   s.lse_chunks = (s.V + td::kLseChunk - 1) / td::kLseChunk;
   s.topk_half = (size_t)T * b * s.lse_chunks * 16;
   hipError_t e;

@@ -26,16 +26,16 @@ struct TrieHdr {
 struct DevState {
   int T, b, cap, V, L, Hq, Hkv, D, W, dtype;
   int G;                 // garbage-collection interval g (>= 1)
-  int eos;               // end-of-sequence token, -1 = none
-  float alpha;           // length penalty
-  int early;             // early stopping
+  int eos = -1;          // end-of-sequence token, -1 = none (then the fin_* arrays are unused)
+  float alpha = 1.0f;    // length penalty
+  int early = 0;         // early stopping
   // finished hypotheses (eos >= 0): [T][b], best first, and per trie the count and done flag
-  float* fin_norm;
-  float* fin_score;
-  int32_t* fin_step;
-  int32_t* fin_parent;
-  int32_t* fin_count;    // [T]
-  int32_t* fin_done;     // [T]
+  float* fin_norm = nullptr;
+  float* fin_score = nullptr;
+  int32_t* fin_step = nullptr;
+  int32_t* fin_parent = nullptr;
+  int32_t* fin_count = nullptr;  // [T]
+  int32_t* fin_done = nullptr;   // [T]
   void* k_pool;
   void* v_pool;
   TrieHdr* hdr;          // [T]

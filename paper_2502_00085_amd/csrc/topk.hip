@@ -277,25 +277,23 @@ __device__ inline float length_norm(float score, int length, float alpha) {
   return (float)((double)score / pow((double)length, (double)alpha));
 }
 
-// Adds the step's finishing EOS candidates (row r finishes iff rank[r] >= 0), in rank
-// order, to trie t's pool of the b best finished hypotheses (best first; a newcomer goes
-// after the entries it ties), then sets the done flag.  One thread; best_next = the score
-// of the best next beam.
-__device__ inline void finish_hypotheses(const DevState& s, int t, int n_live, const int* rank,
-                                         const float* val, float best_next) {
-  if (s.fin_done[t]) return;
+// Adds the step's finishing EOS candidates (bit k of `ranks`: the EOS candidate of row
+// row[k], score val[k], holds rank k of the step's ranking), in rank order, to trie t's
+// pool of the b best finished hypotheses (best first; a newcomer goes after the entries it
+// ties), then sets the done flag.  One thread, for a trie that is not done; best_next =
+// the score of the best next beam, count = the pool's size, step = this decode step.
+__device__ inline void finish_hypotheses(const DevState& s, int t, uint64_t ranks, const int* row,
+                                         const float* val, float best_next, int count, int step) {
   const int b = s.b;
-  const int step = s.hdr[t].step + 1;
   float* norm = s.fin_norm + (size_t)t * b;
   float* score = s.fin_score + (size_t)t * b;
   int32_t* stp = s.fin_step + (size_t)t * b;
   int32_t* par = s.fin_parent + (size_t)t * b;
-  int count = s.fin_count[t];
-  for (int k = 0; k < b; ++k) {  // rank k of this step's ranking, if an EOS candidate holds it
-    int r = -1;
-    for (int i = 0; i < n_live; ++i) r = rank[i] == k ? i : r;
-    if (r < 0) continue;
-    const float nv = length_norm(val[r], step, s.alpha);
+  const int count0 = count;
+  for (uint64_t m = ranks; m != 0ull; m &= m - 1ull) {
+    const int k = __ffsll((unsigned long long)m) - 1;
+    const int r = row[k];
+    const float nv = length_norm(val[k], step, s.alpha);
     int p = count;
     while (p > 0 && norm[p - 1] < nv) --p;
     if (p >= b) continue;
@@ -306,12 +304,12 @@ __device__ inline void finish_hypotheses(const DevState& s, int t, int n_live, c
       par[q] = par[q - 1];
     }
     norm[p] = nv;
-    score[p] = val[r];
+    score[p] = val[k];
     stp[p] = step;
     par[p] = r;
     count = min(count + 1, b);
   }
-  s.fin_count[t] = count;
+  if (count != count0) s.fin_count[t] = count;
   if (count == b && (s.early || norm[b - 1] >= length_norm(best_next, step, s.alpha))) s.fin_done[t] = 1;
 }
 
@@ -332,8 +330,8 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
   __shared__ float row_lse[kMaxBeam], row_score[kMaxBeam];
   __shared__ int ncand, nhot;
   __shared__ uint64_t eos_key[kMaxBeam];
-  __shared__ int eos_at[kMaxBeam];
-  __shared__ float eos_val[kMaxBeam];
+  __shared__ int acc_row[kMaxBeam];
+  __shared__ float acc_val[kMaxBeam];
   __shared__ int hot[kCandMax];
   const float* lrow = logits + (size_t)t * b * V;
   // Entry j of wave w is sub-chunk w of (row j / nch, chunk j % nch): every wave covers
@@ -360,6 +358,17 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     pp = pair_parent[(size_t)t * b + pj];
     pv = pair_token[(size_t)t * b + pj];
     if (pp >= 0 && pp < b && pv >= 0 && pv < V) pair_x = lrow[(size_t)pp * V + pv];
+  }
+  // end of sequence: every row's EOS logit (thread r), and the pool's state (thread 0)
+  float eos_x = 0.0f;
+  int pool_done = 1, pool_count = 0, pool_step = 0;
+  if (s.eos >= 0) {
+    if (threadIdx.x < b) eos_x = lrow[(size_t)threadIdx.x * V + s.eos];
+    if (threadIdx.x == 0) {
+      pool_done = s.fin_done[t];
+      pool_count = s.fin_count[t];
+      pool_step = s.hdr[t].step + 1;
+    }
   }
   for (int r = threadIdx.x; r < b; r += kFinalThreads) row_score[r] = s.leaf_score[(size_t)t * b + r];
   for (int r = wave; r < b; r += kFinalWaves) {
@@ -524,12 +533,16 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
   rank_topb(cand, cand_x, min(ncand, kCandMax), b, best_k, best_c);
   // End of sequence: the EOS candidate of live row r finishes a hypothesis iff fewer than b
   // candidates beat it: the selected non-EOS ones above it and the other rows' EOS above it.
-  int eos_rank = -1;
+  // Finishing candidates are recorded by rank (acc_row / acc_val); bit k of acc_mask (wave
+  // 0) marks rank k.
   float eos_sc = 0.0f;
-  if (s.eos >= 0 && threadIdx.x < n_live) {
+  if (s.eos >= 0 && threadIdx.x < b) {
     const int r = threadIdx.x;
-    eos_sc = score_only(lrow[(size_t)r * V + s.eos], row_lse[r], row_score[r]);
-    eos_key[r] = s_key(eos_sc, (uint32_t)(r * V + s.eos));
+    acc_row[r] = -1;
+    if (r < n_live) {
+      eos_sc = score_only(eos_x, row_lse[r], row_score[r]);
+      eos_key[r] = s_key(eos_sc, (uint32_t)(r * V + s.eos));
+    }
   }
   __syncthreads();
   if (s.eos >= 0 && threadIdx.x < n_live) {
@@ -537,11 +550,13 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     int better = 0;
     for (int j = 0; j < b; ++j) better += best_k[j] > k;
     for (int r = 0; r < n_live; ++r) better += eos_key[r] > k;
-    eos_rank = better < b ? better : -1;
-    eos_at[threadIdx.x] = eos_rank;
-    eos_val[threadIdx.x] = eos_sc;
+    if (better < b) {
+      acc_row[better] = threadIdx.x;
+      acc_val[better] = eos_sc;
+    }
   }
   __syncthreads();
+  const uint64_t acc_mask = s.eos >= 0 && wave == 0 ? __ballot(lane < b && acc_row[lane] >= 0) : 0ull;
 
   for (int j = threadIdx.x; j < b; j += kFinalThreads) {
     const uint64_t kx = best_c[j];
@@ -559,7 +574,8 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     sel_token[(size_t)t * b + j] = v;
     sel_score[(size_t)t * b + j] = sc;
     sel_logprob[(size_t)t * b + j] = lp;
-    if (j == 0 && s.eos >= 0) finish_hypotheses(s, t, n_live, eos_at, eos_val, sc);
+    if (j == 0 && s.eos >= 0 && !pool_done)
+      finish_hypotheses(s, t, acc_mask, acc_row, acc_val, sc, pool_count, pool_step);
   }
   if (lse_out != nullptr) {
     for (int r = threadIdx.x; r < b; r += kFinalThreads)
