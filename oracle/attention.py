@@ -7,6 +7,10 @@ the output of leaf i is ordinary softmax attention over exactly the nodes of
 that path.  This module computes that definition directly: materialise the
 path, then dense softmax attention over it, in float64.
 
+``tree_attention`` generalises this to any set of query nodes, several per branch (Alg 3's
+mask with one row per query node, as drawn in Figure 3): the prefill of a serialized trie,
+or the verification of a draft tree hung under the leaves.
+
 Conventions (standard model attention): query head h reads KV head
 ``h // (Hq / Hkv)`` (grouped-query attention with contiguous groups); the
 scores are scaled by ``scale`` (normally 1/sqrt(d)); the query attends to its
@@ -58,3 +62,35 @@ def path_weights(trie, q: np.ndarray, scale: float, layer: int, leaf: int, head:
     z = z - z.max()
     p = np.exp(z)
     return p / p.sum()
+
+
+def node_path(trie, node):
+    """Root-to-node ancestor path of any stored node, clipped to the node's window."""
+    p = trie.path(node)
+    if trie.window > 0:
+        p = [n for n in p if node.depth - n.depth < trie.window]
+    return p
+
+
+def tree_attention(trie, slots, q: np.ndarray, scale: float) -> np.ndarray:
+    """Multi-query tree attention (Alg 3's mask with one row per query node, Figure 3): the
+    query of stored node ``slots[j]`` attends to that node's visible root path.  A slot of
+    -1, or of a node on no live leaf's path (a dead node awaiting collection), has no keys:
+    its output is zero.
+
+    q: [L'][Q][Hq][d].  Returns [L'][Q][Hq][d] float64."""
+    n_layers, nq, n_q_heads, d = q.shape
+    out = np.zeros((n_layers, nq, n_q_heads, d), dtype=np.float64)
+    alive = trie.alg3_mask() != 0
+    for j, slot in enumerate(slots):
+        if slot < 0 or not alive[slot]:
+            continue
+        path = node_path(trie, trie.order[slot])
+        for li in range(n_layers):
+            kp = np.stack([n.k[li] for n in path]).astype(np.float64)
+            vp = np.stack([n.v[li] for n in path]).astype(np.float64)
+            group = n_q_heads // kp.shape[1]
+            for h in range(n_q_heads):
+                out[li, j, h] = softmax_attention(q[li, j, h].astype(np.float64), kp[:, h // group, :],
+                                                  vp[:, h // group, :], scale)
+    return out

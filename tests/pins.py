@@ -554,3 +554,105 @@ def pin_pool_is_best_of_events(seed, steps=40, b=4, alpha=0.8):
     best = sorted(events, key=lambda e: (-float(np.float32(e[0])), e[1]))[:b]
     assert [(h.step, h.parent, float(h.score)) for h in pool.hyps] == [(e[2], e[3], e[4]) for e in best]
     assert pool.done == (done_at is not None)
+
+
+# --------------------------------------------------------------------------------------------
+# multi-query tree attention
+# --------------------------------------------------------------------------------------------
+def grown_trie_with_kv(w, seed, steps):
+    """A trie after `steps` scripted decode steps with every node's K/V written (the last
+    leaves' too), and the K/V rows that wrote them."""
+    tok, pk, pv = _prompt(w, seed)
+    trie = otrie.Trie(tok, pk, pv, w.beam_width, w.window, w.gc_interval)
+    scale = 1.0 / np.sqrt(w.head_dim)
+    for s in range(1, steps + 1):
+        q, kn, vn, logits = _step_inputs(w, s, seed)
+        par, tk = synth.step_script(w, s, seed)
+        odec.decode_step(trie, s, None, kn, vn, logits, scale, (par[0], tk[0]))
+    _, kn, vn, _ = _step_inputs(w, steps + 1, seed)
+    trie.write_leaf_kv(kn[:, :trie.n_live], vn[:, :trie.n_live])
+    return trie
+
+
+def pin_tree_at_leaves_is_decode_attention(w, seed, steps=6):
+    """Queries at the live leaves: tree attention is the decode attention of Section 3.3."""
+    trie = grown_trie_with_kv(w, seed, steps)
+    g = np.random.default_rng(seed)
+    q = g.standard_normal((w.n_layers, trie.n_live, w.n_q_heads, w.head_dim)).astype(np.float32)
+    slots = trie.state()["leaf_slot"]
+    a = oatt.tree_attention(trie, slots, q, 0.3)
+    b = oatt.path_attention(trie, q, 0.3)
+    assert np.array_equal(a, b)
+
+
+def ancestors_by_walk(trie):
+    """A[n][m] = slot m is node n or one of its ancestors (walking parent pointers)."""
+    slot = {id(n): i for i, n in enumerate(trie.order)}
+    N = len(trie.order)
+    anc = np.zeros((N, N), dtype=bool)
+    for i, n in enumerate(trie.order):
+        x = n
+        while x is not None:
+            anc[i, slot[id(x)]] = True
+            x = x.parent
+    return anc
+
+
+def pin_ancestry_is_mask_containment(w, seed, steps=8):
+    """For live nodes, m is an ancestor-or-self of n exactly when depth(m) <= depth(n) and
+    m's leaf mask contains n's (every leaf below n lies below m): the test the device uses."""
+    trie = grown_trie_with_kv(w, seed, steps)
+    anc = ancestors_by_walk(trie)
+    st = trie.state()
+    m, dep = st["mask"], st["depth"]
+    live = np.nonzero(m != 0)[0]
+    for n in live:
+        for k in live:
+            rule = dep[k] <= dep[n] and (int(m[k]) & int(m[n])) == int(m[n])
+            assert rule == anc[n, k], (n, k)
+
+
+def pin_tree_dense_mask(w, seed, steps=6):
+    """All live nodes as queries against dense attention (torch SDPA, float64) over every
+    stored node with the square mask of Figure 3 (ancestor-or-self, within the window)."""
+    import torch
+    import torch.nn.functional as F
+    trie = grown_trie_with_kv(w, seed, steps)
+    anc = ancestors_by_walk(trie)
+    dep = np.array([n.depth for n in trie.order])
+    if w.window > 0:
+        anc &= (dep[:, None] - dep[None, :]) < w.window
+    live = trie.alg3_mask() != 0
+    slots = np.nonzero(live)[0]
+    g = np.random.default_rng(seed)
+    q = g.standard_normal((w.n_layers, len(slots), w.n_q_heads, w.head_dim)).astype(np.float32)
+    scale = 0.25
+    got = oatt.tree_attention(trie, slots, q, scale)
+    add = torch.from_numpy(np.where(anc[slots], 0.0, -np.inf))
+    G = w.n_q_heads // w.n_kv_heads
+    for li in range(w.n_layers):
+        kk = torch.from_numpy(np.stack([n.k[li] for n in trie.order], axis=1).astype(np.float64))
+        vv = torch.from_numpy(np.stack([n.v[li] for n in trie.order], axis=1).astype(np.float64))
+        qq = torch.from_numpy(q[li].astype(np.float64)).transpose(0, 1)  # [Hq][Q][d]
+        ref = F.scaled_dot_product_attention(qq, kk.repeat_interleave(G, 0), vv.repeat_interleave(G, 0),
+                                             attn_mask=add, scale=scale)
+        err = float(np.max(np.abs(ref.transpose(0, 1).numpy() - got[li])))
+        assert err <= 1e-12, err
+
+
+def pin_tree_chain_is_causal(seed, P=24):
+    """A prompt chain with every node as a query is causal self-attention (torch SDPA with
+    is_causal, float64)."""
+    import torch
+    import torch.nn.functional as F
+    w = small_workload(b=1, P=P, L=1, Hq=2, Hkv=2, d=8)
+    tok, pk, pv = _prompt(w, seed)
+    trie = otrie.Trie(tok, pk, pv, 1)
+    g = np.random.default_rng(seed)
+    q = g.standard_normal((1, P, 2, 8)).astype(np.float32)
+    got = oatt.tree_attention(trie, np.arange(P), q, 0.5)
+    qq = torch.from_numpy(q[0].astype(np.float64)).transpose(0, 1)
+    kk = torch.from_numpy(pk[0].astype(np.float64))
+    vv = torch.from_numpy(pv[0].astype(np.float64))
+    ref = F.scaled_dot_product_attention(qq, kk, vv, is_causal=True, scale=0.5)
+    assert float(np.max(np.abs(ref.transpose(0, 1).numpy() - got[0]))) <= 1e-12

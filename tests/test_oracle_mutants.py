@@ -206,3 +206,17 @@ def test_mutant_done_on_raw_scores(monkeypatch):
         self.done = self.early or bool(self.worst() >= np.float32(best_next_score))
     monkeypatch.setattr(ofin.FinishedPool, "update_done", bad)
     _fails(pins.pin_pool_is_best_of_events, 63)
+
+
+def test_mutant_tree_query_skips_itself(monkeypatch):
+    monkeypatch.setattr(oatt, "node_path", lambda trie, node: trie.path(node)[:-1] or trie.path(node))
+    _fails(pins.pin_tree_dense_mask, pins.small_workload(b=4, V=30), 79)
+
+
+def test_mutant_tree_window_from_the_leaves(monkeypatch):
+    # the window measured from the deepest leaf instead of the query node
+    def bad(trie, node):
+        p = trie.path(node)
+        return [n for n in p if trie.leaf_depth - n.depth < trie.window] or p[-1:]
+    monkeypatch.setattr(oatt, "node_path", bad)
+    _fails(pins.pin_tree_dense_mask, pins.small_workload(b=4, V=30, W=3), 80)

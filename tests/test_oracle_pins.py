@@ -114,3 +114,22 @@ def test_eos_greedy_length_convention():
 @pytest.mark.parametrize("seed", [57, 58, 59])
 def test_finished_pool_is_the_best_of_its_events(seed):
     pins.pin_pool_is_best_of_events(seed)
+
+
+@pytest.mark.parametrize("W,g,seed", [(0, 1, 70), (4, 1, 71), (0, 3, 72)])
+def test_tree_attention_at_the_leaves_is_decode_attention(W, g, seed):
+    pins.pin_tree_at_leaves_is_decode_attention(pins.small_workload(b=4, V=30, W=W, g=g), seed)
+
+
+@pytest.mark.parametrize("b,alpha,seed", [(3, 1.0, 73), (5, 0.0, 74), (8, 0.5, 75)])
+def test_ancestry_is_mask_containment(b, alpha, seed):
+    pins.pin_ancestry_is_mask_containment(pins.small_workload(b=b, V=30, alpha=alpha), seed)
+
+
+@pytest.mark.parametrize("W,seed", [(0, 76), (3, 77)])
+def test_tree_attention_equals_dense_fig3_mask(W, seed):
+    pins.pin_tree_dense_mask(pins.small_workload(b=4, V=30, W=W), seed)
+
+
+def test_tree_attention_of_a_chain_is_causal():
+    pins.pin_tree_chain_is_causal(78)
