@@ -219,4 +219,4 @@ def test_mutant_tree_window_from_the_leaves(monkeypatch):
         p = trie.path(node)
         return [n for n in p if trie.leaf_depth - n.depth < trie.window] or p[-1:]
     monkeypatch.setattr(oatt, "node_path", bad)
-    _fails(pins.pin_tree_dense_mask, pins.small_workload(b=4, V=30, W=3), 80)
+    _fails(pins.pin_tree_dense_mask, pins.small_workload(b=4, V=30, W=3, g=4), 80)

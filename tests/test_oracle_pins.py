@@ -126,9 +126,9 @@ def test_ancestry_is_mask_containment(b, alpha, seed):
     pins.pin_ancestry_is_mask_containment(pins.small_workload(b=b, V=30, alpha=alpha), seed)
 
 
-@pytest.mark.parametrize("W,seed", [(0, 76), (3, 77)])
-def test_tree_attention_equals_dense_fig3_mask(W, seed):
-    pins.pin_tree_dense_mask(pins.small_workload(b=4, V=30, W=W), seed)
+@pytest.mark.parametrize("W,g,seed", [(0, 1, 76), (3, 1, 77), (3, 4, 81)])
+def test_tree_attention_equals_dense_fig3_mask(W, g, seed):
+    pins.pin_tree_dense_mask(pins.small_workload(b=4, V=30, W=W, g=g), seed)
 
 
 def test_tree_attention_of_a_chain_is_causal():
