@@ -142,6 +142,21 @@ td_status trie_attn_decode(td_ctx* ctx, int32_t layer_begin, int32_t n_layers, c
                            const void* d_k_new, const void* d_v_new, void* d_out, float scale,
                            hipStream_t stream);
 
+/* Multi-query tree attention (Section 3.3, Alg 3's mask with one row per query node, as
+ * in Figure 3): the prefill of a serialized trie, or the verification of draft nodes hung
+ * under the leaves.  For every trie t and j < q_max, the query of the stored node at
+ * logical slot d_qslots[t][j] attends to that node's root path - its ancestors and itself
+ * - restricted to keys with depth(q) - depth < W when a window is set:
+ * out = softmax(scale * q.K^T) V over those keys, query head h using KV head h / (Hq/Hkv).
+ * d_qslots [T][q_max] int32 device (-1 = no query); d_q, d_out [nl][T][q_max][Hq][d]
+ * (desc.dtype), layers [layer_begin, +n_layers).  A row with no query, or whose node lies
+ * on no live leaf's path (a dead node awaiting collection), is written as zeros.  Every
+ * node's K/V must be in the pools: TD_ESTATE while the leaves' rows are pending.  Needs the
+ * matrix-core kernel (bf16, attn_impl != TD_ATTN_VALU), else TD_EUNSUPPORTED. */
+td_status trie_tree_attn(td_ctx* ctx, int32_t layer_begin, int32_t n_layers, int32_t q_max,
+                         const int32_t* d_qslots, const void* d_q, void* d_out, float scale,
+                         hipStream_t stream);
+
 /* Phases of a decode step that td_set_kernel_events can time. */
 typedef enum {
   TD_PHASE_ATTN = 0,    /* trie_attn_decode: the attention kernel (and its split combine)   */

@@ -8,4 +8,5 @@ from .binding import (BatchBeamDecoder, TD_ATTN_AUTO, TD_ATTN_MFMA, TD_ATTN_VALU
                       TD_PHASE_APPEND, TD_PHASE_ATTN, TD_PHASE_MOVES, TD_PHASE_TOPB, KernelEvents,
                       TdError, TrieDecoder, beam_logsoftmax_topk, lib, td_create, td_destroy,
                       td_get_status, td_init_prompt, td_load_state, td_read_state,
-                      td_set_kernel_events, trie_append_prune, trie_attn_decode)
+                      td_set_kernel_events, trie_append_prune, trie_attn_decode,
+                      trie_tree_attn)

@@ -85,6 +85,7 @@ def lib() -> ctypes.CDLL:
         L.td_get_status.argtypes = [vp]
         L.td_set_kernel_events.argtypes = [vp, i32, vp, vp]
         L.td_read_finished.argtypes = [vp, i32, vp, vp, vp, vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+        L.trie_tree_attn.argtypes = [vp, i32, i32, i32, vp, vp, vp, f32, vp]
         L.td_error_string.argtypes = [vp]
         L.td_error_string.restype = ctypes.c_char_p
         L.td_status_name.argtypes = [i32]
@@ -102,7 +103,7 @@ def lib() -> ctypes.CDLL:
         L.bbs_error_string.restype = ctypes.c_char_p
         for name in ("td_create", "td_destroy", "td_init_prompt", "trie_attn_decode",
                      "beam_logsoftmax_topk", "trie_append_prune", "td_read_state", "td_load_state",
-                     "td_get_status", "td_set_kernel_events", "td_read_finished", "bbs_create", "bbs_destroy",
+                     "td_get_status", "td_set_kernel_events", "td_read_finished", "trie_tree_attn", "bbs_create", "bbs_destroy",
                      "bbs_init_prompt", "batch_beam_attn_decode", "batch_beam_logsoftmax_topk",
                      "batch_beam_reorder", "bbs_current_cache", "bbs_read_beams", "bbs_get_status"):
             getattr(L, name).restype = ctypes.c_int32
@@ -182,6 +183,21 @@ def trie_attn_decode(ctx, dims: Dims, layer_begin: int, n_layers: int, q, k_new,
     _check(ctx, lib().trie_attn_decode(
         ctx, int(layer_begin), int(n_layers), _ptr(q, tdt, nq, "q"), _ptr(k_new, tdt, nk, "k_new"),
         _ptr(v_new, tdt, nk, "v_new"), _ptr(out, tdt, nq, "out"), float(scale), _stream(stream)))
+
+
+def trie_tree_attn(ctx, dims: Dims, layer_begin: int, n_layers: int, qslots, q, out, scale: float,
+                   stream=None):
+    """Multi-query tree attention: qslots [T][q_max] int32 (-1 = none), q / out
+    [n_layers][T][q_max][Hq][d]."""
+    import torch
+    tdt = torch.float32 if dims.dtype == TD_F32 else torch.bfloat16
+    if qslots.dim() != 2 or qslots.shape[0] != dims.T:
+        raise ValueError("qslots must be [T][q_max]")
+    qmax = int(qslots.shape[1])
+    nq = n_layers * dims.T * qmax * dims.Hq * dims.D
+    _check(ctx, lib().trie_tree_attn(ctx, int(layer_begin), int(n_layers), qmax,
+                                     _ptr(qslots, torch.int32, dims.T * qmax, "qslots"), _ptr(q, tdt, nq, "q"),
+                                     _ptr(out, tdt, nq, "out"), float(scale), _stream(stream)))
 
 
 def td_set_kernel_events(ctx, phase, start, stop):
@@ -355,6 +371,9 @@ class TrieDecoder:
 
     def read_finished(self, trie=0):
         return td_read_finished(self.ctx, self.dims, trie)
+
+    def tree_attn(self, layer_begin, n_layers, qslots, q, out, scale, stream=None):
+        trie_tree_attn(self.ctx, self.dims, layer_begin, n_layers, qslots, q, out, scale, stream)
 
     def status(self):
         return td_get_status(self.ctx)

@@ -25,10 +25,11 @@ __global__ __launch_bounds__(256) void k_attn_combine(DevState s, AttnArgs a, in
   const int n_live = s.hdr[t].n_live;
   const float* part = s.attn_part + (size_t)unit * a.splits * R * (D + 2);
   T* outp = static_cast<T*>(a.out);
+  const int nrows = a.tree ? a.qmax : s.b;  // row owners per trie in out
   for (int idx = threadIdx.x; idx < R * D; idx += blockDim.x) {
     const int i = idx / D, c = idx % D;
     const int rr = rb * R + i;
-    if (rr >= s.b * G) continue;
+    if (rr >= nrows * G) continue;
     float M = -1.0e30f;
     for (int sp = 0; sp < a.splits; ++sp) M = fmaxf(M, part[((size_t)sp * R + i) * (D + 2) + D]);
     float L = 0.0f, O = 0.0f;
@@ -39,8 +40,8 @@ __global__ __launch_bounds__(256) void k_attn_combine(DevState s, AttnArgs a, in
       O += pp[c] * f;
     }
     const int bm = rr / G;
-    const float val = (bm < n_live && L > 0.0f) ? O / L : 0.0f;
-    outp[((((size_t)li * s.T + t) * s.b + bm) * s.Hq + g * G + rr % G) * D + c] = (T)val;
+    const float val = ((a.tree || bm < n_live) && L > 0.0f) ? O / L : 0.0f;
+    outp[((((size_t)li * s.T + t) * nrows + bm) * s.Hq + g * G + rr % G) * D + c] = (T)val;
   }
 }
 

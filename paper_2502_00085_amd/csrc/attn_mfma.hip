@@ -72,7 +72,14 @@ __device__ inline int phys_chunk(int r, int c) {
 constexpr int kWaitVmAll = 0 | (7 << 4) | (15 << 8);            // vmcnt(0)
 constexpr int kWaitLgkmAll = 15 | (3 << 14) | (7 << 4) | (0 << 8);  // lgkmcnt(0)
 
-template <int D, int NW>
+// TREE: multi-query tree attention.  The rows are (query node, query head) instead of
+// (live leaf, query head): query j of trie t is the node at logical slot a.qslots[t][j]
+// (-1: none), and key node m is visible to it iff it is an ancestor-or-self: depth(m) <=
+// depth(q) and mask(m) contains mask(q) (for nodes on a live path these are the same
+// relation), within the window of the query's depth.  A block's key range ends at its
+// deepest query slot (ancestors precede their descendants in slot order) and starts at the
+// window of its shallowest query.  Nothing is pending: no leaf rows, no moves.
+template <int D, int NW, bool TREE>
 __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   using C = MfmaCfg<D, NW>;
   __shared__ __attribute__((aligned(16))) unsigned char lds[C::LDS];
@@ -81,11 +88,53 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   const int N = h.n_nodes, base = h.base, n_live = h.n_live, Dq = h.leaf_depth;
   const int G = s.Hq / s.Hkv;
   const int lab = a.layer_begin + u.li;
-
-  const int lo = window_lo(s, u.t, base, N, Dq);
-  const int per = (N - lo + a.splits - 1) / a.splits;
-  const int n0 = lo + u.split * per, n1 = min(N, n0 + per);
   const int lane = threadIdx.x & 63;
+  const int col = lane & 31, hh = lane >> 5;
+  const uint64_t* maskp = s.mask + (size_t)u.t * s.cap + base;
+  const int32_t* depthp = s.depth + (size_t)u.t * s.cap + base;
+
+  // this lane's query row: r = (leaf or query node) * G + query head within the group
+  const int r = u.rb * kRows + col;
+  const int nrows = TREE ? a.qmax : s.b;  // row owners per trie in q / out
+  const int owner = r / G;                // leaf rank, or query index
+  bool row_ok;
+  uint64_t qmask = 0;
+  int qdepth = -1;  // (TREE) no key is visible to a row without a live query node
+  int lo, n0, n1;
+  if constexpr (TREE) {
+    __shared__ int qrange[2];  // the block's key range end, its shallowest query depth
+    int slot = r < a.qmax * G ? a.qslots[(size_t)u.t * a.qmax + owner] : -1;
+    row_ok = slot >= 0 && slot < N;
+    if (row_ok) {
+      qmask = maskp[slot];
+      row_ok = qmask != 0ull;
+    }
+    if (row_ok) qdepth = depthp[slot];
+    if (threadIdx.x < 64) {  // wave 0 holds every row of the block (lanes 32..63 repeat them)
+      int hi = row_ok ? slot + 1 : 0, dmin = row_ok ? qdepth : INT_MAX;
+      for (int o = 16; o > 0; o >>= 1) {
+        hi = max(hi, __shfl_xor(hi, o));
+        dmin = min(dmin, __shfl_xor(dmin, o));
+      }
+      if (threadIdx.x == 0) {
+        qrange[0] = hi;
+        qrange[1] = dmin;
+      }
+    }
+    __syncthreads();
+    const int hi = qrange[0];
+    lo = hi > 0 ? window_lo(s, u.t, base, N, qrange[1]) : 0;
+    const int span = max(0, hi - lo);
+    const int per = (span + a.splits - 1) / a.splits;
+    n0 = lo + u.split * per;
+    n1 = min(lo + span, n0 + per);
+  } else {
+    row_ok = r < s.b * G && owner < n_live;
+    lo = window_lo(s, u.t, base, N, Dq);
+    const int per = (N - lo + a.splits - 1) / a.splits;
+    n0 = lo + u.split * per;
+    n1 = min(N, n0 + per);
+  }
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
   // Rows moved by the last compaction (this WG is the only one of its layer and head):
   // their destinations are the consecutive slots first_moved, first_moved + 1, ...  This
@@ -125,7 +174,6 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   // pending leaf rows are read from k_new / v_new by the main loop and stored into the
   // pool after it (by every WG whose node range holds them: identical data)
   const int leaf0 = a.kv_pending ? N - n_live : N;
-  const int col = lane & 31, hh = lane >> 5;
 
   const __bf16* kpool = static_cast<const __bf16*>(s.k_pool) + pool_row(s, u.t, lab, u.g, base);
   const __bf16* vpool = static_cast<const __bf16*>(s.v_pool) + pool_row(s, u.t, lab, u.g, base);
@@ -133,7 +181,6 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   const __bf16* knew = static_cast<const __bf16*>(a.k_new) + leaf_off;
   const __bf16* vnew = static_cast<const __bf16*>(a.v_new) + leaf_off;
   const int leaf_stride = s.Hkv * D;
-  const uint64_t* maskp = s.mask + (size_t)u.t * s.cap + base;
   unsigned char* kbuf = lds + wave * 2 * C::TILE_BYTES;
   unsigned char* vbuf = kbuf + C::TILE_BYTES;
 
@@ -176,10 +223,19 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   // range's last, partial tile, rows past the end are clamped to its last node and masked
   // out later
   const int moved_end = staged || late_copy ? first_moved + nmoves : INT_MIN;
+  // (TREE) depth and mask of tile node lane % 32, loaded with the tile (the visibility test
+  // gathers a lane's 16 nodes from them by lane permutes)
+  int tdep = 0;
+  uint64_t tmk = 0;
   auto issue = [&](int tile) {
     const int tb = n0 + tile * 32;
     const bool full = tb + 32 <= n1;
     const bool any_moved = tb + 32 > first_moved && tb < moved_end;  // wave-uniform
+    if constexpr (TREE) {
+      const int nn = min(tb + col, n1 - 1);
+      tdep = depthp[nn];
+      tmk = maskp[nn];
+    }
 #pragma unroll
     for (int i = 0; i < C::VINST; ++i) {
       const int nv = full ? tb + vrow[i] : min(tb + vrow[i], n1 - 1);
@@ -237,15 +293,12 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   if (my_tiles > 0 && !early) issue(wave);
   // (the query rows load while the first tile is in flight)
   // this lane's query row (B operand of S^T): half hh of the row's d range
-  const int r = u.rb * kRows + col;
-  const int beam = r / G;
-  const bool row_ok = r < s.b * G && beam < n_live;
-  const int beam_bit = beam < 64 ? beam : 63;
+  const int beam_bit = owner < 64 ? owner : 63;
   bf16x8 qv[C::KSTEPS];
   {
     const uint4* qp = reinterpret_cast<const uint4*>(
         static_cast<const __bf16*>(a.q) +
-        ((((size_t)u.li * s.T + u.t) * s.b + (row_ok ? beam : 0)) * s.Hq + u.g * G + r % G) * D +
+        ((((size_t)u.li * s.T + u.t) * nrows + (row_ok ? owner : 0)) * s.Hq + u.g * G + r % G) * D +
         hh * (D / 2));
 #pragma unroll
     for (int t = 0; t < C::KSTEPS; ++t) {
@@ -258,6 +311,8 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     const int tile = wave + NW * k;
     const int tb = n0 + tile * 32;
     __builtin_amdgcn_s_waitcnt(kWaitVmAll);  // this tile's K and V rows have landed in LDS
+    const int cdep = tdep;  // (TREE) this tile's node depth and mask of lane % 32
+    const uint64_t cmk = tmk;
     // all LDS reads of the tile first: K operands (MFMA layout) and V^T operands (two
     // transposed reads per 16 nodes x 32 d, giving this lane column d = 32 dt + col at 4
     // nodes 16uu + 8 half + 4hh + tm')
@@ -298,7 +353,27 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     // visibility of this lane's nodes 8(v/4) + 4hh + v%4: all inside the shared prefix of
     // a full tile (wave-uniform test); otherwise range end and the ancestor bit of the
     // row's beam; hidden scores become -inf
-    if (tb + 32 > n1 || tb + 32 > h.n_shared) {
+    if constexpr (TREE) {
+      // ancestor-or-self of the row's query node, within its window; the node's depth and
+      // mask come from the lane that loaded them.  Branch-free: the test only selects.  (A
+      // form with loads under per-node branches was compiled by hipcc with the mask and
+      // window conditions of the first node dropped.)
+      const int mlo = (int)(uint32_t)cmk, mhi = (int)(uint32_t)(cmk >> 32);
+      const uint32_t qlo = (uint32_t)qmask, qhi = (uint32_t)(qmask >> 32);
+      uint32_t vis = 0;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int i = 8 * (v >> 2) + 4 * hh + (v & 3);
+        const int dn = __builtin_amdgcn_ds_bpermute(i << 2, cdep);
+        const uint32_t lo_ = (uint32_t)__builtin_amdgcn_ds_bpermute(i << 2, mlo);
+        const uint32_t hi_ = (uint32_t)__builtin_amdgcn_ds_bpermute(i << 2, mhi);
+        const bool ok = (tb + i < n1) & (dn <= qdepth) & ((lo_ & qlo) == qlo) & ((hi_ & qhi) == qhi) &
+                        ((s.W <= 0) | (qdepth - dn < s.W));
+        vis |= (uint32_t)ok << v;
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[v] = (vis >> v) & 1u ? acc[v] : -INFINITY;
+    } else if (tb + 32 > n1 || tb + 32 > h.n_shared) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int n = tb + 8 * (v >> 2) + 4 * hh + (v & 3);
@@ -419,14 +494,14 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     const float Mi = rowm[i], L = rowl[i];
     if (a.splits == 1) {
       const int rr = u.rb * kRows + i;
-      if (rr < s.b * G) {
+      if (rr < nrows * G) {
         const int bm = rr / G;
-        const bool live = bm < n_live && L > 0.0f;
+        const bool live = (TREE || bm < n_live) && L > 0.0f;
         const float inv = live ? 1.0f / L : 0.0f;
         bf16x8 y;
 #pragma unroll
         for (int e = 0; e < 8; ++e) y[e] = (__bf16)(O[e] * inv);
-        *reinterpret_cast<bf16x8*>(outp + ((((size_t)u.li * s.T + u.t) * s.b + bm) * s.Hq + u.g * G + rr % G) * D + c) = y;
+        *reinterpret_cast<bf16x8*>(outp + ((((size_t)u.li * s.T + u.t) * nrows + bm) * s.Hq + u.g * G + rr % G) * D + c) = y;
       }
     } else {
       float* pp = part + ((size_t)u.split * kRows + i) * (D + 2);
@@ -469,10 +544,13 @@ hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st
   // (4-wave WGs, two per CU, measured slower than 8-wave WGs one per CU on every shape
   // here, also for launches of several WG rounds)
   const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * a.splits), block(kNW * 64);
+#define LAUNCH_MFMA(DD)                                                                              \
+  (a.tree ? hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW, true>), grid, block, 0, st, ev0, ev1, 0, s, a) \
+          : hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW, false>), grid, block, 0, st, ev0, ev1, 0, s, a))
   switch (s.D) {
-    case 64: hipExtLaunchKernelGGL((k_attn_mfma<64, kNW>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
-    case 96: hipExtLaunchKernelGGL((k_attn_mfma<96, kNW>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
-    case 128: hipExtLaunchKernelGGL((k_attn_mfma<128, kNW>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
+    case 64: LAUNCH_MFMA(64); break;
+    case 96: LAUNCH_MFMA(96); break;
+    case 128: LAUNCH_MFMA(128); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

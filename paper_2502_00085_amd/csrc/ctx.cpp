@@ -232,7 +232,7 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
     return fail(c, TD_EINVAL, "k_new / v_new must be 16-byte aligned");
   if (!(scale > 0.0f) || !std::isfinite(scale)) return fail(c, TD_EINVAL, "scale must be finite and > 0");
   const bool mfma = s.dtype == TD_BF16 && c->desc.attn_impl != TD_ATTN_VALU;
-  td::AttnArgs a;
+  td::AttnArgs a{};
   a.q = d_q;
   a.k_new = d_k_new;
   a.v_new = d_v_new;
@@ -292,6 +292,43 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
     for (int l = 0; l < s.L; ++l) all = all && c->layer_written[l];
     if (all) c->pending = c->moves_pending = false;
   }
+  return TD_OK;
+}
+
+td_status trie_tree_attn(td_ctx* c, int32_t layer_begin, int32_t n_layers, int32_t q_max,
+                         const int32_t* d_qslots, const void* d_q, void* d_out, float scale, hipStream_t st) {
+  td_status r = check_ready(c);
+  if (r != TD_OK) return r;
+  const td::DevState& s = c->dev;
+  if (n_layers < 1 || layer_begin < 0 || layer_begin + n_layers > s.L)
+    return fail(c, TD_EINVAL, "layer range [%d, %d) outside [0, %d)", layer_begin, layer_begin + n_layers, s.L);
+  if (q_max < 1 || (int64_t)q_max * (s.Hq / s.Hkv) > (1 << 24)) return fail(c, TD_EINVAL, "q_max must be in [1, 2^24 / G]");
+  if (!d_qslots || !d_q || !d_out || !aligned16(d_q) || !aligned16(d_out))
+    return fail(c, TD_EINVAL, "qslots, q and out must be non-null (q, out 16-byte aligned)");
+  if (!(scale > 0.0f) || !std::isfinite(scale)) return fail(c, TD_EINVAL, "scale must be finite and > 0");
+  if (s.dtype != TD_BF16 || c->desc.attn_impl == TD_ATTN_VALU)
+    return fail(c, TD_EUNSUPPORTED, "tree attention runs on the matrix-core kernel (bf16)");
+  if (c->pending) return fail(c, TD_ESTATE, "the leaves' K/V are pending: run trie_attn_decode first");
+  td::AttnArgs a{};
+  a.q = d_q;
+  a.out = d_out;
+  a.layer_begin = layer_begin;
+  a.n_layers = n_layers;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.tree = 1;
+  a.qslots = d_qslots;
+  a.qmax = q_max;
+  const int rpb = td::attn_mfma_rows_per_block();
+  a.row_blocks = (q_max * (s.Hq / s.Hkv) + rpb - 1) / rpb;
+  a.splits = c->splits_override > 0 ? c->splits_override : td::attn_choose_splits(s, n_layers, a.row_blocks);
+  const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
+  if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;
+  a.xcd_group = a.row_blocks > 1 && ((long)s.T * n_layers * s.Hkv * a.splits) % 8 == 0 ? 1 : 0;
+  hipEvent_t ev0 = c->ev[TD_PHASE_ATTN][0], ev1 = c->ev[TD_PHASE_ATTN][1];
+  c->ev[TD_PHASE_ATTN][0] = c->ev[TD_PHASE_ATTN][1] = nullptr;
+  hipError_t e = td::launch_attn_mfma(s, a, st, ev0, a.splits > 1 ? nullptr : ev1);
+  if (e == hipSuccess && a.splits > 1) e = td::launch_attn_combine(s, a, rpb, st, nullptr, ev1);
+  if (e != hipSuccess) return hip_fail(c, e, "trie_tree_attn launch");
   return TD_OK;
 }
 

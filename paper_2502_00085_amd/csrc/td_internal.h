@@ -100,6 +100,9 @@ struct AttnArgs {
   int splits;            // WGs per (trie, layer, kv head, row block) along the node axis
   int row_blocks;        // ceil(b * G / rows_per_block)
   int xcd_group;         // place the row blocks of a node range on one XCD (see attn_unit)
+  int tree = 0;                    // 1: multi-query tree attention (rows = query nodes)
+  const int32_t* qslots = nullptr; // (tree) [T][qmax] logical slots of the queries, -1 = none
+  int qmax = 0;                    // (tree) query nodes per trie in q / out
 };
 
 hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const int32_t* d_tokens,

@@ -80,6 +80,7 @@ def test_null_context_is_rejected_by_every_call():
     assert L.td_load_state(None, 0, None) == B.TD_EINVAL
     assert L.td_set_kernel_events(None, B.TD_PHASE_ATTN, None, None) == B.TD_EINVAL
     assert L.td_read_finished(None, 0, None, None, None, None, None, None) == B.TD_EINVAL
+    assert L.trie_tree_attn(None, 0, 1, 1, None, None, None, 1.0, None) == B.TD_EINVAL
     assert L.td_status_name(B.TD_ECAPACITY) == b"TD_ECAPACITY"
 
 

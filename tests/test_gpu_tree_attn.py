@@ -1,0 +1,104 @@
+"""GPU parity of multi-query tree attention (trie_tree_attn) against the oracle's
+``tree_attention``: queries at any set of stored nodes - every node (the prefill of a
+serialized trie), random subsets with empty (-1) entries, dead nodes awaiting a deferred
+collection, nodes outside the leaves' window - each attending to its own root path.
+
+The tries are grown by the scripted decode (parity-checked on the way), then one more
+attention call stores the last leaves' K/V, so every node's K/V is in the pools.
+Tolerance: the bf16 attention bar of the decode parity tests.
+"""
+import numpy as np
+import pytest
+
+import oracle.attention as oatt
+import synth
+from gpu_harness import ATTN_ABS_TOL, ATTN_REL_TOL, Run, from_dev, log, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def small(**kw):
+    base = dict(name="small", cfg_id=240, n_layers=2, n_q_heads=16, n_kv_heads=4, head_dim=128,
+                dtype="bf16", n_tries=1, prompt_min=100, prompt_max=100, beam_width=8, steps=10,
+                vocab=3000, window=0, alpha=1.0, qkv_std=1.0, logit_std=3.0)
+    base.update(kw)
+    return synth.Workload(**base)
+
+
+def run_tree(w, seed, pick, capacity=None):
+    log(f"tree case T={w.n_tries} L={w.n_layers} Hq={w.n_q_heads} Hkv={w.n_kv_heads} d={w.head_dim} "
+        f"P={w.prompt_min}-{w.prompt_max} b={w.beam_width} W={w.window} g={w.gc_interval} steps={w.steps} "
+        f"seed={seed}")
+    import torch
+    r = Run(w, seed, capacity=capacity)
+    for _ in range(w.steps):
+        errs, _ = r.step()
+        assert not errs, "\n".join(errs[:10])
+    s = w.steps + 1
+    q, kn, vn, _, _, _ = r.inputs(s)
+    out = torch.empty_like(to_dev(w, q))
+    r.dec.attn_decode(0, w.n_layers, to_dev(w, q), to_dev(w, kn), to_dev(w, vn), out, r.scale)
+    knf, vnf = synth.as_f32(w, kn), synth.as_f32(w, vn)
+    g = np.random.default_rng(seed + 1000)
+    slots = []
+    for t, tr in enumerate(r.tries):
+        tr.write_leaf_kv(knf[:, t, :tr.n_live], vnf[:, t, :tr.n_live])
+        slots.append(pick(tr, g))
+    qmax = max(len(x) for x in slots)
+    qs = np.full((w.n_tries, qmax), -1, np.int32)
+    for t, x in enumerate(slots):
+        qs[t, :len(x)] = x
+    qt = synth.f32_to_bf16_bits(g.standard_normal((w.n_layers, w.n_tries, qmax, w.n_q_heads, w.head_dim),
+                                                  dtype=np.float32))
+    qd = to_dev(w, qt)
+    ot = torch.full_like(qd, 5.0)
+    r.dec.tree_attn(0, w.n_layers, torch.from_numpy(qs).cuda(), qd, ot, r.scale)
+    torch.cuda.synchronize()
+    got = from_dev(ot)
+    qf = synth.as_f32(w, qt)
+    for t, tr in enumerate(r.tries):
+        ref = oatt.tree_attention(tr, qs[t], qf[:, t], r.scale)
+        err = float(np.max(np.abs(got[:, t] - ref)))
+        mx = float(np.max(np.abs(ref)))
+        assert err <= ATTN_ABS_TOL and err <= ATTN_REL_TOL * mx + 1e-6, (t, err, mx)
+        dead = [j for j, x in enumerate(qs[t]) if x < 0 or tr.alg3_mask()[x] == 0]
+        assert np.all(got[:, t, dead] == 0)
+    assert r.dec.status() == 0
+    r.dec.close()
+    return qs
+
+
+def every_node(tr, g):
+    return np.arange(len(tr.order), dtype=np.int32)
+
+
+def some_nodes(tr, g):
+    n = len(tr.order)
+    x = g.choice(n, size=min(n, 37), replace=False).astype(np.int32)
+    return np.concatenate([x, [-1, -1]]).astype(np.int32)
+
+
+def test_every_node_of_a_gqa_trie():
+    run_tree(small(), seed=1, pick=every_node)
+
+
+def test_random_queries_with_empty_rows():
+    run_tree(small(steps=8), seed=2, pick=some_nodes)
+
+
+def test_window_and_deferred_collection_dead_and_old_nodes():
+    # g = 5: dead nodes (mask 0) and nodes outside the leaves' window are still stored; a
+    # dead query gets zeros, an old one its own window
+    qs = run_tree(small(window=30, gc_interval=5, steps=13), seed=3, pick=every_node)
+    assert qs.shape[1] > 0
+
+
+def test_several_tries_mha_d96():
+    run_tree(small(n_tries=3, prompt_min=20, prompt_max=70, n_q_heads=4, n_kv_heads=4, head_dim=96,
+                   beam_width=4, steps=6, qkv_std=1.0 / np.sqrt(96.0)), seed=4, pick=some_nodes)
+
+
+def test_long_prefill_of_a_chain_with_branches():
+    # 700 prompt nodes and 3 steps: 2800 query rows per KV head, many row blocks
+    run_tree(small(n_layers=1, prompt_min=700, prompt_max=700, beam_width=4, steps=3), seed=5,
+             pick=every_node)
