@@ -32,15 +32,16 @@ import synth  # noqa: E402
 HBM_PEAK_GBS = 8000.0
 
 # HBM traffic of the attention kernel measured by rocprofv3 (separate --pmc FETCH_SIZE and
-# --pmc WRITE_SIZE runs of `bench.py --profile-only --copy-ref-mib 512`, llama8b), scaled
-# by what the same counters read for a plain 512 MiB device copy (fetch x 2.0, write x 1.0),
-# as the mean bytes per launch over that run's launches.  Valid only for the kernel
-# sources it was measured on: reported as null once their digest differs.
+# --pmc WRITE_SIZE runs of `bench.py --profile-only --no-batch-baseline --no-tree
+# --copy-ref-mib 512`, llama8b), scaled by what the same counters read for a plain 512 MiB
+# device copy (fetch x 2.0, write x 1.0), per launch for the 64 graph-replayed launches at
+# the step-K/2 trie: the launches `roofline.achieved` is timed on.  Valid only for the
+# kernel sources it was measured on: reported as null once their digest differs.
 ATTN_TRAFFIC = {
     "workload": "llama8b",
-    "sources_sha256": "25eef2fadad6839c893e2fc93df1544f35c1438271bc8505cc381405ee508e9a",
-    "bytes_per_launch": 286253422,             # 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE
-    "algorithmic_bytes_per_launch": 286847941,  # KV rows, q, new leaves, moved rows, out
+    "sources_sha256": "2edbe4b9516f0d507dd38e12c4e8c0bd3db0b7eac10d4af2b3c74c2bc6b03f86",
+    "bytes_per_launch": 283740756,             # 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE
+    "algorithmic_bytes_per_launch": 283377664,  # unique K+V rows, q, out
 }
 ATTN_SOURCES = ("attn_mfma.hip", "attn_common.h", "td_internal.h")
 
@@ -69,6 +70,8 @@ def parse():
     p.add_argument("--attn-reps", type=int, default=32, help="launches in the attention timing graph")
     p.add_argument("--copy-ref-mib", type=int, default=0,
                    help="also run one plain device copy of this many MiB (reference for HBM counters)")
+    p.add_argument("--no-tree", action="store_true",
+                   help="skip the multi-query tree attention measurement (every node a query)")
     p.add_argument("--no-batch-baseline", action="store_true",
                    help="skip the batch-based beam search baseline on the same inputs")
     p.add_argument("--eos", type=int, default=-1, help="end-of-sequence token (-1: none)")
@@ -263,6 +266,7 @@ def gpu_bench(args, w, K):
         raise RuntimeError(f"device status {status} after the timed run")
     finished = [bench.dec.read_finished(t) for t in range(w.n_tries)] if args.eos >= 0 else None
     attn_graph_ms, attn_graph_nodes = attn_graph_time(bench, K, args.attn_reps)
+    tree = None if args.no_tree or w.dtype != "bf16" else tree_prefill_time(bench, K, 8)
     phase_ms = phase_times(bench, K)
     nodes = bench.nodes_per_step(K)
     collects = np.array([bench.collects(i) for i in range(K)])
@@ -270,7 +274,9 @@ def gpu_bench(args, w, K):
     batch = None if args.no_batch_baseline else batch_bench(bench, K, args.warmup)
     return dict(mode=mode, seconds=t1 - t0, eager_seconds=eager_s, attn_ms=attn_ms, nodes=nodes,
                 attn_graph_ms=attn_graph_ms, attn_graph_nodes=attn_graph_nodes, phase_ms=phase_ms,
-                collects=collects, stored=bench.stored, batch=batch, finished=finished)
+                collects=collects, stored=bench.stored, batch=batch, finished=finished, tree=tree,
+                qo_bytes=int(bench.q[0].numel() * bench.q[0].element_size() +
+                             bench.out.numel() * bench.out.element_size()))
 
 
 def batch_bench(bench, K, warmup):
@@ -439,6 +445,65 @@ def attn_graph_time(bench, K, reps):
     return e0.elapsed_time(e1) / reps, nodes
 
 
+def tree_prefill_time(bench, K, reps):
+    """Multi-query tree attention with every stored node of the step-K/2 trie as a query (the
+    prefill of that serialized trie, Figure 3's square mask), all layers: `reps` launches
+    graph-replayed between events.  Returns (ms per launch, queries, algorithmic flops per
+    launch = 4 d Hq L x the keys each query sees, summed over the queries)."""
+    import torch
+    stream = torch.cuda.current_stream().cuda_stream
+    L, ctx, w = bench.B.lib(), bench.dec.ctx, bench.w
+    mid = K // 2
+    bench.init()
+    for i in range(mid):
+        bench.step(i, stream)
+    st = L.trie_attn_decode(ctx, 0, w.n_layers, bench.q[mid].data_ptr(),
+                            bench.kn[mid].data_ptr() if mid > 0 else None,
+                            bench.vn[mid].data_ptr() if mid > 0 else None, bench.out.data_ptr(),
+                            ctypes.c_float(bench.scale), stream)
+    if st != 0:
+        raise RuntimeError(bench.B.td_error_string(ctx))
+    torch.cuda.synchronize()
+    seen, qmax = [], 0
+    for t in range(w.n_tries):
+        state = bench.dec.read_state(t)
+        n, par, live = state["n_nodes"], state["parent_slot"], state["mask"] != 0
+        plen = np.zeros(n, np.int64)
+        for j in range(n):  # path length of each node (parents precede children)
+            plen[j] = 1 + (plen[par[j]] if par[j] >= 0 else 0)
+        vis = np.minimum(plen, w.window) if w.window > 0 else plen
+        seen.append(int(vis[live].sum()))
+        qmax = max(qmax, n)
+    qs = np.full((w.n_tries, qmax), -1, np.int32)
+    for t in range(w.n_tries):
+        n = bench.dec.read_state(t)["n_nodes"]
+        qs[t, :n] = np.arange(n)
+    qsd = torch.from_numpy(qs).cuda()
+    g = torch.Generator(device="cuda").manual_seed(bench.seed)
+    shape = (w.n_layers, w.n_tries, qmax, w.n_q_heads, w.head_dim)
+    q = torch.randn(shape, generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    out = torch.empty_like(q)
+    args = (ctx, 0, w.n_layers, qmax, qsd.data_ptr(), q.data_ptr(), out.data_ptr(), ctypes.c_float(bench.scale))
+    st = L.trie_tree_attn(*args, stream)
+    torch.cuda.synchronize()
+    graph, cs = torch.cuda.CUDAGraph(), torch.cuda.Stream()
+    with torch.cuda.graph(graph, stream=cs):
+        s_ = torch.cuda.current_stream().cuda_stream
+        for _ in range(reps):
+            st |= L.trie_tree_attn(*args, s_)
+    if st != 0:
+        raise RuntimeError(bench.B.td_error_string(ctx))
+    graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    flops = 4.0 * w.head_dim * w.n_q_heads * w.n_layers * float(sum(seen))
+    return e0.elapsed_time(e1) / reps, int(sum(int(bench.dec.read_state(t)["n_nodes"]) for t in range(w.n_tries))), flops
+
+
 def cpu_baseline(w, seed, budget_s):
     """The CPU oracle on the same workload: decode steps from the start, all layers, until
     the time budget is used; steps/s over the completed steps."""
@@ -518,6 +583,7 @@ def main():
                      "kernel": "k_attn_mfma (trie_attn_decode, all layers, one launch)",
                      "attn_us_per_launch": round(r["attn_graph_ms"] * 1e3, 2),
                      "unique_kv_bytes_per_launch": int(graph_bytes),
+                     "algorithmic_bytes_per_launch": int(graph_bytes) + r["qo_bytes"],
                      "timing": f"{args.attn_reps} back-to-back launches at the step-{K // 2} trie, "
                                f"graph-replayed between events",
                      "attn_us_eager_events_mean": round(float(attn_s.mean() * 1e6), 2)},
@@ -526,6 +592,15 @@ def main():
         "nodes_per_step_mean": round(float(r["nodes"].sum(axis=1).mean()), 1),
         "gc": gc_summary(w, r["phase_ms"], r["collects"]),
     }
+    if r["tree"] is not None:
+        ms, nq, flops = r["tree"]
+        out["tree_attention"] = {
+            "what": "trie_tree_attn with every stored node of the step-K/2 trie as a query (its "
+                    "prefill, Figure 3's square mask), all layers, one launch",
+            "queries": nq, "us_per_launch": round(ms * 1e3, 2), "query_nodes_per_s": round(nq / (ms / 1e3), 1),
+            "bound": "mfma", "achieved": round(flops / (ms / 1e3) / 1e12, 2), "peak": 2500.0,
+            "unit": "TFLOP/s", "frac": round(flops / (ms / 1e3) / 1e12 / 2500.0, 4),
+            "flops_per_launch": flops}
     if r["batch"] is not None:
         trie_bytes = float(r["stored"].sum(axis=1).mean()) * w.node_bytes
         bb = r["batch"]
