@@ -133,13 +133,16 @@ __device__ inline void wave_append(const T1* val, const T2* val2, const bool* ta
 }
 
 // Writes the b largest of the distinct keys cand[0..n) to out[0..b) in order, with their
-// companions.  Wave 0 alone ranks up to 64 keys held in registers; more keys are ranked by
-// the whole block by counting.  Call from uniform control flow.
+// companions (0 where there are fewer than b keys).  Wave 0 alone ranks up to 64 keys held
+// in registers (and only wave 0 has written out when this returns); more keys are ranked
+// by the whole block by counting (out complete after the caller's next barrier).  Call
+// from uniform control flow.
 __device__ inline void rank_topb(const uint64_t* cand, const uint64_t* comp, int n, int b, uint64_t* out,
                                  uint64_t* out_comp) {
   if (n <= 64) {
     if (threadIdx.x < 64) {
       const int lane = threadIdx.x;
+      if (lane < b) out[lane] = out_comp[lane] = 0;  // (in order before the rank stores below)
       const uint64_t k = lane < n ? cand[lane] : 0;
       int rank = 0;
       for (int j = 0; j < n; ++j) {
@@ -154,6 +157,8 @@ __device__ inline void rank_topb(const uint64_t* cand, const uint64_t* comp, int
     }
     return;
   }
+  for (int j = threadIdx.x; j < b; j += blockDim.x) out[j] = out_comp[j] = 0;
+  __syncthreads();
   for (int i = threadIdx.x; i < n; i += blockDim.x) {
     const uint64_t k = cand[i];
     int rank = 0;
@@ -313,7 +318,10 @@ __device__ inline void finish_hypotheses(const DevState& s, int t, uint64_t rank
   if (count == b && (s.early || norm[b - 1] >= length_norm(best_next, step, s.alpha))) s.fin_done[t] = 1;
 }
 
-// Merge of one trie's chunks into the final selection, then the outputs.
+// Merge of one trie's chunks into the final selection, then the outputs.  PER: entries per
+// lane held in registers (a wave's entries beyond 64 PER are read again); with PER <= 4
+// the second-largest keys are loaded up front too.
+template <int PER>
 __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const float* logits,
                                                               int32_t* sel_parent, int32_t* sel_token,
                                                               float* sel_score, float* sel_logprob,
@@ -343,11 +351,17 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
 
   // Independent loads first: the first batch of this wave's entries (rows >= n_live are
   // dropped once n_live is known), pair logits, leaf scores, every row's lse, then n_live.
-  uint64_t km0[kPer];
+  constexpr int PRE2 = PER <= 4 ? PER : 0;  // second-largest keys held in registers
+  uint64_t km0[PER], km20[PRE2 > 0 ? PRE2 : 1];
 #pragma unroll
-  for (int q = 0; q < kPer; ++q) {
+  for (int q = 0; q < PER; ++q) {
     const int j = q * 64 + lane;
-    km0[q] = j < e_all ? ekey[j] : 0;
+    km0[q] = 0;
+    if (PRE2 > 0) km20[q < PRE2 ? q : 0] = 0;
+    if (q * 64 < e_all) {  // (wave-uniform)
+      km0[q] = j < e_all ? ekey[j] : 0;
+      if (PRE2 > 0) km20[q < PRE2 ? q : 0] = j < e_all ? ekey2[j] : 0;
+    }
   }
   // pairs: the last b threads (their wave has no row below; the dependent logit load
   // waits there)
@@ -387,15 +401,18 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     const int r = div_small(j, inv_nch);
     return km != 0 ? ord_score(score_only(key_x(km), row_lse[r], row_score[r])) : 0u;
   };
-  uint32_t o0[kPer];
+  uint32_t o0[PER];
   uint32_t lmax = 0;
 #pragma unroll
-  for (int q = 0; q < kPer; ++q) {
+  for (int q = 0; q < PER; ++q) {
     const int j = q * 64 + lane;
-    o0[q] = entry_ord(j, j < e_live ? km0[q] : 0);
-    lmax = o0[q] > lmax ? o0[q] : lmax;
+    o0[q] = 0;
+    if (q * 64 < e_live) {  // (wave-uniform)
+      o0[q] = entry_ord(j, j < e_live ? km0[q] : 0);
+      lmax = o0[q] > lmax ? o0[q] : lmax;
+    }
   }
-  for (int j = kPer * 64 + lane; j < e_live; j += 64) {
+  for (int j = PER * 64 + lane; j < e_live; j += 64) {
     const uint32_t oj = entry_ord(j, ekey[j]);
     lmax = oj > lmax ? oj : lmax;
   }
@@ -434,8 +451,8 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
       const int j = (g0 + q) * 64 + lane;
       uint32_t v = 0;
 #pragma unroll
-      for (int u = 0; u < kPer; ++u) v = (g0 + q == u) ? o0[u] : v;
-      og[q] = g0 + q < kPer ? v : (j < e_live ? entry_ord(j, ekey[j]) : 0u);
+      for (int u = 0; u < PER; ++u) v = (g0 + q == u) ? o0[u] : v;
+      og[q] = g0 + q < PER ? v : (j < e_live ? entry_ord(j, ekey[j]) : 0u);
     }
     bool any = false;
 #pragma unroll
@@ -449,7 +466,10 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
       const int j = (g0 + q) * 64 + lane;
       const bool hotq = og[q] >= L && og[q] != 0u;
       uint64_t km = 0, k2 = 0;
-      if (hotq) {
+      if (PRE2 >= 4 && g0 == 0) {  // the first group: both keys in registers
+        km = hotq ? km0[q < PER ? q : 0] : 0;
+        k2 = hotq ? km20[q < PRE2 ? q : 0] : 0;
+      } else if (hotq) {
         km = ekey[j];
         k2 = ekey2[j];
       }
@@ -528,35 +548,39 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     }
     __syncthreads();
   }
-  for (int j = threadIdx.x; j < b; j += kFinalThreads) best_k[j] = best_c[j] = 0;
-  __syncthreads();
-  rank_topb(cand, cand_x, min(ncand, kCandMax), b, best_k, best_c);
+  const int n_cand = min(ncand, kCandMax);
+  rank_topb(cand, cand_x, n_cand, b, best_k, best_c);
   // End of sequence: the EOS candidate of live row r finishes a hypothesis iff fewer than b
   // candidates beat it: the selected non-EOS ones above it and the other rows' EOS above it.
   // Finishing candidates are recorded by rank (acc_row / acc_val); bit k of acc_mask (wave
   // 0) marks rank k.
-  float eos_sc = 0.0f;
-  if (s.eos >= 0 && threadIdx.x < b) {
-    const int r = threadIdx.x;
-    acc_row[r] = -1;
-    if (r < n_live) {
-      eos_sc = score_only(eos_x, row_lse[r], row_score[r]);
-      eos_key[r] = s_key(eos_sc, (uint32_t)(r * V + s.eos));
+  uint64_t acc_mask = 0;
+  if (s.eos >= 0) {  // (uniform)
+    float eos_sc = 0.0f;
+    if (threadIdx.x < b) {
+      const int r = threadIdx.x;
+      acc_row[r] = -1;
+      if (r < n_live) {
+        eos_sc = score_only(eos_x, row_lse[r], row_score[r]);
+        eos_key[r] = s_key(eos_sc, (uint32_t)(r * V + s.eos));
+      }
     }
-  }
-  __syncthreads();
-  if (s.eos >= 0 && threadIdx.x < n_live) {
-    const uint64_t k = eos_key[threadIdx.x];
-    int better = 0;
-    for (int j = 0; j < b; ++j) better += best_k[j] > k;
-    for (int r = 0; r < n_live; ++r) better += eos_key[r] > k;
-    if (better < b) {
-      acc_row[better] = threadIdx.x;
-      acc_val[better] = eos_sc;
+    __syncthreads();
+    if (threadIdx.x < n_live) {
+      const uint64_t k = eos_key[threadIdx.x];
+      int better = 0;
+      for (int j = 0; j < b; ++j) better += best_k[j] > k;
+      for (int r = 0; r < n_live; ++r) better += eos_key[r] > k;
+      if (better < b) {
+        acc_row[better] = threadIdx.x;
+        acc_val[better] = eos_sc;
+      }
     }
+    __syncthreads();
+    if (wave == 0) acc_mask = __ballot(lane < b && acc_row[lane] >= 0);
+  } else if (n_cand > 64) {
+    __syncthreads();  // best_k / best_c were written by the whole block
   }
-  __syncthreads();
-  const uint64_t acc_mask = s.eos >= 0 && wave == 0 ? __ballot(lane < b && acc_row[lane] >= 0) : 0ull;
 
   for (int j = threadIdx.x; j < b; j += kFinalThreads) {
     const uint64_t kx = best_c[j];
@@ -598,9 +622,16 @@ hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_
                         nullptr, 0, s, logits);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipExtLaunchKernelGGL(k_topb_final, dim3(s.T), dim3(kFinalThreads), 0, st, nullptr, ev1, 0, s, logits,
-                        sel_parent, sel_token, sel_score, sel_logprob, lse, pair_parent, pair_token,
-                        pair_score);
+  // entries per wave: b * chunks (every wave covers every row); up to 256 of them fit the
+  // 4-per-lane variant
+  if (s.b * s.lse_chunks <= 4 * 64)
+    hipExtLaunchKernelGGL(k_topb_final<4>, dim3(s.T), dim3(kFinalThreads), 0, st, nullptr, ev1, 0, s, logits,
+                          sel_parent, sel_token, sel_score, sel_logprob, lse, pair_parent, pair_token,
+                          pair_score);
+  else
+    hipExtLaunchKernelGGL(k_topb_final<kPer>, dim3(s.T), dim3(kFinalThreads), 0, st, nullptr, ev1, 0, s,
+                          logits, sel_parent, sel_token, sel_score, sel_logprob, lse, pair_parent,
+                          pair_token, pair_score);
   return hipGetLastError();
 }
 

@@ -119,3 +119,15 @@ def test_single_live_beam():
     g = np.random.default_rng(5)
     b, V = 16, 128256
     run_topb(b, g.normal(0, 3, (1, V)).astype(np.float32), np.array([-3.25], np.float32))
+
+
+@pytest.mark.parametrize("b", [8, 9])
+def test_register_batch_boundary_llama_vocab(b):
+    """b * chunks = 256 entries per wave (the largest count the four-per-lane variant of the
+    merge takes) and 288 (the general variant), at the Llama-3 vocabulary."""
+    g = np.random.default_rng(6 + b)
+    V = 128256
+    logits = g.normal(0, 3, (b, V)).astype(np.float32)
+    scores = -np.sort(g.uniform(0, 2, b)).astype(np.float32)
+    pairs = (g.integers(0, b, b), g.integers(0, V, b))
+    run_topb(b, logits, scores, pairs)
