@@ -266,6 +266,7 @@ def gpu_bench(args, w, K):
         raise RuntimeError(f"device status {status} after the timed run")
     finished = [bench.dec.read_finished(t) for t in range(w.n_tries)] if args.eos >= 0 else None
     attn_graph_ms, attn_graph_nodes = attn_graph_time(bench, K, args.attn_reps)
+    attn_cold_ms = attn_cold_time(bench, max(4, args.attn_reps // 4))
     tree = None if args.no_tree or w.dtype != "bf16" else tree_prefill_time(bench, K, 8)
     phase_ms = phase_times(bench, K)
     nodes = bench.nodes_per_step(K)
@@ -274,6 +275,7 @@ def gpu_bench(args, w, K):
     batch = None if args.no_batch_baseline else batch_bench(bench, K, args.warmup)
     return dict(mode=mode, seconds=t1 - t0, eager_seconds=eager_s, attn_ms=attn_ms, nodes=nodes,
                 attn_graph_ms=attn_graph_ms, attn_graph_nodes=attn_graph_nodes, phase_ms=phase_ms,
+                attn_cold_ms=attn_cold_ms,
                 collects=collects, stored=bench.stored, batch=batch, finished=finished, tree=tree,
                 qo_bytes=int(bench.q[0].numel() * bench.q[0].element_size() +
                              bench.out.numel() * bench.out.element_size()))
@@ -445,6 +447,30 @@ def attn_graph_time(bench, K, reps):
     return e0.elapsed_time(e1) / reps, nodes
 
 
+def attn_cold_time(bench, reps):
+    """The same launch as attn_graph_time (the trie it leaves: nothing pending), with the
+    last-level cache cleared first: before each launch a 1 GiB buffer is read (four times
+    the 256 MB cache), then the kernel alone is timed by kernel-timestamp events.  Returns
+    the mean ms per launch."""
+    import torch
+    stream = torch.cuda.current_stream().cuda_stream
+    L, ctx, w = bench.B.lib(), bench.dec.ctx, bench.w
+    flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    ev = bench.B.KernelEvents()
+    ms = []
+    for _ in range(reps):
+        float(flush.sum())
+        bench.B.td_set_kernel_events(ctx, bench.B.TD_PHASE_ATTN, ev.start, ev.stop)
+        st = L.trie_attn_decode(ctx, 0, w.n_layers, bench.q[0].data_ptr(), None, None, bench.out.data_ptr(),
+                                ctypes.c_float(bench.scale), stream)
+        if st != 0:
+            raise RuntimeError(bench.B.td_error_string(ctx))
+        ms.append(ev.elapsed_ms())
+    ev.close()
+    del flush
+    return float(np.mean(ms))
+
+
 def tree_prefill_time(bench, K, reps):
     """Multi-query tree attention with every stored node of the step-K/2 trie as a query (the
     prefill of that serialized trie, Figure 3's square mask), all layers: `reps` launches
@@ -586,7 +612,11 @@ def main():
                      "algorithmic_bytes_per_launch": int(graph_bytes) + r["qo_bytes"],
                      "timing": f"{args.attn_reps} back-to-back launches at the step-{K // 2} trie, "
                                f"graph-replayed between events",
-                     "attn_us_eager_events_mean": round(float(attn_s.mean() * 1e6), 2)},
+                     "attn_us_eager_events_mean": round(float(attn_s.mean() * 1e6), 2),
+                     "attn_us_llc_cold": round(r["attn_cold_ms"] * 1e3, 2),
+                     "achieved_llc_cold": round(graph_bytes / (r["attn_cold_ms"] / 1e3) / 1e9, 1),
+                     "llc_cold": "the same launch with the 256 MB last-level cache cleared before it "
+                                 "(a 1 GiB read), timed alone by kernel-timestamp events"},
         "hbm_gbps_unique_kv_whole_step": round(float(kv_bytes.mean() / (ms_per_step / 1e3) / 1e9), 1),
         "eager_ms_per_step": round(r["eager_seconds"] * 1e3 / K, 5),
         "nodes_per_step_mean": round(float(r["nodes"].sum(axis=1).mean()), 1),
