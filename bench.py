@@ -70,6 +70,9 @@ def parse():
     p.add_argument("--attn-reps", type=int, default=32, help="launches in the attention timing graph")
     p.add_argument("--copy-ref-mib", type=int, default=0,
                    help="also run one plain device copy of this many MiB (reference for HBM counters)")
+    p.add_argument("--unfused", action="store_true",
+                   help="run the selection and the append as two calls (beam_logsoftmax_topk, "
+                        "trie_append_prune) instead of the fused beam_topk_append")
     p.add_argument("--no-tree", action="store_true",
                    help="skip the multi-query tree attention measurement (every node a query)")
     p.add_argument("--no-batch-baseline", action="store_true",
@@ -90,7 +93,7 @@ def log(*a):
 
 
 class Bench:
-    def __init__(self, w, steps, seed, input_period=0, eos=-1, eos_boost=0.0):
+    def __init__(self, w, steps, seed, input_period=0, eos=-1, eos_boost=0.0, fused=True):
         import torch
         import paper_2502_00085_amd.binding as B
         self.B, self.torch, self.w, self.seed = B, torch, w, seed
@@ -98,6 +101,7 @@ class Bench:
         self.cap = w.prompt_max + (steps + 2) * w.beam_width
         self.scale = 1.0 / float(np.sqrt(w.head_dim))
         t0 = time.time()
+        self.fused = fused  # one beam_topk_append call for the selection and the append
         self.dec = B.TrieDecoder(w.n_tries, w.beam_width, self.cap, w.vocab, w.n_layers, w.n_q_heads,
                                  w.n_kv_heads, w.head_dim, w.window, w.dtype, gc_interval=w.gc_interval,
                                  eos_token=eos)
@@ -162,12 +166,15 @@ class Bench:
                                 self.kn[i].data_ptr() if pend else None,
                                 self.vn[i].data_ptr() if pend else None, self.out.data_ptr(),
                                 ctypes.c_float(self.scale), stream)
-        st |= L.beam_logsoftmax_topk(ctx, self.logits[i].data_ptr(), self.sp.data_ptr(), self.st.data_ptr(),
-                                     self.ss.data_ptr(), self.sl.data_ptr(), self.lse.data_ptr(),
-                                     self.par[i].data_ptr(), self.tok[i].data_ptr(), self.ps.data_ptr(),
-                                     stream)
-        st |= L.trie_append_prune(ctx, self.par[i].data_ptr(), self.tok[i].data_ptr(), self.ps.data_ptr(),
-                                  stream)
+        sel = (self.logits[i].data_ptr(), self.sp.data_ptr(), self.st.data_ptr(), self.ss.data_ptr(),
+               self.sl.data_ptr(), self.lse.data_ptr(), self.par[i].data_ptr(), self.tok[i].data_ptr(),
+               self.ps.data_ptr(), stream)
+        if self.fused and phases is None:
+            st |= L.beam_topk_append(ctx, *sel)
+        else:  # (every phase timed: the selection and the append as calls of their own)
+            st |= L.beam_logsoftmax_topk(ctx, *sel)
+            st |= L.trie_append_prune(ctx, self.par[i].data_ptr(), self.tok[i].data_ptr(),
+                                      self.ps.data_ptr(), stream)
         if st != 0:
             raise RuntimeError(f"step {i}: {self.B.td_error_string(ctx)}")
 
@@ -211,7 +218,7 @@ def gpu_bench(args, w, K):
         torch.cuda.synchronize()
         log(f"[bench] reference copy: {args.copy_ref_mib} MiB read + {args.copy_ref_mib} MiB written")
         del src, dst
-    bench = Bench(w, K, args.seed, args.input_period, args.eos, args.eos_boost)
+    bench = Bench(w, K, args.seed, args.input_period, args.eos, args.eos_boost, fused=not args.unfused)
     stream = torch.cuda.current_stream().cuda_stream
     # warmup (eager)
     bench.init()
@@ -603,7 +610,9 @@ def main():
                    "prompt": [w.prompt_min, w.prompt_max], "beam_width": w.beam_width,
                    "vocab": w.vocab, "window": w.window, "gc_interval": w.gc_interval,
                    "eos_token": args.eos, "eos_boost": args.eos_boost,
-                   "growth": f"scripted, parent rank ~ (r+1)^-{w.alpha}", "launch": r["mode"]},
+                   "growth": f"scripted, parent rank ~ (r+1)^-{w.alpha}", "launch": r["mode"],
+                   "step_calls": "trie_attn_decode, beam_logsoftmax_topk, trie_append_prune" if args.unfused
+                   else "trie_attn_decode, beam_topk_append"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": "k_attn_mfma (trie_attn_decode, all layers, one launch)",

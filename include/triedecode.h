@@ -222,6 +222,22 @@ td_status beam_logsoftmax_topk(td_ctx* ctx, const float* d_logits, int32_t* d_se
 td_status trie_append_prune(td_ctx* ctx, const int32_t* d_sel_parent, const int32_t* d_sel_token,
                             const float* d_sel_score, hipStream_t stream);
 
+/* The selection and the append of one step of Alg 2 in one call: beam_logsoftmax_topk
+ * followed by trie_append_prune, fused.  The arguments, outputs and errors are those of
+ * beam_logsoftmax_topk.  The nodes appended are the pairs (d_pair_parent, d_pair_token)
+ * with their d_pair_score when the pairs are given, and otherwise the selection
+ * (d_sel_parent, d_sel_token, d_sel_score).  Results are identical to the two calls in
+ * order.  The second launch of the selection performs the append within the same block,
+ * and the trie reads that do not depend on the selection are issued with its first loads.
+ * Preconditions and errors of the append hold too: TD_ESTATE while leaves are pending,
+ * and the sticky device status for invalid pairs or capacity overflow (trie unchanged).
+ * Kernel events: the top-b phase's events bracket the whole call; the append phase's
+ * events are left for the next trie_append_prune. */
+td_status beam_topk_append(td_ctx* ctx, const float* d_logits, int32_t* d_sel_parent, int32_t* d_sel_token,
+                           float* d_sel_score, float* d_sel_logprob, float* d_lse,
+                           const int32_t* d_pair_parent, const int32_t* d_pair_token, float* d_pair_score,
+                           hipStream_t stream);
+
 /* The finished hypotheses of trie t (synchronises the device): *count (<= b) entries, best
  * first - norm, score, step (its length), parent (rank of the live beam it extends at
  * that step; with the selections of steps 1 .. step-1 this names its tokens) - and *done.

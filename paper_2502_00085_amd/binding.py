@@ -80,6 +80,7 @@ def lib() -> ctypes.CDLL:
         L.trie_attn_decode.argtypes = [vp, i32, i32, vp, vp, vp, vp, f32, vp]
         L.beam_logsoftmax_topk.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.trie_append_prune.argtypes = [vp, vp, vp, vp, vp]
+        L.beam_topk_append.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.td_read_state.argtypes = [vp, i32, ctypes.POINTER(TdState)]
         L.td_load_state.argtypes = [vp, i32, ctypes.POINTER(TdState)]
         L.td_get_status.argtypes = [vp]
@@ -255,6 +256,19 @@ def beam_logsoftmax_topk(ctx, dims: Dims, logits, sel_parent, sel_token, sel_sco
         _ptr(pair_score, torch.float32, tb, "pair_score"), _stream(stream)))
 
 
+def beam_topk_append(ctx, dims: Dims, logits, sel_parent, sel_token, sel_score, sel_logprob,
+                     lse=None, pair_parent=None, pair_token=None, pair_score=None, stream=None):
+    import torch
+    tb = dims.T * dims.b
+    _check(ctx, lib().beam_topk_append(
+        ctx, _ptr(logits, torch.float32, tb * dims.V, "logits"),
+        _ptr(sel_parent, torch.int32, tb, "sel_parent"), _ptr(sel_token, torch.int32, tb, "sel_token"),
+        _ptr(sel_score, torch.float32, tb, "sel_score"),
+        _ptr(sel_logprob, torch.float32, tb, "sel_logprob"), _ptr(lse, torch.float32, tb, "lse"),
+        _ptr(pair_parent, torch.int32, tb, "pair_parent"), _ptr(pair_token, torch.int32, tb, "pair_token"),
+        _ptr(pair_score, torch.float32, tb, "pair_score"), _stream(stream)))
+
+
 def trie_append_prune(ctx, dims: Dims, sel_parent, sel_token, sel_score, stream=None):
     import torch
     tb = dims.T * dims.b
@@ -362,6 +376,11 @@ class TrieDecoder:
 
     def append_prune(self, sel_parent, sel_token, sel_score, stream=None):
         trie_append_prune(self.ctx, self.dims, sel_parent, sel_token, sel_score, stream)
+
+    def topk_append(self, logits, sel_parent, sel_token, sel_score, sel_logprob, lse=None,
+                    pair_parent=None, pair_token=None, pair_score=None, stream=None):
+        beam_topk_append(self.ctx, self.dims, logits, sel_parent, sel_token, sel_score, sel_logprob, lse,
+                         pair_parent, pair_token, pair_score, stream)
 
     def read_state(self, trie=0):
         return td_read_state(self.ctx, self.dims, trie)

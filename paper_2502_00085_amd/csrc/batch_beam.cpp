@@ -275,7 +275,8 @@ td_status batch_beam_logsoftmax_topk(bbs_ctx* c, const float* d_logits, int32_t*
   if ((d_pair_parent == nullptr) != (d_pair_token == nullptr) || (d_pair_parent != nullptr && d_pair_score == nullptr))
     return bfail(c, TD_EINVAL, "pair_parent / pair_token / pair_score must be given together");
   hipError_t e = td::launch_logsoftmax_topk(c->sel, d_logits, d_sel_parent, d_sel_token, d_sel_score, d_sel_logprob,
-                                            d_lse, d_pair_parent, d_pair_token, d_pair_score, st, nullptr, nullptr);
+                                            d_lse, d_pair_parent, d_pair_token, d_pair_score, false, st, nullptr,
+                                            nullptr);
   if (e != hipSuccess) return bhip(c, e, "batch_beam_logsoftmax_topk launch");
   return TD_OK;
 }

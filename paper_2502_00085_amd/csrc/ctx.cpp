@@ -355,10 +355,46 @@ td_status beam_logsoftmax_topk(td_ctx* c, const float* d_logits, int32_t* d_sel_
     return fail(c, TD_EINVAL, "pair_parent / pair_token / pair_score must be given together");
   hipError_t e = td::launch_logsoftmax_topk(c->dev, d_logits, d_sel_parent, d_sel_token, d_sel_score,
                                             d_sel_logprob, d_lse, d_pair_parent, d_pair_token,
-                                            d_pair_score, st, c->ev[TD_PHASE_TOPB][0],
+                                            d_pair_score, false, st, c->ev[TD_PHASE_TOPB][0],
                                             c->ev[TD_PHASE_TOPB][1]);
   c->ev[TD_PHASE_TOPB][0] = c->ev[TD_PHASE_TOPB][1] = nullptr;
   if (e != hipSuccess) return hip_fail(c, e, "beam_logsoftmax_topk launch");
+  return TD_OK;
+}
+
+// Host bookkeeping after an append has been launched: the leaves' K/V are pending, and rows
+// move only where this append collects (Alg 2: the next position is a multiple of g).
+static void note_append(td_ctx* c) {
+  bool collects = false;
+  for (int t = 0; t < c->dev.T; ++t) {
+    ++c->leaf_depth[t];
+    collects = collects || (c->leaf_depth[t] + 1) % c->dev.G == 0;
+  }
+  c->pending = true;
+  c->moves_pending = collects;
+  c->layer_written.assign(c->dev.L, 0);
+}
+
+td_status beam_topk_append(td_ctx* c, const float* d_logits, int32_t* d_sel_parent, int32_t* d_sel_token,
+                           float* d_sel_score, float* d_sel_logprob, float* d_lse,
+                           const int32_t* d_pair_parent, const int32_t* d_pair_token, float* d_pair_score,
+                           hipStream_t st) {
+  td_status r = check_ready(c);
+  if (r != TD_OK) return r;
+  if (!d_logits || !d_sel_parent || !d_sel_token || !d_sel_score || !d_sel_logprob)
+    return fail(c, TD_EINVAL, "logits and the four selection outputs are required");
+  if ((d_pair_parent == nullptr) != (d_pair_token == nullptr) ||
+      (d_pair_parent != nullptr && d_pair_score == nullptr))
+    return fail(c, TD_EINVAL, "pair_parent / pair_token / pair_score must be given together");
+  if (c->pending)
+    return fail(c, TD_ESTATE, "trie_attn_decode has not stored the leaves' K/V for every layer");
+  hipError_t e = td::launch_logsoftmax_topk(c->dev, d_logits, d_sel_parent, d_sel_token, d_sel_score,
+                                            d_sel_logprob, d_lse, d_pair_parent, d_pair_token,
+                                            d_pair_score, true, st, c->ev[TD_PHASE_TOPB][0],
+                                            c->ev[TD_PHASE_TOPB][1]);
+  c->ev[TD_PHASE_TOPB][0] = c->ev[TD_PHASE_TOPB][1] = nullptr;
+  if (e != hipSuccess) return hip_fail(c, e, "beam_topk_append launch");
+  note_append(c);
   return TD_OK;
 }
 
@@ -374,15 +410,7 @@ td_status trie_append_prune(td_ctx* c, const int32_t* d_sel_parent, const int32_
                                          c->ev[TD_PHASE_APPEND][0], c->ev[TD_PHASE_APPEND][1]);
   c->ev[TD_PHASE_APPEND][0] = c->ev[TD_PHASE_APPEND][1] = nullptr;
   if (e != hipSuccess) return hip_fail(c, e, "trie_append_prune launch");
-  // rows move only where this append collects (Alg 2: the next position is a multiple of g)
-  bool collects = false;
-  for (int t = 0; t < c->dev.T; ++t) {
-    ++c->leaf_depth[t];
-    collects = collects || (c->leaf_depth[t] + 1) % c->dev.G == 0;
-  }
-  c->pending = true;
-  c->moves_pending = collects;
-  c->layer_written.assign(c->dev.L, 0);
+  note_append(c);
   return TD_OK;
 }
 

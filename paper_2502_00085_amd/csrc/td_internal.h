@@ -121,7 +121,8 @@ int attn_choose_splits(const DevState& s, int n_layers, int row_blocks);
 hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_t* sel_parent,
                                   int32_t* sel_token, float* sel_score, float* sel_logprob,
                                   float* lse, const int32_t* pair_parent, const int32_t* pair_token,
-                                  float* pair_score, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1);
+                                  float* pair_score, bool append, hipStream_t st, hipEvent_t ev0,
+                                  hipEvent_t ev1);
 int topb_max_chunk_lists();  // limit of b * lse_chunks per trie
 hipError_t launch_append_prune(const DevState& s, const int32_t* sel_parent,
                                const int32_t* sel_token, const float* sel_score, hipStream_t st,

@@ -24,7 +24,7 @@
 // scoring >= L lies in a sub-chunk whose best score is >= L: a hot one.
 // (Two launches instead of a last-arriving-WG merge: a device-scope fence costs an L2
 // writeback + invalidate per WG on this multi-XCD part.)
-#include "td_internal.h"
+#include "trie_append.h"
 
 namespace td {
 
@@ -40,6 +40,7 @@ constexpr int kSub = kChunkWaves;                     // sub-chunks (waves) per 
 constexpr int kPer = 16;                              // entries per lane held in registers
 constexpr int kMaxEntries = 2048;                     // entries per wave (b * chunks per row)
 static_assert(kSub == kFinalThreads / 64, "the final merge maps sub-chunk w of a chunk to wave w");
+static_assert(kAppThreads == kFinalThreads, "the fused merge runs the append with its own block");
 
 // Order-preserving maps of floats to unsigned integers: raw (-0 below +0) for logits, so
 // a key keeps the logit's exact bits; merged zeros for scores (equal scores tie).
@@ -320,8 +321,10 @@ __device__ inline void finish_hypotheses(const DevState& s, int t, uint64_t rank
 
 // Merge of one trie's chunks into the final selection, then the outputs.  PER: entries per
 // lane held in registers (a wave's entries beyond 64 PER are read again); with PER <= 4
-// the second-largest keys are loaded up front too.
-template <int PER>
+// the second-largest keys are loaded up front too.  APPEND: then the trie append of the
+// pairs (when given, with their scores) or else of the selection, by the same block: the
+// append's reads that do not depend on the selection go out with the merge's first loads.
+template <int PER, bool APPEND>
 __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const float* logits,
                                                               int32_t* sel_parent, int32_t* sel_token,
                                                               float* sel_score, float* sel_logprob,
@@ -385,11 +388,14 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     }
   }
   for (int r = threadIdx.x; r < b; r += kFinalThreads) row_score[r] = s.leaf_score[(size_t)t * b + r];
+  __shared__ AppShared ash;
+  AppPre pre;
+  if constexpr (APPEND) append_prefetch(s, t, s.hdr[t], false, ash, pre);
   for (int r = wave; r < b; r += kFinalWaves) {
     const float l = row_lse32_wave(s.lse_part + ((size_t)t * b + r) * nch * 2, nch);
     if (lane == 0) row_lse[r] = l;
   }
-  const int n_live = s.hdr[t].n_live;
+  const int n_live = APPEND ? pre.h.n_live : s.hdr[t].n_live;
   if (threadIdx.x == 0) ncand = nhot = 0;
   __syncthreads();
   const int e_live = n_live * nch;
@@ -598,6 +604,11 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     sel_token[(size_t)t * b + j] = v;
     sel_score[(size_t)t * b + j] = sc;
     sel_logprob[(size_t)t * b + j] = lp;
+    if (APPEND && pair_parent == nullptr) {
+      ash.sp[j] = r;
+      ash.stok[j] = v;
+      ash.ssc[j] = sc;
+    }
     if (j == 0 && s.eos >= 0 && !pool_done)
       finish_hypotheses(s, t, acc_mask, acc_row, acc_val, sc, pool_count, pool_step);
   }
@@ -609,7 +620,13 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     float sc = __uint_as_float(0x7fc00000u);  // NaN for an out-of-range pair
     if (pp >= 0 && pp < n_live && pv >= 0 && pv < V) sc = score_only(pair_x, row_lse[pp], row_score[pp]);
     pair_score[(size_t)t * b + pj] = sc;
+    if (APPEND) {
+      ash.sp[pj] = pp;
+      ash.stok[pj] = pv;
+      ash.ssc[pj] = sc;
+    }
   }
+  if constexpr (APPEND) append_apply(s, t, pre, ash);
 }
 
 }  // namespace
@@ -617,21 +634,27 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
 hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_t* sel_parent,
                                   int32_t* sel_token, float* sel_score, float* sel_logprob,
                                   float* lse, const int32_t* pair_parent, const int32_t* pair_token,
-                                  float* pair_score, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+                                  float* pair_score, bool append, hipStream_t st, hipEvent_t ev0,
+                                  hipEvent_t ev1) {
   hipExtLaunchKernelGGL(k_topb_chunk, dim3(s.lse_chunks, s.b, s.T), dim3(kChunkThreads), 0, st, ev0,
                         nullptr, 0, s, logits);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // entries per wave: b * chunks (every wave covers every row); up to 256 of them fit the
   // 4-per-lane variant
-  if (s.b * s.lse_chunks <= 4 * 64)
-    hipExtLaunchKernelGGL(k_topb_final<4>, dim3(s.T), dim3(kFinalThreads), 0, st, nullptr, ev1, 0, s, logits,
-                          sel_parent, sel_token, sel_score, sel_logprob, lse, pair_parent, pair_token,
-                          pair_score);
-  else
-    hipExtLaunchKernelGGL(k_topb_final<kPer>, dim3(s.T), dim3(kFinalThreads), 0, st, nullptr, ev1, 0, s,
-                          logits, sel_parent, sel_token, sel_score, sel_logprob, lse, pair_parent,
-                          pair_token, pair_score);
+  const bool four = s.b * s.lse_chunks <= 4 * 64;
+#define TOPB_FINAL(PER, APP)                                                                          \
+  hipExtLaunchKernelGGL((k_topb_final<PER, APP>), dim3(s.T), dim3(kFinalThreads), 0, st, nullptr, ev1, 0, s, \
+                        logits, sel_parent, sel_token, sel_score, sel_logprob, lse, pair_parent,        \
+                        pair_token, pair_score)
+  if (append) {
+    if (four) TOPB_FINAL(4, true);
+    else TOPB_FINAL(kPer, true);
+  } else {
+    if (four) TOPB_FINAL(4, false);
+    else TOPB_FINAL(kPer, false);
+  }
+#undef TOPB_FINAL
   return hipGetLastError();
 }
 

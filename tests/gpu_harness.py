@@ -42,10 +42,11 @@ class Run:
 
     def __init__(self, w, seed=0, layers=None, attn_impl=0, capacity=None, mode="scripted",
                  oracle=True, phase_events=False, eos=-1, eos_boost=0.0, length_penalty=1.0,
-                 early_stopping=False):
+                 early_stopping=False, fused=False):
         import torch
         import paper_2502_00085_amd.binding as B
         self.w, self.seed, self.mode, self.phase_events = w, seed, mode, phase_events
+        self.fused = fused  # beam_topk_append instead of beam_logsoftmax_topk + trie_append_prune
         self.eos, self.eos_boost = eos, eos_boost
         self.layers = list(range(w.n_layers)) if layers is None else list(layers)
         self.cap = capacity or w.capacity
@@ -104,12 +105,18 @@ class Run:
         if self.mode == "scripted":
             pp, pt = torch.from_numpy(par).cuda(), torch.from_numpy(tok).cuda()
             ps = torch.empty((T, b), **f32)
-            dec.logsoftmax_topk(ld, sp, st, ss, sl, lse, pp, pt, ps)
-            dec.append_prune(pp, pt, ps)
+            if self.fused:
+                dec.topk_append(ld, sp, st, ss, sl, lse, pp, pt, ps)
+            else:
+                dec.logsoftmax_topk(ld, sp, st, ss, sl, lse, pp, pt, ps)
+                dec.append_prune(pp, pt, ps)
         else:
             ps = None
-            dec.logsoftmax_topk(ld, sp, st, ss, sl, lse)
-            dec.append_prune(sp, st, ss)
+            if self.fused:
+                dec.topk_append(ld, sp, st, ss, sl, lse)
+            else:
+                dec.logsoftmax_topk(ld, sp, st, ss, sl, lse)
+                dec.append_prune(sp, st, ss)
         torch.cuda.synchronize()
         self.pending = True
         res = {"o": from_dev(out), "sel_parent": sp.cpu().numpy(), "sel_token": st.cpu().numpy(),

@@ -28,11 +28,11 @@ def small(**kw):
     return synth.Workload(**base)
 
 
-def run_case(w, seed=0, mode="scripted", impl=B.TD_ATTN_AUTO, capacity=None, repack_steps=()):
+def run_case(w, seed=0, mode="scripted", impl=B.TD_ATTN_AUTO, capacity=None, repack_steps=(), fused=False):
     log(f"gc case T={w.n_tries} L={w.n_layers} Hq={w.n_q_heads} Hkv={w.n_kv_heads} d={w.head_dim} "
         f"{w.dtype} P={w.prompt_min}-{w.prompt_max} b={w.beam_width} W={w.window} g={w.gc_interval} "
-        f"cap={capacity} mode={mode} impl={impl} seed={seed}")
-    r = Run(w, seed, attn_impl=impl, mode=mode, capacity=capacity)
+        f"cap={capacity} mode={mode} impl={impl} seed={seed} fused={fused}")
+    r = Run(w, seed, attn_impl=impl, mode=mode, capacity=capacity, fused=fused)
     prev_base = 0
     repacks, dead_seen = [], 0
     for s in range(1, w.steps + 1):

@@ -22,11 +22,11 @@ def small(**kw):
     return synth.Workload(**base)
 
 
-def run_case(w, seed=0, mode="scripted", impl=B.TD_ATTN_AUTO, steps=None, capacity=None):
+def run_case(w, seed=0, mode="scripted", impl=B.TD_ATTN_AUTO, steps=None, capacity=None, fused=False):
     log(f"case {w.name} T={w.n_tries} L={w.n_layers} Hq={w.n_q_heads} Hkv={w.n_kv_heads} d={w.head_dim} "
         f"{w.dtype} P={w.prompt_min}-{w.prompt_max} b={w.beam_width} V={w.vocab} W={w.window} "
-        f"mode={mode} impl={impl} seed={seed}")
-    r = Run(w, seed, attn_impl=impl, mode=mode, capacity=capacity)
+        f"mode={mode} impl={impl} seed={seed} fused={fused}")
+    r = Run(w, seed, attn_impl=impl, mode=mode, capacity=capacity, fused=fused)
     for _ in range(steps or w.steps):
         errs, _ = r.step()
         assert not errs, "\n".join(errs[:10])
