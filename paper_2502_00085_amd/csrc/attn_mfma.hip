@@ -25,17 +25,11 @@
 // a range start found by binary search on depth.  Waves of a WG and node splits over WGs
 // are merged with max/sum rescaling; the last split WG to finish merges the splits.
 #include "attn_common.h"
+#include "mfma_tile.h"
 
 namespace td {
 
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef short i16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kRows = 32;
 constexpr float kNegBig = -1.0e30f;
@@ -58,19 +52,6 @@ struct MfmaCfg {
   static constexpr int MOVE_LDS = LDS - MOVE0;
   static constexpr int ROW_BYTES = 4 * D;      // K + V of one node row
 };
-
-// Physical 16-byte chunk of logical chunk c of tile row r: rows are rotated by whole
-// 64-byte blocks so that the transposed reads of four consecutive rows hit four
-// different groups of 16 banks.
-template <int CPR, int NBLK>
-__device__ inline int phys_chunk(int r, int c) {
-  return (c + 4 * (r % NBLK)) % CPR;
-}
-
-// s_waitcnt immediates (gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14,
-// expcnt in 6:4, lgkmcnt in 11:8)
-constexpr int kWaitVmAll = 0 | (7 << 4) | (15 << 8);            // vmcnt(0)
-constexpr int kWaitLgkmAll = 15 | (3 << 14) | (7 << 4) | (0 << 8);  // lgkmcnt(0)
 
 // TREE: multi-query tree attention.  The rows are (query node, query head) instead of
 // (live leaf, query head): query j of trie t is the node at logical slot a.qslots[t][j]

@@ -318,13 +318,26 @@ td_status trie_tree_attn(td_ctx* c, int32_t layer_begin, int32_t n_layers, int32
   a.tree = 1;
   a.qslots = d_qslots;
   a.qmax = q_max;
+  hipEvent_t ev0 = c->ev[TD_PHASE_ATTN][0], ev1 = c->ev[TD_PHASE_ATTN][1];
+  const long rows = (long)q_max * (s.Hq / s.Hkv);
+  if (rows >= td::attn_tree_rows_per_block()) {
+    // at least one full block of query rows: the prefill-shaped kernel (256 rows per WG,
+    // the key range streamed once for all of them)
+    const int tpb = td::attn_tree_rows_per_block();
+    a.row_blocks = (int)((rows + tpb - 1) / tpb);
+    a.splits = 1;
+    a.xcd_group = a.row_blocks > 1 && ((long)s.T * n_layers * s.Hkv) % 8 == 0 ? 1 : 0;
+    c->ev[TD_PHASE_ATTN][0] = c->ev[TD_PHASE_ATTN][1] = nullptr;
+    hipError_t e = td::launch_attn_tree(s, a, st, ev0, ev1);
+    if (e != hipSuccess) return hip_fail(c, e, "trie_tree_attn launch");
+    return TD_OK;
+  }
   const int rpb = td::attn_mfma_rows_per_block();
   a.row_blocks = (q_max * (s.Hq / s.Hkv) + rpb - 1) / rpb;
   a.splits = c->splits_override > 0 ? c->splits_override : td::attn_choose_splits(s, n_layers, a.row_blocks);
   const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;
   a.xcd_group = a.row_blocks > 1 && ((long)s.T * n_layers * s.Hkv * a.splits) % 8 == 0 ? 1 : 0;
-  hipEvent_t ev0 = c->ev[TD_PHASE_ATTN][0], ev1 = c->ev[TD_PHASE_ATTN][1];
   c->ev[TD_PHASE_ATTN][0] = c->ev[TD_PHASE_ATTN][1] = nullptr;
   hipError_t e = td::launch_attn_mfma(s, a, st, ev0, a.splits > 1 ? nullptr : ev1);
   if (e == hipSuccess && a.splits > 1) e = td::launch_attn_combine(s, a, rpb, st, nullptr, ev1);

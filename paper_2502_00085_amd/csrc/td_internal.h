@@ -116,6 +116,9 @@ hipError_t launch_attn_valu(const DevState& s, const AttnArgs& a, hipStream_t st
 hipError_t launch_attn_combine(const DevState& s, const AttnArgs& a, int rows_per_block, hipStream_t st,
                                hipEvent_t ev0, hipEvent_t ev1);
 int attn_mfma_rows_per_block();
+int attn_tree_rows_per_block();
+hipError_t launch_attn_tree(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
+                            hipEvent_t ev1);
 int attn_valu_rows_per_block();
 int attn_choose_splits(const DevState& s, int n_layers, int row_blocks);
 hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_t* sel_parent,

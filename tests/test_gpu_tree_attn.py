@@ -102,3 +102,44 @@ def test_long_prefill_of_a_chain_with_branches():
     # 700 prompt nodes and 3 steps: 2800 query rows per KV head, many row blocks
     run_tree(small(n_layers=1, prompt_min=700, prompt_max=700, beam_width=4, steps=3), seed=5,
              pick=every_node)
+
+
+# The prefill-shaped kernel takes query sets of at least one full block (256 rows of
+# (query node, query head)); the cases below reach it with every branch of its visibility
+# test and both block placements.
+
+def shuffled_nodes_with_gaps(tr, g):
+    # every stored node in a random order, each twice, with empty entries: wide key ranges
+    n = len(tr.order)
+    x = np.concatenate([g.permutation(n), g.permutation(n), [-1] * 7]).astype(np.int32)
+    return x[g.permutation(len(x))]
+
+
+def deep_nodes_only(tr, g):
+    # only nodes past the prompt: every half is tested key by key
+    n = len(tr.order)
+    return np.arange(n - 1, max(-1, n - 90), -1, dtype=np.int32)
+
+
+def test_prefill_shuffled_duplicated_queries():
+    run_tree(small(steps=8), seed=6, pick=shuffled_nodes_with_gaps)
+
+
+def test_prefill_deep_nodes_gqa():
+    run_tree(small(steps=12), seed=7, pick=deep_nodes_only)
+
+
+def test_prefill_mha_d96_xcd_grouping():
+    # G = 1: 256 query nodes per block; 2 tries x 2 layers x 2 heads = 8 units (XCD grouping)
+    run_tree(small(n_tries=2, prompt_min=260, prompt_max=300, n_q_heads=2, n_kv_heads=2, head_dim=96,
+                   beam_width=4, steps=5, qkv_std=1.0 / np.sqrt(96.0)), seed=8, pick=every_node)
+
+
+def test_prefill_d64_g2_tight_window():
+    # window 3: most halves are cut by the window; 1 layer x 2 heads (no XCD grouping)
+    run_tree(small(n_layers=1, n_q_heads=4, n_kv_heads=2, head_dim=64, prompt_min=150, prompt_max=150,
+                   window=3, steps=9), seed=9, pick=every_node)
+
+
+def test_prefill_window_deferred_collection_random_order():
+    run_tree(small(window=45, gc_interval=4, steps=14), seed=10, pick=shuffled_nodes_with_gaps)
