@@ -39,8 +39,8 @@ HBM_PEAK_GBS = 8000.0
 # kernel sources it was measured on: reported as null once their digest differs.
 ATTN_TRAFFIC = {
     "workload": "llama8b",
-    "sources_sha256": "2edbe4b9516f0d507dd38e12c4e8c0bd3db0b7eac10d4af2b3c74c2bc6b03f86",
-    "bytes_per_launch": 283740756,             # 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE
+    "sources_sha256": "f90657d41d6f7a5c2f44d5b0e4dca8ea34998dc89bdf07b2ae85d4d9e8579ace",
+    "bytes_per_launch": 283740732,             # 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE
     "algorithmic_bytes_per_launch": 283377664,  # unique K+V rows, q, out
 }
 ATTN_SOURCES = ("attn_mfma.hip", "attn_common.h", "td_internal.h")
@@ -482,7 +482,8 @@ def tree_prefill_time(bench, K, reps):
     """Multi-query tree attention with every stored node of the step-K/2 trie as a query (the
     prefill of that serialized trie, Figure 3's square mask), all layers: `reps` launches
     graph-replayed between events.  Returns (ms per launch, queries, algorithmic flops per
-    launch = 4 d Hq L x the keys each query sees, summed over the queries)."""
+    launch = 4 d Hq L x the keys each query sees, summed over the queries).  Three replays
+    warm up first."""
     import torch
     stream = torch.cuda.current_stream().cuda_stream
     L, ctx, w = bench.B.lib(), bench.dec.ctx, bench.w
@@ -526,7 +527,8 @@ def tree_prefill_time(bench, K, reps):
             st |= L.trie_tree_attn(*args, s_)
     if st != 0:
         raise RuntimeError(bench.B.td_error_string(ctx))
-    graph.replay()
+    for _ in range(3):  # (the clocks settle over the first few dozen launches)
+        graph.replay()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
