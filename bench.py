@@ -274,6 +274,8 @@ def gpu_bench(args, w, K):
     finished = [bench.dec.read_finished(t) for t in range(w.n_tries)] if args.eos >= 0 else None
     attn_graph_ms, attn_graph_nodes = attn_graph_time(bench, K, args.attn_reps)
     attn_cold_ms = attn_cold_time(bench, max(4, args.attn_reps // 4))
+    per_layer_ms = attn_per_layer_time(bench, max(4, args.attn_reps // 4))
+    copy_gbs = device_copy_gbs()
     tree = None if args.no_tree or w.dtype != "bf16" else tree_prefill_time(bench, K, 8)
     phase_ms = phase_times(bench, K)
     nodes = bench.nodes_per_step(K)
@@ -282,7 +284,7 @@ def gpu_bench(args, w, K):
     batch = None if args.no_batch_baseline else batch_bench(bench, K, args.warmup)
     return dict(mode=mode, seconds=t1 - t0, eager_seconds=eager_s, attn_ms=attn_ms, nodes=nodes,
                 attn_graph_ms=attn_graph_ms, attn_graph_nodes=attn_graph_nodes, phase_ms=phase_ms,
-                attn_cold_ms=attn_cold_ms,
+                attn_cold_ms=attn_cold_ms, per_layer_ms=per_layer_ms, copy_gbs=copy_gbs,
                 collects=collects, stored=bench.stored, batch=batch, finished=finished, tree=tree,
                 qo_bytes=int(bench.q[0].numel() * bench.q[0].element_size() +
                              bench.out.numel() * bench.out.element_size()))
@@ -478,6 +480,55 @@ def attn_cold_time(bench, reps):
     return float(np.mean(ms))
 
 
+def attn_per_layer_time(bench, reps):
+    """The same step-64 trie attended by L one-layer trie_attn_decode calls (one per layer,
+    as a model interleaves them with its other layers' work), the L calls captured in a
+    graph and replayed `reps` times between events.  Returns ms per step (all L calls)."""
+    import torch
+    L, ctx, w = bench.B.lib(), bench.dec.ctx, bench.w
+    q, out = bench.q[0], bench.out
+    lq = q[0].numel() * q.element_size()  # bytes of one layer's queries (and outputs)
+    graph, cs = torch.cuda.CUDAGraph(), torch.cuda.Stream()
+    st = 0
+    with torch.cuda.graph(graph, stream=cs):
+        s_ = torch.cuda.current_stream().cuda_stream
+        for layer in range(w.n_layers):
+            st |= L.trie_attn_decode(ctx, layer, 1, q.data_ptr() + layer * lq, None, None,
+                                     out.data_ptr() + layer * lq, ctypes.c_float(bench.scale), s_)
+    if st != 0:
+        raise RuntimeError(bench.B.td_error_string(ctx))
+    for _ in range(2):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def device_copy_gbs(mib=1024, reps=10):
+    """Bandwidth of a plain device-to-device copy of `mib` MiB (torch copy_), read + write
+    bytes over time: the measured reference the roofline is also quoted against."""
+    import torch
+    src = torch.ones(mib << 18, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    return 2.0 * (mib << 20) / (ms / 1e3) / 1e9
+
+
 def tree_prefill_time(bench, K, reps):
     """Multi-query tree attention with every stored node of the step-K/2 trie as a query (the
     prefill of that serialized trie, Figure 3's square mask), all layers: `reps` launches
@@ -627,7 +678,15 @@ def main():
                      "attn_us_llc_cold": round(r["attn_cold_ms"] * 1e3, 2),
                      "achieved_llc_cold": round(graph_bytes / (r["attn_cold_ms"] / 1e3) / 1e9, 1),
                      "llc_cold": "the same launch with the 256 MB last-level cache cleared before it "
-                                 "(a 1 GiB read), timed alone by kernel-timestamp events"},
+                                 "(a 1 GiB read), timed alone by kernel-timestamp events",
+                     "device_copy_gbs": round(r["copy_gbs"], 1),
+                     "frac_of_device_copy": round(achieved / r["copy_gbs"], 4),
+                     "device_copy": "a plain 1 GiB device-to-device copy (torch copy_), read + write bytes "
+                                    "over time, on the same GPU in the same run",
+                     "attn_us_per_step_layer_calls": round(r["per_layer_ms"] * 1e3, 2),
+                     "layer_calls": f"the same trie attended by {w.n_layers} one-layer calls (as a model "
+                                    "interleaves them with its other work), graph-replayed: all calls of a "
+                                    "step"},
         "hbm_gbps_unique_kv_whole_step": round(float(kv_bytes.mean() / (ms_per_step / 1e3) / 1e9), 1),
         "eager_ms_per_step": round(r["eager_seconds"] * 1e3 / K, 5),
         "nodes_per_step_mean": round(float(r["nodes"].sum(axis=1).mean()), 1),

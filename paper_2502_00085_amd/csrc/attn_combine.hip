@@ -1,7 +1,8 @@
 // Merge of node-split attention partials (when one (trie, layer, KV head) is split over
 // several WGs to fill the chip).  Each split wrote, per query row of its block, the
-// unnormalised output O, its running max M (log2 domain) and sum L; the merge rescales
-// every split to the common max:  out = sum_s O_s 2^(M_s - M) / sum_s L_s 2^(M_s - M).
+// unnormalised output O, its running max M (log2 domain) and sum L ([unit][split][row]
+// records of D + 2 floats); the merge rescales every split to the common max:
+// out = sum_s O_s 2^(M_s - M) / sum_s L_s 2^(M_s - M).
 // A separate launch (instead of a last-arriving-WG merge) avoids device-scope fences,
 // which cost an L2 writeback + invalidate per WG on this multi-XCD part.
 #include "attn_common.h"
@@ -10,9 +11,28 @@ namespace td {
 
 namespace {
 
+constexpr int kCombineThreads = 256;
+
+__device__ inline void store8(float* p, const float* v) {
+  reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+  reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+__device__ inline void store8(__bf16* p, const float* v) {
+  typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+  bf16x8_t y;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) y[e] = (__bf16)v[e];
+  *reinterpret_cast<bf16x8_t*>(p) = y;
+}
+
+// Grid: (trie, layer, KV head, row block) units x parts; each thread one (row, 8-element
+// chunk of d).  The splits' maxima, then their sums and 8-element O chunks, are loaded
+// with the loop unrolled so that the loads of several splits are in flight together (the
+// merge is a few dependent memory rounds, not one per split).
 template <typename T>
-__global__ __launch_bounds__(256) void k_attn_combine(DevState s, AttnArgs a, int R) {
-  const int unit = blockIdx.x;  // ((t * nl + li) * Hkv + g) * row_blocks + rb
+__global__ __launch_bounds__(kCombineThreads) void k_attn_combine(DevState s, AttnArgs a, int R, int parts) {
+  const int unit = blockIdx.x / parts;  // ((t * nl + li) * Hkv + g) * row_blocks + rb
+  const int item = (blockIdx.x % parts) * kCombineThreads + (int)threadIdx.x;
   int x = unit;
   const int rb = x % a.row_blocks;
   x /= a.row_blocks;
@@ -22,38 +42,54 @@ __global__ __launch_bounds__(256) void k_attn_combine(DevState s, AttnArgs a, in
   const int t = x / a.n_layers;
   const int G = s.Hq / s.Hkv;
   const int D = s.D;
-  const int n_live = s.hdr[t].n_live;
-  const float* part = s.attn_part + (size_t)unit * a.splits * R * (D + 2);
-  T* outp = static_cast<T*>(a.out);
+  const int CH = D / 8;
+  if (item >= R * CH) return;
+  const int i = item / CH, c = (item % CH) * 8;
+  const int rr = rb * R + i;
   const int nrows = a.tree ? a.qmax : s.b;  // row owners per trie in out
-  for (int idx = threadIdx.x; idx < R * D; idx += blockDim.x) {
-    const int i = idx / D, c = idx % D;
-    const int rr = rb * R + i;
-    if (rr >= nrows * G) continue;
-    float M = -1.0e30f;
-    for (int sp = 0; sp < a.splits; ++sp) M = fmaxf(M, part[((size_t)sp * R + i) * (D + 2) + D]);
-    float L = 0.0f, O = 0.0f;
-    for (int sp = 0; sp < a.splits; ++sp) {
-      const float* pp = part + ((size_t)sp * R + i) * (D + 2);
-      const float f = exp2f(pp[D] - M);
-      L += pp[D + 1] * f;
-      O += pp[c] * f;
+  if (rr >= nrows * G) return;
+  const int n_live = s.hdr[t].n_live;
+  const size_t stride = (size_t)R * (D + 2);  // one split's records
+  const float* rec = s.attn_part + (size_t)unit * a.splits * stride + (size_t)i * (D + 2);
+  float M = -1.0e30f;
+#pragma unroll 8
+  for (int sp = 0; sp < a.splits; ++sp) M = fmaxf(M, rec[sp * stride + D]);
+  float L = 0.0f, O[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) O[e] = 0.0f;
+#pragma unroll 8
+  for (int sp = 0; sp < a.splits; ++sp) {
+    const float* pp = rec + sp * stride;
+    const float f = exp2f(pp[D] - M);
+    L += pp[D + 1] * f;
+    // (records are D + 2 floats: 8-byte aligned)
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const float2 v = *reinterpret_cast<const float2*>(pp + c + e);
+      O[e] += v.x * f;
+      O[e + 1] += v.y * f;
     }
-    const int bm = rr / G;
-    const float val = ((a.tree || bm < n_live) && L > 0.0f) ? O / L : 0.0f;
-    outp[((((size_t)li * s.T + t) * nrows + bm) * s.Hq + g * G + rr % G) * D + c] = (T)val;
   }
+  const int bm = rr / G;
+  const float inv = ((a.tree || bm < n_live) && L > 0.0f) ? 1.0f / L : 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) O[e] *= inv;
+  T* outp = static_cast<T*>(a.out);
+  store8(outp + ((((size_t)li * s.T + t) * nrows + bm) * s.Hq + g * G + rr % G) * D + c, O);
 }
 
 }  // namespace
 
 hipError_t launch_attn_combine(const DevState& s, const AttnArgs& a, int rows_per_block, hipStream_t st,
                                hipEvent_t ev0, hipEvent_t ev1) {
-  const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks);
+  const int parts = (rows_per_block * (s.D / 8) + kCombineThreads - 1) / kCombineThreads;
+  const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * parts);
   if (s.dtype == TD_F32)
-    hipExtLaunchKernelGGL(k_attn_combine<float>, grid, dim3(256), 0, st, ev0, ev1, 0, s, a, rows_per_block);
+    hipExtLaunchKernelGGL(k_attn_combine<float>, grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a,
+                          rows_per_block, parts);
   else
-    hipExtLaunchKernelGGL(k_attn_combine<__bf16>, grid, dim3(256), 0, st, ev0, ev1, 0, s, a, rows_per_block);
+    hipExtLaunchKernelGGL(k_attn_combine<__bf16>, grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a,
+                          rows_per_block, parts);
   return hipGetLastError();
 }
 
