@@ -75,6 +75,7 @@ def test_null_context_is_rejected_by_every_call():
     assert L.trie_attn_decode(None, 0, 1, None, None, None, None, 1.0, None) == B.TD_EINVAL
     assert L.beam_logsoftmax_topk(None, *([None] * 10)) == B.TD_EINVAL
     assert L.trie_append_prune(None, None, None, None, None) == B.TD_EINVAL
+    assert L.beam_topk_append(None, *([None] * 10)) == B.TD_EINVAL
     assert L.td_get_status(None) == B.TD_EINVAL
     assert L.td_read_state(None, 0, None) == B.TD_EINVAL
     assert L.td_load_state(None, 0, None) == B.TD_EINVAL

@@ -143,3 +143,33 @@ def test_prefill_d64_g2_tight_window():
 
 def test_prefill_window_deferred_collection_random_order():
     run_tree(small(window=45, gc_interval=4, steps=14), seed=10, pick=shuffled_nodes_with_gaps)
+
+
+def test_tree_attn_rejects_bad_arguments():
+    import torch
+    import paper_2502_00085_amd.binding as B
+    w = small(steps=2, n_layers=1)
+    r = Run(w, 11)
+    r.step()  # the leaves of step 1 are pending
+    qs = torch.zeros((1, 4), dtype=torch.int32, device="cuda")
+    q = torch.zeros((1, 1, 4, w.n_q_heads, w.head_dim), dtype=torch.bfloat16, device="cuda")
+    out = torch.empty_like(q)
+    L, ctx = B.lib(), r.dec.ctx
+    args = lambda qmax, qsp, qp, op, sc: (ctx, 0, 1, qmax, qsp, qp, op, sc, None)
+    assert L.trie_tree_attn(*args(4, qs.data_ptr(), q.data_ptr(), out.data_ptr(), 1.0)) == B.TD_ESTATE
+    q2, kn, vn, _, _, _ = r.inputs(2)
+    qd = to_dev(w, q2)
+    r.dec.attn_decode(0, w.n_layers, qd, to_dev(w, kn), to_dev(w, vn), torch.empty_like(qd), r.scale)
+    assert L.trie_tree_attn(*args(0, qs.data_ptr(), q.data_ptr(), out.data_ptr(), 1.0)) == B.TD_EINVAL
+    assert L.trie_tree_attn(*args(4, None, q.data_ptr(), out.data_ptr(), 1.0)) == B.TD_EINVAL
+    assert L.trie_tree_attn(*args(4, qs.data_ptr(), q.data_ptr() + 2, out.data_ptr(), 1.0)) == B.TD_EINVAL
+    assert L.trie_tree_attn(*args(4, qs.data_ptr(), q.data_ptr(), out.data_ptr(), 0.0)) == B.TD_EINVAL
+    assert L.trie_tree_attn(ctx, 0, 2, 4, qs.data_ptr(), q.data_ptr(), out.data_ptr(), 1.0, None) == B.TD_EINVAL
+    assert L.trie_tree_attn(*args(4, qs.data_ptr(), q.data_ptr(), out.data_ptr(), 1.0)) == B.TD_OK
+    torch.cuda.synchronize()
+    r.dec.close()
+    # the vector-ALU kernel and fp32 have no tree variant
+    r2 = Run(synth.WORKLOADS["tiny"], 0, oracle=False)
+    assert L.trie_tree_attn(r2.dec.ctx, 0, 1, 4, qs.data_ptr(), q.data_ptr(), out.data_ptr(), 1.0,
+                            None) == B.TD_EUNSUPPORTED
+    r2.dec.close()
