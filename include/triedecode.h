@@ -13,6 +13,9 @@
  *                         Alg 2), then, every g-th position, garbage-collect: mark,
  *                         prune, compact (Section 3.5)
  *
+ * beam_topk_append does the last two in one call (same results).  trie_tree_attn runs
+ * the same attention with any set of stored nodes as queries (a prefill, or draft nodes).
+ *
  * Memory.  The caller owns every tensor (K/V pools, queries, outputs, logits and
  * selections) as device memory; PyTorch tensors are the intended source.  The library
  * owns only the trie metadata and a fixed workspace, both allocated in td_create.  The
