@@ -156,8 +156,8 @@ td_status trie_attn_decode(td_ctx* ctx, int32_t layer_begin, int32_t n_layers, c
  * on no live leaf's path (a dead node awaiting collection), is written as zeros.  Every
  * node's K/V must be in the pools: TD_ESTATE while the leaves' rows are pending.  Needs the
  * matrix-core kernel (bf16, attn_impl != TD_ATTN_VALU), else TD_EUNSUPPORTED.  q_max >= 1
- * and q_max * (Hq/Hkv) <= 2^24, else TD_EINVAL.  Query sets of at least 256 rows
- * (q_max * Hq/Hkv) run on a prefill-shaped kernel (256 rows per workgroup, the key range
+ * and q_max * (Hq/Hkv) <= 2^24, else TD_EINVAL.  Query sets of at least 128 rows
+ * (q_max * Hq/Hkv) run on a prefill-shaped kernel (128 rows per workgroup, the key range
  * streamed once for all of them); smaller ones on the decode layout with node splits. */
 td_status trie_tree_attn(td_ctx* ctx, int32_t layer_begin, int32_t n_layers, int32_t q_max,
                          const int32_t* d_qslots, const void* d_q, void* d_out, float scale,

@@ -5,9 +5,10 @@
 // on a live path is exactly the ancestor-or-self relation, within the window of depth(q).
 // When many nodes are queries (the prefill of a serialized trie), the decode kernel's
 // layout is wasteful: each 32-row block streams its whole key range through LDS for 32 x
-// 32 scores per tile.  Here a WG of 8 waves holds 256 query rows (wave w: rows 32w ..
+// 32 scores per tile.  Here a WG of 4 waves holds 128 query rows (wave w: rows 32w ..
 // 32w + 31, each a (query node, query head) pair of one KV head) and streams the key range
-// once for all of them:
+// once for all of them; two such WGs share a CU (64 KiB of LDS and 256 VGPRs each at
+// d = 128), so one computes while the other waits at its tile barrier:
 //
 //   * a tile is 64 keys (two 32-key halves), K and V loaded by the whole WG with direct
 //     16-byte global -> LDS loads into one of two buffers while the other is consumed;
@@ -28,7 +29,7 @@ namespace td {
 
 namespace {
 
-constexpr int kTreeWaves = 8;
+constexpr int kTreeWaves = 4;  // (two WGs per CU: their barriers do not wait on each other)
 constexpr int kTreeThreads = kTreeWaves * 64;
 constexpr int kTreeRows = kTreeWaves * 32;  // query rows per WG
 constexpr float kTreeNegBig = -1.0e30f;
@@ -46,7 +47,7 @@ struct TreeCfg {
 };
 
 template <int D>
-__global__ __launch_bounds__(kTreeThreads) void k_attn_tree(DevState s, AttnArgs a) {
+__global__ __launch_bounds__(kTreeThreads, 2) void k_attn_tree(DevState s, AttnArgs a) {
   using C = TreeCfg<D>;
   __shared__ __attribute__((aligned(16))) unsigned char lds[2 * C::TILE];
   __shared__ int wred[2][kTreeWaves];  // per wave: deepest query slot + 1, shallowest depth

@@ -321,7 +321,7 @@ td_status trie_tree_attn(td_ctx* c, int32_t layer_begin, int32_t n_layers, int32
   hipEvent_t ev0 = c->ev[TD_PHASE_ATTN][0], ev1 = c->ev[TD_PHASE_ATTN][1];
   const long rows = (long)q_max * (s.Hq / s.Hkv);
   if (rows >= td::attn_tree_rows_per_block()) {
-    // at least one full block of query rows: the prefill-shaped kernel (256 rows per WG,
+    // at least one full block of query rows: the prefill-shaped kernel (128 rows per WG,
     // the key range streamed once for all of them)
     const int tpb = td::attn_tree_rows_per_block();
     a.row_blocks = (int)((rows + tpb - 1) / tpb);

@@ -104,9 +104,25 @@ def test_long_prefill_of_a_chain_with_branches():
              pick=every_node)
 
 
-# The prefill-shaped kernel takes query sets of at least one full block (256 rows of
+# The prefill-shaped kernel takes query sets of at least one full block (128 rows of
 # (query node, query head)); the cases below reach it with every branch of its visibility
-# test and both block placements.
+# test and both block placements.  Smaller sets run on the decode layout (the first cases
+# of this file with fewer than 128 rows, and the ones right below).
+
+def few_nodes(tr, g):
+    # 20 random nodes and empty entries: 88 rows at G = 4, the decode-layout variant
+    n = len(tr.order)
+    x = g.choice(n, size=min(n, 20), replace=False).astype(np.int32)
+    return np.concatenate([[-1], x, [-1]]).astype(np.int32)
+
+
+def test_small_set_decode_layout_window_deferred():
+    run_tree(small(window=30, gc_interval=5, steps=13), seed=12, pick=few_nodes)
+
+
+def test_small_set_decode_layout_several_tries():
+    run_tree(small(n_tries=2, prompt_min=40, prompt_max=90, steps=7), seed=13, pick=few_nodes)
+
 
 def shuffled_nodes_with_gaps(tr, g):
     # every stored node in a random order, each twice, with empty entries: wide key ranges
