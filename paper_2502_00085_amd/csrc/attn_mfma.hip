@@ -60,8 +60,13 @@ struct MfmaCfg {
 // relation), within the window of the query's depth.  A block's key range ends at its
 // deepest query slot (ancestors precede their descendants in slot order) and starts at the
 // window of its shallowest query.  Nothing is pending: no leaf rows, no moves.
-template <int D, int NW, bool TREE>
+//
+// RB: 32-row blocks per WG (decode only).  With b G = 64 query rows per KV head (say b = 16
+// at G = 4) one WG takes both blocks: each wave's tile serves 64 rows, instead of two WGs
+// streaming the same nodes side by side.
+template <int D, int NW, bool TREE, int RB>
 __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
+  static_assert(RB == 1 || (RB == 2 && !TREE), "two row blocks per WG: decode only");
   using C = MfmaCfg<D, NW>;
   __shared__ __attribute__((aligned(16))) unsigned char lds[C::LDS];
   const AttnUnit u = attn_unit(s, a);
@@ -74,8 +79,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   const uint64_t* maskp = s.mask + (size_t)u.t * s.cap + base;
   const int32_t* depthp = s.depth + (size_t)u.t * s.cap + base;
 
-  // this lane's query row: r = (leaf or query node) * G + query head within the group
-  const int r = u.rb * kRows + col;
+  // this lane's query row (of the WG's first row block): r = (leaf or query node) * G +
+  // query head within the group
+  const int r = u.rb * RB * kRows + col;
   const int nrows = TREE ? a.qmax : s.b;  // row owners per trie in q / out
   const int owner = r / G;                // leaf rank, or query index
   bool row_ok;
@@ -125,6 +131,10 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   // issued with the first tile, then written after the main loop.  More: the table goes to
   // LDS (one block barrier) and the rows are copied at the end.  More than that table
   // holds: copied first.  The leaf store, whose slots may be sources of moves, follows.
+  // (two row blocks: their query rows sit in LDS, ahead of the staging area)
+  constexpr int kQBytes = RB == 2 ? RB * kRows * D * 2 : 0;
+  constexpr int kMove0 = C::MOVE0 + kQBytes, kMoveLds = C::MOVE_LDS - kQBytes;
+  static_assert(kMoveLds > 0, "LDS for the staging area");
   const int nmoves = a.moves ? s.n_moves[u.t] : 0;
   const int first_moved = nmoves > 0 ? s.moves[(size_t)u.t * s.cap].y - base : INT_MAX;
   // The pending leaves' rows of a WG whose range holds them are staged the same way (from
@@ -135,12 +145,12 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   const int leaf_bytes = (leaf_chunks + 63) / 64 * 1024;
   const int stage_chunks = nmoves * 2 * C::CPR;        // 16-byte chunks of the moved rows
   const bool staged = nmoves > 0 && nmoves <= kRegMoves &&
-                      (leaves_here ? leaf_bytes : 0) + (stage_chunks + 63) / 64 * 1024 <= C::MOVE_LDS;
-  int* msrc = reinterpret_cast<int*>(lds + C::MOVE0);  // [nmoves] source slot - base (late)
-  const bool late_copy = nmoves > 0 && !staged && nmoves * 4 <= C::MOVE_LDS;
-  const bool leaves_staged = leaves_here && (nmoves == 0 || staged) && leaf_bytes <= C::MOVE_LDS;
-  unsigned char* lstage = lds + C::MOVE0;                                  // staged leaf rows
-  unsigned char* mstage = lds + C::MOVE0 + (leaves_staged ? leaf_bytes : 0);  // staged moved rows
+                      (leaves_here ? leaf_bytes : 0) + (stage_chunks + 63) / 64 * 1024 <= kMoveLds;
+  int* msrc = reinterpret_cast<int*>(lds + kMove0);  // [nmoves] source slot - base (late)
+  const bool late_copy = nmoves > 0 && !staged && nmoves * 4 <= kMoveLds;
+  const bool leaves_staged = leaves_here && (nmoves == 0 || staged) && leaf_bytes <= kMoveLds;
+  unsigned char* lstage = lds + kMove0;                                  // staged leaf rows
+  unsigned char* mstage = lds + kMove0 + (leaves_staged ? leaf_bytes : 0);  // staged moved rows
   int mt0 = 0, mt1 = 0;  // register source table (staged)
   if (staged) {
     const int2* mv = s.moves + (size_t)u.t * s.cap;
@@ -169,12 +179,17 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   // block, 4-element column quarter q
   const int grp = lane >> 4, tm = (lane & 15) >> 2, tq = lane & 3;
 
-  float m = kNegBig, lsum = 0.0f;
-  f32x16 o[C::DT];
+  float m[RB], lsum[RB];
+  f32x16 o[RB][C::DT];
 #pragma unroll
-  for (int dt = 0; dt < C::DT; ++dt)
+  for (int k = 0; k < RB; ++k) {
+    m[k] = kNegBig;
+    lsum[k] = 0.0f;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) o[dt][v] = 0.0f;
+    for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) o[k][dt][v] = 0.0f;
+  }
 
   const int ntiles = n1 > n0 ? (n1 - n0 + 31) / 32 : 0;
   const int my_tiles = ntiles > wave ? (ntiles - wave + NW - 1) / NW : 0;
@@ -184,15 +199,16 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   // reads of 16 consecutive rows then hit 16 different bank groups); V rows by one
   // 64-byte block per row (transposed reads of 4 consecutive rows use 4 bank groups).
   // koff / voff: element offset, inside the row, of the logical chunk this lane loads.
+  auto tile_geom = [&](int i, int ln, int& row, int& ko, int& vo) {
+    const int p = 64 * i + ln;
+    const int pc = p % C::CPR;
+    row = p / C::CPR;
+    ko = (pc + C::CPR - row % C::CPR) % C::CPR * 8;
+    vo = (pc + C::CPR - 4 * (row % C::NBLK)) % C::CPR * 8;
+  };
   int vrow[C::VINST], koff[C::VINST], voff[C::VINST];
 #pragma unroll
-  for (int i = 0; i < C::VINST; ++i) {
-    const int p = 64 * i + lane;
-    const int row = p / C::CPR, pc = p % C::CPR;
-    vrow[i] = row;
-    koff[i] = (pc + C::CPR - row % C::CPR) % C::CPR * 8;
-    voff[i] = (pc + C::CPR - 4 * (row % C::NBLK)) % C::CPR * 8;
-  }
+  for (int i = 0; i < C::VINST; ++i) tile_geom(i, lane, vrow[i], koff[i], voff[i]);
   // this lane's K operand chunks for the 32x32x16 steps: row col, logical chunk
   // hh * CPR / 2 + t, rotated by col
   int kread[C::KSTEPS];
@@ -219,7 +235,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < C::VINST; ++i) {
-      const int nv = full ? tb + vrow[i] : min(tb + vrow[i], n1 - 1);
+      int vr = vrow[i], ko = koff[i], vo = voff[i];
+      if constexpr (RB == 2) {  // (recomputed per call: registers are short with two row blocks)
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        tile_geom(i, ln, vr, ko, vo);
+      }
+      const int nv = full ? tb + vr : min(tb + vr, n1 - 1);
       const bool leaf = nv >= leaf0;
       int src = nv;
       if (any_moved) {
@@ -233,8 +255,8 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
         }
       }
       const size_t kr = leaf ? (size_t)(nv - leaf0) * leaf_stride : (size_t)src * D;
-      const __bf16* ks = (leaf ? knew : kpool) + kr + koff[i];
-      const __bf16* vs = (leaf ? vnew : vpool) + kr + voff[i];
+      const __bf16* ks = (leaf ? knew : kpool) + kr + ko;
+      const __bf16* vs = (leaf ? vnew : vpool) + kr + vo;
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)ks,
                                        (__attribute__((address_space(3))) void*)(kbuf + i * 1024), 16, 0, 0);
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)vs,
@@ -269,24 +291,37 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     for (int k = threadIdx.x; k < nmoves; k += NW * 64) msrc[k] = s.moves[(size_t)u.t * s.cap + k].x - base;
     __syncthreads();
   } else if (nmoves > 0) {
-    move_rows_block<__bf16>(s, u.t, lab, u.g, reinterpret_cast<uint4*>(lds + C::MOVE0), C::MOVE_LDS / 16);
+    move_rows_block<__bf16>(s, u.t, lab, u.g, reinterpret_cast<uint4*>(lds + kMove0), kMoveLds / 16);
   }
   if (my_tiles > 0 && !early) issue(wave);
   // (the query rows load while the first tile is in flight)
-  // this lane's query row (B operand of S^T): half hh of the row's d range
-  const int beam_bit = owner < 64 ? owner : 63;
-  bf16x8 qv[C::KSTEPS];
-  {
-    const uint4* qp = reinterpret_cast<const uint4*>(
-        static_cast<const __bf16*>(a.q) +
-        ((((size_t)u.li * s.T + u.t) * nrows + (row_ok ? owner : 0)) * s.Hq + u.g * G + r % G) * D +
-        hh * (D / 2));
+  // this lane's query row of each row block (B operand of S^T): half hh of its d range
+  int beam_bit[RB];
+  bool rok[RB];
+  bf16x8 qv[RB][C::KSTEPS];
+  unsigned char* qlds = lds + C::MOVE0;  // (two row blocks) [64 rows][D], chunks rotated by row
 #pragma unroll
-    for (int t = 0; t < C::KSTEPS; ++t) {
-      const uint4 x = row_ok ? qp[t] : make_uint4(0, 0, 0, 0);
-      qv[t] = __builtin_bit_cast(bf16x8, x);
+  for (int k = 0; k < RB; ++k) {
+    const int rk = r + k * kRows, ok_ = k == 0 ? row_ok : (rk < s.b * G && rk / G < n_live);
+    rok[k] = ok_;
+    beam_bit[k] = rk / G < 64 ? rk / G : 63;
+    if (RB == 1 || wave == 0) {
+      const uint4* qp = reinterpret_cast<const uint4*>(
+          static_cast<const __bf16*>(a.q) +
+          ((((size_t)u.li * s.T + u.t) * nrows + (ok_ ? rk / G : 0)) * s.Hq + u.g * G + rk % G) * D +
+          hh * (D / 2));
+#pragma unroll
+      for (int t = 0; t < C::KSTEPS; ++t) {
+        const uint4 x = ok_ ? qp[t] : make_uint4(0, 0, 0, 0);
+        qv[k][t] = __builtin_bit_cast(bf16x8, x);
+        if (RB == 2) {
+          const int row = k * kRows + col;
+          *reinterpret_cast<bf16x8*>(qlds + row * (2 * D) + (hh * (C::CPR / 2) + t + row) % C::CPR * 16) = qv[k][t];
+        }
+      }
     }
   }
+  if constexpr (RB == 2) __syncthreads();  // the query rows are in LDS
 
   for (int k = 0; k < my_tiles; ++k) {
     const int tile = wave + NW * k;
@@ -300,6 +335,22 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     bf16x8 kv[C::KSTEPS];
 #pragma unroll
     for (int t = 0; t < C::KSTEPS; ++t) kv[t] = *reinterpret_cast<const bf16x8*>(kbuf + kread[t]);
+    // (two row blocks: both blocks' scores first, so that the K operands are dead before the
+    // V operands are read; the query rows come from LDS)
+    f32x16 acc2[RB];
+    if constexpr (RB == 2) {
+#pragma unroll
+      for (int rbk = 0; rbk < RB; ++rbk) {
+        const int row = rbk * kRows + col;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc2[rbk][v] = 0.0f;
+#pragma unroll
+        for (int t = 0; t < C::KSTEPS; ++t) {
+          const bf16x8 qk = *reinterpret_cast<const bf16x8*>(qlds + row * (2 * D) + (hh * (C::CPR / 2) + t + row) % C::CPR * 16);
+          acc2[rbk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv[t], qk, acc2[rbk], 0, 0, 0);
+        }
+      }
+    }
     bf16x8 va[2][C::DT];
     const __bf16* vb = reinterpret_cast<const __bf16*>(vbuf);
 #pragma unroll
@@ -324,82 +375,90 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     __builtin_amdgcn_s_waitcnt(kWaitLgkmAll);
     if (k + 1 < my_tiles) issue(tile + NW);
 
-    f32x16 acc;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+    for (int rbk = 0; rbk < RB; ++rbk) {  // each row block on the same K and V operands
+      f32x16 acc;
+      if constexpr (RB == 2) {
+        acc = acc2[rbk];
+      } else {
 #pragma unroll
-    for (int t = 0; t < C::KSTEPS; ++t)
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv[t], qv[t], acc, 0, 0, 0);
+        for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+#pragma unroll
+        for (int t = 0; t < C::KSTEPS; ++t)
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv[t], qv[rbk][t], acc, 0, 0, 0);
+      }
 
-    // visibility of this lane's nodes 8(v/4) + 4hh + v%4: all inside the shared prefix of
-    // a full tile (wave-uniform test); otherwise range end and the ancestor bit of the
-    // row's beam; hidden scores become -inf
-    if constexpr (TREE) {
-      // ancestor-or-self of the row's query node, within its window; the node's depth and
-      // mask come from the lane that loaded them.  Branch-free: the test only selects.  (A
-      // form with loads under per-node branches was compiled by hipcc with the mask and
-      // window conditions of the first node dropped.)
-      const int mlo = (int)(uint32_t)cmk, mhi = (int)(uint32_t)(cmk >> 32);
-      const uint32_t qlo = (uint32_t)qmask, qhi = (uint32_t)(qmask >> 32);
-      uint32_t vis = 0;
+      // visibility of this lane's nodes 8(v/4) + 4hh + v%4: all inside the shared prefix of
+      // a full tile (wave-uniform test); otherwise range end and the ancestor bit of the
+      // row's beam; hidden scores become -inf
+      if constexpr (TREE) {
+        // ancestor-or-self of the row's query node, within its window; the node's depth and
+        // mask come from the lane that loaded them.  Branch-free: the test only selects.  (A
+        // form with loads under per-node branches was compiled by hipcc with the mask and
+        // window conditions of the first node dropped.)
+        const int mlo = (int)(uint32_t)cmk, mhi = (int)(uint32_t)(cmk >> 32);
+        const uint32_t qlo = (uint32_t)qmask, qhi = (uint32_t)(qmask >> 32);
+        uint32_t vis = 0;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int i = 8 * (v >> 2) + 4 * hh + (v & 3);
-        const int dn = __builtin_amdgcn_ds_bpermute(i << 2, cdep);
-        const uint32_t lo_ = (uint32_t)__builtin_amdgcn_ds_bpermute(i << 2, mlo);
-        const uint32_t hi_ = (uint32_t)__builtin_amdgcn_ds_bpermute(i << 2, mhi);
-        const bool ok = (tb + i < n1) & (dn <= qdepth) & ((lo_ & qlo) == qlo) & ((hi_ & qhi) == qhi) &
-                        ((s.W <= 0) | (qdepth - dn < s.W));
-        vis |= (uint32_t)ok << v;
+        for (int v = 0; v < 16; ++v) {
+          const int i = 8 * (v >> 2) + 4 * hh + (v & 3);
+          const int dn = __builtin_amdgcn_ds_bpermute(i << 2, cdep);
+          const uint32_t lo_ = (uint32_t)__builtin_amdgcn_ds_bpermute(i << 2, mlo);
+          const uint32_t hi_ = (uint32_t)__builtin_amdgcn_ds_bpermute(i << 2, mhi);
+          const bool ok = (tb + i < n1) & (dn <= qdepth) & ((lo_ & qlo) == qlo) & ((hi_ & qhi) == qhi) &
+                          ((s.W <= 0) | (qdepth - dn < s.W));
+          vis |= (uint32_t)ok << v;
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[v] = (vis >> v) & 1u ? acc[v] : -INFINITY;
+      } else if (tb + 32 > n1 || tb + 32 > h.n_shared) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int n = tb + 8 * (v >> 2) + 4 * hh + (v & 3);
+          bool ok = n < n1;
+          if (ok && n >= h.n_shared) ok = (maskp[n] >> beam_bit[rbk]) & 1ull;
+          if (!ok) acc[v] = -INFINITY;
+        }
       }
+      float tmax = acc[0];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[v] = (vis >> v) & 1u ? acc[v] : -INFINITY;
-    } else if (tb + 32 > n1 || tb + 32 > h.n_shared) {
+      for (int v = 1; v < 16; ++v) tmax = fmaxf(tmax, acc[v]);
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+      // running max in the scaled log2 domain; p = 2^(scale * s - m) in one FMA + v_exp
+      // (arguments are <= 0 or -inf: the bare v_exp_f32, results below 2^-126 flush to 0)
+      const float mn = fmaxf(m[rbk], tmax * scale);
+      const float alpha = __builtin_amdgcn_exp2f(m[rbk] - mn);
+      m[rbk] = mn;
+      bf16x8 pb[2];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int n = tb + 8 * (v >> 2) + 4 * hh + (v & 3);
-        bool ok = n < n1;
-        if (ok && n >= h.n_shared) ok = (maskp[n] >> beam_bit) & 1ull;
-        if (!ok) acc[v] = -INFINITY;
+      for (int v = 0; v < 16; ++v) pb[v >> 3][v & 7] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(acc[v], scale, -mn));
+      // row sum of the rounded weights (the ones PV uses), two bf16 per dot2
+      float ps = 0.0f;
+      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+      for (int v = 0; v < 16; v += 2) {
+        const bf16x2 pair = {pb[v >> 3][v & 7], pb[v >> 3][(v & 7) + 1]};
+        ps = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, ps, false);
       }
+      lsum[rbk] = lsum[rbk] * alpha + ps;
+      if (__any(alpha != 1.0f)) {
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) o[rbk][dt][v] *= alpha;
+      }
+      // O^T += V^T P^T; P's register order (nodes 16uu + 8(j/4) + 4hh + j%4) matches va
+#pragma unroll
+      for (int uu = 0; uu < 2; ++uu)
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt)
+          o[rbk][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[uu][dt], pb[uu], o[rbk][dt], 0, 0, 0);
     }
-    float tmax = acc[0];
-#pragma unroll
-    for (int v = 1; v < 16; ++v) tmax = fmaxf(tmax, acc[v]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-    // running max in the scaled log2 domain; p = 2^(scale * s - m) in one FMA + v_exp
-    // (arguments are <= 0 or -inf: the bare v_exp_f32, results below 2^-126 flush to 0)
-    const float mn = fmaxf(m, tmax * scale);
-    const float alpha = __builtin_amdgcn_exp2f(m - mn);
-    m = mn;
-    bf16x8 pb[2];
-#pragma unroll
-    for (int v = 0; v < 16; ++v) pb[v >> 3][v & 7] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(acc[v], scale, -mn));
-    // row sum of the rounded weights (the ones PV uses), two bf16 per dot2
-    float ps = 0.0f;
-    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-#pragma unroll
-    for (int v = 0; v < 16; v += 2) {
-      const bf16x2 pair = {pb[v >> 3][v & 7], pb[v >> 3][(v & 7) + 1]};
-      ps = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, ps, false);
-    }
-    lsum = lsum * alpha + ps;
-    if (__any(alpha != 1.0f)) {
-#pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) o[dt][v] *= alpha;
-    }
-    // O^T += V^T P^T; P's register order (nodes 16uu + 8(j/4) + 4hh + j%4) matches va
-#pragma unroll
-    for (int uu = 0; uu < 2; ++uu)
-#pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt)
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[uu][dt], pb[uu], o[dt], 0, 0, 0);
   }
 
   // ---- merge the waves of this WG: every wave stores its state, one combine ----
-  lsum += __shfl_xor(lsum, 32);
+#pragma unroll
+  for (int k = 0; k < RB; ++k) lsum[k] += __shfl_xor(lsum[k], 32);
   __builtin_amdgcn_s_waitcnt(kWaitVmAll);  // (staged moved rows of a wave without tiles)
   __syncthreads();  // the tile buffers are reused below; every read of the pool is done
   if (leaves_staged) {
@@ -422,75 +481,81 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
       *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(mstage + q * 16);
     }
   }
-  float* obuf = reinterpret_cast<float*>(lds);  // [NW][kRows][OS] unscaled O of each wave
-  float* smx = obuf + NW * kRows * C::OS;        // [NW][kRows] running max
-  float* ssum = smx + NW * kRows;                // [NW][kRows] weight sum
-  float* fw = ssum + NW * kRows;                 // [NW][kRows] wave weight 2^(m_w - M)
-  float* rowm = fw + NW * kRows;                 // [kRows] M
-  float* rowl = rowm + kRows;                    // [kRows] sum of weights
-  if (hh == 0) {
-    smx[wave * kRows + col] = m;
-    ssum[wave * kRows + col] = lsum;
-  }
-  {
-    float* ow = obuf + (wave * kRows + col) * C::OS;
+  // one pass per row block (the merge buffers take one block's rows at a time)
 #pragma unroll
-    for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) ow[dt * 32 + 8 * (v >> 2) + 4 * hh + (v & 3)] = o[dt][v];
-  }
-  __syncthreads();
-  if (threadIdx.x < kRows) {
-    const int i = threadIdx.x;
-    float Mi = smx[i];
-    for (int w = 1; w < NW; ++w) Mi = fmaxf(Mi, smx[w * kRows + i]);
-    float L = 0.0f;
-    for (int w = 0; w < NW; ++w) {
-      const float f = __builtin_amdgcn_exp2f(smx[w * kRows + i] - Mi);
-      fw[w * kRows + i] = f;
-      L += ssum[w * kRows + i] * f;  // fixed wave order
+  for (int rbk = 0; rbk < RB; ++rbk) {
+    if (rbk > 0) __syncthreads();  // the previous pass has read the buffers
+    float* obuf = reinterpret_cast<float*>(lds);  // [NW][kRows][OS] unscaled O of each wave
+    float* smx = obuf + NW * kRows * C::OS;        // [NW][kRows] running max
+    float* ssum = smx + NW * kRows;                // [NW][kRows] weight sum
+    float* fw = ssum + NW * kRows;                 // [NW][kRows] wave weight 2^(m_w - M)
+    float* rowm = fw + NW * kRows;                 // [kRows] M
+    float* rowl = rowm + kRows;                    // [kRows] sum of weights
+    if (hh == 0) {
+      smx[wave * kRows + col] = m[rbk];
+      ssum[wave * kRows + col] = lsum[rbk];
     }
-    rowm[i] = Mi;
-    rowl[i] = L;
-  }
-  __syncthreads();
-
-  // 8 consecutive output elements per thread: 16-byte LDS reads, one 16-byte store
-  __bf16* outp = static_cast<__bf16*>(a.out);
-  const int unit = u.unit;
-  float* part = s.attn_part + (size_t)unit * a.splits * kRows * (D + 2);
-  for (int idx = threadIdx.x; idx < kRows * (D / 8); idx += NW * 64) {
-    const int i = idx / (D / 8), c = idx % (D / 8) * 8;
-    float O[8];
+    {
+      float* ow = obuf + (wave * kRows + col) * C::OS;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) O[e] = 0.0f;
+      for (int dt = 0; dt < C::DT; ++dt)
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const float f = fw[w * kRows + i];
-      const float4* src = reinterpret_cast<const float4*>(obuf + (w * kRows + i) * C::OS + c);
-      const float4 x0 = src[0], x1 = src[1];
-      O[0] += x0.x * f; O[1] += x0.y * f; O[2] += x0.z * f; O[3] += x0.w * f;
-      O[4] += x1.x * f; O[5] += x1.y * f; O[6] += x1.z * f; O[7] += x1.w * f;
+        for (int v = 0; v < 16; ++v) ow[dt * 32 + 8 * (v >> 2) + 4 * hh + (v & 3)] = o[rbk][dt][v];
     }
-    const float Mi = rowm[i], L = rowl[i];
-    if (a.splits == 1) {
-      const int rr = u.rb * kRows + i;
-      if (rr < nrows * G) {
-        const int bm = rr / G;
-        const bool live = (TREE || bm < n_live) && L > 0.0f;
-        const float inv = live ? 1.0f / L : 0.0f;
-        bf16x8 y;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) y[e] = (__bf16)(O[e] * inv);
-        *reinterpret_cast<bf16x8*>(outp + ((((size_t)u.li * s.T + u.t) * nrows + bm) * s.Hq + u.g * G + rr % G) * D + c) = y;
+    __syncthreads();
+    if (threadIdx.x < kRows) {
+      const int i = threadIdx.x;
+      float Mi = smx[i];
+      for (int w = 1; w < NW; ++w) Mi = fmaxf(Mi, smx[w * kRows + i]);
+      float L = 0.0f;
+      for (int w = 0; w < NW; ++w) {
+        const float f = __builtin_amdgcn_exp2f(smx[w * kRows + i] - Mi);
+        fw[w * kRows + i] = f;
+        L += ssum[w * kRows + i] * f;  // fixed wave order
       }
-    } else {
-      float* pp = part + ((size_t)u.split * kRows + i) * (D + 2);
+      rowm[i] = Mi;
+      rowl[i] = L;
+    }
+    __syncthreads();
+
+    // 8 consecutive output elements per thread: 16-byte LDS reads, one 16-byte store
+    __bf16* outp = static_cast<__bf16*>(a.out);
+    // (partials are numbered by 32-row block: the combine's units)
+    const int unit = RB == 1 ? u.unit : (u.unit / a.row_blocks) * a.row_blocks32 + u.rb * RB + rbk;
+    float* part = s.attn_part + (size_t)unit * a.splits * kRows * (D + 2);
+    for (int idx = threadIdx.x; idx < kRows * (D / 8); idx += NW * 64) {
+      const int i = idx / (D / 8), c = idx % (D / 8) * 8;
+      float O[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pp[c + e] = O[e];
-      if (c == 0) {
-        pp[D] = Mi;
-        pp[D + 1] = L;
+      for (int e = 0; e < 8; ++e) O[e] = 0.0f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const float f = fw[w * kRows + i];
+        const float4* src = reinterpret_cast<const float4*>(obuf + (w * kRows + i) * C::OS + c);
+        const float4 x0 = src[0], x1 = src[1];
+        O[0] += x0.x * f; O[1] += x0.y * f; O[2] += x0.z * f; O[3] += x0.w * f;
+        O[4] += x1.x * f; O[5] += x1.y * f; O[6] += x1.z * f; O[7] += x1.w * f;
+      }
+      const float Mi = rowm[i], L = rowl[i];
+      if (a.splits == 1) {
+        const int rr = (u.rb * RB + rbk) * kRows + i;
+        if (rr < nrows * G) {
+          const int bm = rr / G;
+          const bool live = (TREE || bm < n_live) && L > 0.0f;
+          const float inv = live ? 1.0f / L : 0.0f;
+          bf16x8 y;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) y[e] = (__bf16)(O[e] * inv);
+          *reinterpret_cast<bf16x8*>(outp + ((((size_t)u.li * s.T + u.t) * nrows + bm) * s.Hq + u.g * G + rr % G) * D + c) = y;
+        }
+      } else {
+        float* pp = part + ((size_t)u.split * kRows + i) * (D + 2);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pp[c + e] = O[e];
+        if (c == 0) {
+          pp[D] = Mi;
+          pp[D + 1] = L;
+        }
       }
     }
   }
@@ -524,10 +589,17 @@ hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st
                             hipEvent_t ev1) {
   // (4-wave WGs, two per CU, measured slower than 8-wave WGs one per CU on every shape
   // here, also for launches of several WG rounds)
+  // (32-row blocks: row_blocks32 = row_blocks WGs of rb_per_wg blocks each, the last
+  // possibly half used)
+  if (a.rb_per_wg < 1 || a.rb_per_wg > 2 || (a.rb_per_wg == 2 && a.tree) ||
+      a.row_blocks32 > a.row_blocks * a.rb_per_wg || a.row_blocks32 <= (a.row_blocks - 1) * a.rb_per_wg)
+    return hipErrorInvalidValue;
   const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * a.splits), block(kNW * 64);
-#define LAUNCH_MFMA(DD)                                                                              \
-  (a.tree ? hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW, true>), grid, block, 0, st, ev0, ev1, 0, s, a) \
-          : hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW, false>), grid, block, 0, st, ev0, ev1, 0, s, a))
+#define LAUNCH_MFMA(DD)                                                                                    \
+  (a.tree ? hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW, true, 1>), grid, block, 0, st, ev0, ev1, 0, s, a)    \
+   : a.rb_per_wg == 2                                                                                        \
+       ? hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW, false, 2>), grid, block, 0, st, ev0, ev1, 0, s, a)     \
+       : hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW, false, 1>), grid, block, 0, st, ev0, ev1, 0, s, a))
   switch (s.D) {
     case 64: LAUNCH_MFMA(64); break;
     case 96: LAUNCH_MFMA(96); break;

@@ -248,6 +248,7 @@ td_status batch_beam_attn_decode(bbs_ctx* c, int32_t layer_begin, int32_t n_laye
   a.moves = 0;
   const int rpb = mfma ? td::attn_mfma_rows_per_block() : td::attn_valu_rows_per_block();
   a.row_blocks = (s.Hq / s.Hkv + rpb - 1) / rpb;
+  a.row_blocks32 = a.row_blocks;
   a.splits = td::attn_choose_splits(s, n_layers, a.row_blocks);
   const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;

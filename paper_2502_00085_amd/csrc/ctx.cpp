@@ -243,8 +243,13 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   a.kv_pending = c->pending ? 1 : 0;
   const int rpb = mfma ? td::attn_mfma_rows_per_block() : td::attn_valu_rows_per_block();
   a.row_blocks = (s.b * (s.Hq / s.Hkv) + rpb - 1) / rpb;
+  a.row_blocks32 = a.row_blocks;
+  if (mfma && a.row_blocks == 2) {  // b G in (32, 64]: one WG over both row blocks
+    a.rb_per_wg = 2;
+    a.row_blocks = 1;
+  }
   a.splits = c->splits_override > 0 ? c->splits_override : td::attn_choose_splits(s, n_layers, a.row_blocks);
-  const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
+  const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks32;  // (partials per 32-row block)
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;
   a.xcd_group = a.row_blocks > 1 && ((long)s.T * n_layers * s.Hkv * a.splits) % 8 == 0 ? 1 : 0;
   hipEvent_t ev0 = c->ev[TD_PHASE_ATTN][0], ev1 = c->ev[TD_PHASE_ATTN][1];
@@ -284,7 +289,11 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
     if (e == hipSuccess) e = hipEventRecord(mv1, st);
   }
   if (e == hipSuccess) e = mfma ? td::launch_attn_mfma(s, a, st, ev0, main_ev1) : td::launch_attn_valu(s, a, st, ev0, main_ev1);
-  if (e == hipSuccess && a.splits > 1) e = td::launch_attn_combine(s, a, rpb, st, nullptr, ev1);
+  if (e == hipSuccess && a.splits > 1) {
+    td::AttnArgs ac = a;  // the combine runs per 32-row block
+    ac.row_blocks = a.row_blocks32;
+    e = td::launch_attn_combine(s, ac, rpb, st, nullptr, ev1);
+  }
   if (e != hipSuccess) return hip_fail(c, e, "trie_attn_decode launch");
   if (c->pending) {
     for (int l = layer_begin; l < layer_begin + n_layers; ++l) c->layer_written[l] = 1;
@@ -334,6 +343,7 @@ td_status trie_tree_attn(td_ctx* c, int32_t layer_begin, int32_t n_layers, int32
   }
   const int rpb = td::attn_mfma_rows_per_block();
   a.row_blocks = (q_max * (s.Hq / s.Hkv) + rpb - 1) / rpb;
+  a.row_blocks32 = a.row_blocks;
   a.splits = c->splits_override > 0 ? c->splits_override : td::attn_choose_splits(s, n_layers, a.row_blocks);
   const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;

@@ -103,6 +103,9 @@ struct AttnArgs {
   int tree = 0;                    // 1: multi-query tree attention (rows = query nodes)
   const int32_t* qslots = nullptr; // (tree) [T][qmax] logical slots of the queries, -1 = none
   int qmax = 0;                    // (tree) query nodes per trie in q / out
+  int rb_per_wg = 1;               // (matrix-core decode) 32-row blocks per WG: 1 or 2
+  int row_blocks32 = 0;            // 32-row blocks per unit (partials and the combine); the
+                                   // grid's row_blocks counts WGs, of rb_per_wg blocks each
 };
 
 hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const int32_t* d_tokens,

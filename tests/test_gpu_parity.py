@@ -203,3 +203,24 @@ def test_closed_forms_on_gpu(form):
                 err = np.max(np.abs(o[:, i, h] - ref))
                 assert err <= 2e-2 and err <= 1e-2 * np.max(np.abs(ref)) + 1e-6, err
     r.dec.close()
+
+
+# b G = 64 query rows per KV head: one WG takes both 32-row blocks on the matrix-core
+# kernel (each wave's tile serves 64 rows; the query rows sit in LDS)
+@pytest.mark.parametrize("d", [64, 96, 128])
+def test_two_row_blocks_per_workgroup(d):
+    run_case(small(n_layers=2, n_q_heads=8, n_kv_heads=2, head_dim=d, beam_width=16, prompt_min=60,
+                   prompt_max=60, vocab=700, alpha=0.5, qkv_std=1.0 / np.sqrt(d), steps=7), seed=30 + d,
+             impl=B.TD_ATTN_MFMA)
+
+
+def test_two_row_blocks_window_deferred_collection():
+    run_case(small(n_layers=1, n_q_heads=16, n_kv_heads=4, beam_width=16, prompt_min=50, prompt_max=50,
+                   vocab=600, window=24, gc_interval=3, alpha=0.3, steps=14), seed=41)
+
+
+def test_two_row_blocks_several_tries_without_splits():
+    # 4 tries x 4 layers x 16 KV heads = 256 units: one WG per (trie, layer, head), so the
+    # moved rows are staged by the attention kernel itself
+    run_case(small(n_tries=4, n_layers=4, n_q_heads=64, n_kv_heads=16, head_dim=64, beam_width=16,
+                   prompt_min=20, prompt_max=70, vocab=500, alpha=0.0, steps=6), seed=42)
