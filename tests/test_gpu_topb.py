@@ -131,3 +131,14 @@ def test_register_batch_boundary_llama_vocab(b):
     scores = -np.sort(g.uniform(0, 2, b)).astype(np.float32)
     pairs = (g.integers(0, b, b), g.integers(0, V, b))
     run_topb(b, logits, scores, pairs)
+
+
+@pytest.mark.parametrize("b", [33, 64])
+def test_entries_beyond_the_register_batch(b):
+    """b * chunks = 1,056 and 2,048 entries per wave at V = 128,256 (2,048 is the documented
+    maximum): the merge holds 1,024 in registers and reads the rest again."""
+    g = np.random.default_rng(40 + b)
+    V = 128256
+    logits = g.normal(0, 3, (b, V)).astype(np.float32)
+    scores = -np.sort(g.uniform(0, 2, b)).astype(np.float32)
+    run_topb(b, logits, scores)
