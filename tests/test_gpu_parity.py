@@ -224,3 +224,9 @@ def test_two_row_blocks_several_tries_without_splits():
     # moved rows are staged by the attention kernel itself
     run_case(small(n_tries=4, n_layers=4, n_q_heads=64, n_kv_heads=16, head_dim=64, beam_width=16,
                    prompt_min=20, prompt_max=70, vocab=500, alpha=0.0, steps=6), seed=42)
+
+
+@pytest.mark.parametrize("mode", ["driven", "scripted"])
+def test_smallest_vocabulary(mode):
+    # V = b: at step 1 every candidate is selected; afterwards b of b * b
+    run_case(small(n_layers=1, beam_width=4, vocab=4, steps=6), seed=50, mode=mode)
