@@ -123,6 +123,23 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     n1 = min(N, n0 + per);
   }
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
+  // (two row blocks: every wave waits for the query rows at a barrier, so wave 0 loads them
+  // first; one row block loads its own after issuing its first tile, measured faster)
+  bf16x8 qv[RB][C::KSTEPS];
+  if constexpr (RB == 2) {
+    if (wave == 0) {
+#pragma unroll
+      for (int k = 0; k < RB; ++k) {
+        const int rk = r + k * kRows, ok_ = rk < s.b * G && rk / G < n_live;
+        const uint4* qp = reinterpret_cast<const uint4*>(
+            static_cast<const __bf16*>(a.q) +
+            ((((size_t)u.li * s.T + u.t) * nrows + (ok_ ? rk / G : 0)) * s.Hq + u.g * G + rk % G) * D +
+            hh * (D / 2));
+#pragma unroll
+        for (int t = 0; t < C::KSTEPS; ++t) qv[k][t] = __builtin_bit_cast(bf16x8, ok_ ? qp[t] : make_uint4(0, 0, 0, 0));
+      }
+    }
+  }
   // Rows moved by the last compaction (this WG is the only one of its layer and head):
   // their destinations are the consecutive slots first_moved, first_moved + 1, ...  This
   // call reads them at their sources (still intact) and writes them to their destinations
@@ -298,7 +315,6 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   // this lane's query row of each row block (B operand of S^T): half hh of its d range
   int beam_bit[RB];
   bool rok[RB];
-  bf16x8 qv[RB][C::KSTEPS];
   unsigned char* qlds = lds + C::MOVE0;  // (two row blocks) [64 rows][D], chunks rotated by row
 #pragma unroll
   for (int k = 0; k < RB; ++k) {
@@ -312,8 +328,10 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
           hh * (D / 2));
 #pragma unroll
       for (int t = 0; t < C::KSTEPS; ++t) {
-        const uint4 x = ok_ ? qp[t] : make_uint4(0, 0, 0, 0);
-        qv[k][t] = __builtin_bit_cast(bf16x8, x);
+        if (RB == 1) {
+          const uint4 x = ok_ ? qp[t] : make_uint4(0, 0, 0, 0);
+          qv[k][t] = __builtin_bit_cast(bf16x8, x);
+        }
         if (RB == 2) {
           const int row = k * kRows + col;
           *reinterpret_cast<bf16x8*>(qlds + row * (2 * D) + (hh * (C::CPR / 2) + t + row) % C::CPR * 16) = qv[k][t];
