@@ -39,8 +39,8 @@ HBM_PEAK_GBS = 8000.0
 # kernel sources it was measured on: reported as null once their digest differs.
 ATTN_TRAFFIC = {
     "workload": "llama8b",
-    "sources_sha256": "655c57d6d9a15b70ff3f9dea053bf147a38d7fc73f43fc8092848536d62d4047",
-    "bytes_per_launch": 283736636,             # 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE
+    "sources_sha256": "32fb292f7befb27a87eb3b009d9d1020ba232f164516933529ce9e2f41383015",
+    "bytes_per_launch": 283743804,             # 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE
     "algorithmic_bytes_per_launch": 283377664,  # unique K+V rows, q, out
 }
 ATTN_SOURCES = ("attn_mfma.hip", "attn_common.h", "td_internal.h")
