@@ -36,22 +36,31 @@ HBM_PEAK_GBS = 8000.0
 # --copy-ref-mib 512`, llama8b), scaled by what the same counters read for a plain 512 MiB
 # device copy (fetch x 2.0, write x 1.0), per launch for the 64 graph-replayed launches at
 # the step-K/2 trie: the launches `roofline.achieved` is timed on.  Valid only for the
-# kernel sources it was measured on: reported as null once their digest differs.
+# kernel sources it was measured on: reported as null once their digest (comments
+# stripped) differs.
 ATTN_TRAFFIC = {
     "workload": "llama8b",
-    "sources_sha256": "32fb292f7befb27a87eb3b009d9d1020ba232f164516933529ce9e2f41383015",
+    "sources_sha256": "09aa57105a6a520fc0223222b71c87f2a896f5893d3085cca6a631a329bc5264",
     "bytes_per_launch": 283743804,             # 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE
     "algorithmic_bytes_per_launch": 283377664,  # unique K+V rows, q, out
 }
 ATTN_SOURCES = ("attn_mfma.hip", "attn_common.h", "td_internal.h")
 
 
+def strip_comments(src: str) -> str:
+    """C++ source without its comments and blank lines (the digest follows the code only)."""
+    import re
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    return "\n".join(ln.rstrip() for ln in src.splitlines() if ln.strip())
+
+
 def attn_sources_digest() -> str:
     import hashlib
     h = hashlib.sha256()
     for f in ATTN_SOURCES:
-        with open(os.path.join(ROOT, "paper_2502_00085_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2502_00085_amd", "csrc", f), encoding="utf-8") as fh:
+            h.update(strip_comments(fh.read()).encode())
     return h.hexdigest()
 
 

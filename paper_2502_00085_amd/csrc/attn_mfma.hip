@@ -22,8 +22,10 @@
 // The S^T layout puts one query row per lane, so the online softmax needs one cross-lane
 // step (the two half-waves) per tile.  Tiles inside the shared prefix (every beam's
 // path) skip the mask; other tiles test the row's beam bit per node.  A sliding window is
-// a range start found by binary search on depth.  Waves of a WG and node splits over WGs
-// are merged with max/sum rescaling; the last split WG to finish merges the splits.
+// a range start found by a block-parallel search on depth.  The waves of a WG are merged
+// with max/sum rescaling through LDS; node splits over WGs write partials that a second
+// launch merges (attn_combine.hip).  Template variants: TREE (rows are arbitrary query
+// nodes) and RB = 2 (one WG over two 32-row blocks).
 #include "attn_common.h"
 #include "mfma_tile.h"
 
