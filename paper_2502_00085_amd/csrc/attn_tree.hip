@@ -33,6 +33,7 @@ constexpr int kTreeWaves = 4;  // (two WGs per CU: their barriers do not wait on
 constexpr int kTreeThreads = kTreeWaves * 64;
 constexpr int kTreeRows = kTreeWaves * 32;  // query rows per WG
 constexpr float kTreeNegBig = -1.0e30f;
+constexpr float kTreeSlack = 8.0f;  // largest probability 2^8 before a row's shift moves
 
 template <int D>
 struct TreeCfg {
@@ -246,10 +247,22 @@ __global__ __launch_bounds__(kTreeThreads, 2) void k_attn_tree(DevState s, AttnA
       float tmax = acc[0];
 #pragma unroll
       for (int v = 1; v < 16; ++v) tmax = fmaxf(tmax, acc[v]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-      const float mn = fmaxf(m, tmax * scale);
-      const float alpha = __builtin_amdgcn_exp2f(m - mn);
-      m = mn;
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32)) * scale;
+      // The row's shift m moves up only when a score exceeds it by more than kTreeSlack
+      // (log2 units): the probabilities stay <= 2^kTreeSlack, and O and l are rescaled on
+      // few tiles instead of on nearly every one (softmax does not depend on the shift).
+      const bool raise = tmax > m + kTreeSlack;
+      float alpha = 1.0f;
+      if (__any(raise)) {
+        const float mn = raise ? tmax : m;
+        alpha = __builtin_amdgcn_exp2f(m - mn);
+        m = mn;
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) o[dt][v] *= alpha;
+      }
+      const float mn = m;
       bf16x8 pb[2];
 #pragma unroll
       for (int v = 0; v < 16; ++v) pb[v >> 3][v & 7] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(acc[v], scale, -mn));
@@ -261,12 +274,6 @@ __global__ __launch_bounds__(kTreeThreads, 2) void k_attn_tree(DevState s, AttnA
         ps = __builtin_amdgcn_fdot2_f32_bf16(pair, ones, ps, false);
       }
       lsum = lsum * alpha + ps;
-      if (__any(alpha != 1.0f)) {
-#pragma unroll
-        for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) o[dt][v] *= alpha;
-      }
 #pragma unroll
       for (int uu = 0; uu < 2; ++uu)
 #pragma unroll
