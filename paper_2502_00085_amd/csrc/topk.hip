@@ -136,8 +136,8 @@ __device__ inline void wave_append(const T1* val, const T2* val2, const bool* ta
 // Writes the b largest of the distinct keys cand[0..n) to out[0..b) in order, with their
 // companions (0 where there are fewer than b keys).  Wave 0 alone ranks up to 64 keys held
 // in registers (and only wave 0 has written out when this returns); more keys are ranked
-// by the whole block by counting (out complete after the caller's next barrier).  Call
-// from uniform control flow.
+// by the whole block (kFinalThreads threads) by counting (out complete after the
+// caller's next barrier).  Call from uniform control flow.
 __device__ inline void rank_topb(const uint64_t* cand, const uint64_t* comp, int n, int b, uint64_t* out,
                                  uint64_t* out_comp) {
   if (n <= 64) {
@@ -158,9 +158,9 @@ __device__ inline void rank_topb(const uint64_t* cand, const uint64_t* comp, int
     }
     return;
   }
-  for (int j = threadIdx.x; j < b; j += blockDim.x) out[j] = out_comp[j] = 0;
+  for (int j = threadIdx.x; j < b; j += kFinalThreads) out[j] = out_comp[j] = 0;
   __syncthreads();
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+  for (int i = threadIdx.x; i < n; i += kFinalThreads) {
     const uint64_t k = cand[i];
     int rank = 0;
     for (int j = 0; j < n; ++j) rank += cand[j] > k;
