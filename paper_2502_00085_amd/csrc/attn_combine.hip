@@ -26,9 +26,9 @@ __device__ inline void store8(__bf16* p, const float* v) {
 }
 
 // Grid: (trie, layer, KV head, row block) units x parts; each thread one (row, 8-element
-// chunk of d).  The splits' maxima, then their sums and 8-element O chunks, are loaded
-// with the loop unrolled so that the loads of several splits are in flight together (the
-// merge is a few dependent memory rounds, not one per split).
+// chunk of d).  The splits are taken in groups of 8: every load of a group (maxima, sums
+// and 8-element O chunks) is issued before any is used, so a merge of up to 8 splits is
+// one memory round; groups are merged with a running max.
 template <typename T>
 __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(DevState s, AttnArgs a, int R, int parts) {
   const int unit = blockIdx.x / parts;  // ((t * nl + li) * Hkv + g) * row_blocks + rb
@@ -51,24 +51,40 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(DevState s, At
   const int n_live = s.hdr[t].n_live;
   const size_t stride = (size_t)R * (D + 2);  // one split's records
   const float* rec = s.attn_part + (size_t)unit * a.splits * stride + (size_t)i * (D + 2);
-  float M = -1.0e30f;
-#pragma unroll 8
-  for (int sp = 0; sp < a.splits; ++sp) M = fmaxf(M, rec[sp * stride + D]);
-  float L = 0.0f, O[8];
+  float M = -1.0e30f, L = 0.0f, O[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) O[e] = 0.0f;
-#pragma unroll 8
-  for (int sp = 0; sp < a.splits; ++sp) {
-    const float* pp = rec + sp * stride;
-    const float f = exp2f(pp[D] - M);
-    L += pp[D + 1] * f;
-    // (records are D + 2 floats: 8-byte aligned)
+  for (int s0 = 0; s0 < a.splits; s0 += 8) {
+    float mv[8], lv[8];
+    float2 ov[8][4];
 #pragma unroll
-    for (int e = 0; e < 8; e += 2) {
-      const float2 v = *reinterpret_cast<const float2*>(pp + c + e);
-      O[e] += v.x * f;
-      O[e + 1] += v.y * f;
+    for (int k = 0; k < 8; ++k) {
+      // (a split past the last reads the group's first again; its weight is zero)
+      const float* pp = rec + (size_t)(s0 + k < a.splits ? s0 + k : s0) * stride;
+      mv[k] = pp[D];
+      lv[k] = pp[D + 1];
+      // (records are D + 2 floats: 8-byte aligned)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ov[k][e] = *reinterpret_cast<const float2*>(pp + c + 2 * e);
     }
+    float Mg = M;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) Mg = s0 + k < a.splits ? fmaxf(Mg, mv[k]) : Mg;
+    const float fo = exp2f(M - Mg);
+    L *= fo;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) O[e] *= fo;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float f = s0 + k < a.splits ? exp2f(mv[k] - Mg) : 0.0f;
+      L += lv[k] * f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        O[2 * e] += ov[k][e].x * f;
+        O[2 * e + 1] += ov[k][e].y * f;
+      }
+    }
+    M = Mg;
   }
   const int bm = rr / G;
   const float inv = ((a.tree || bm < n_live) && L > 0.0f) ? 1.0f / L : 0.0f;

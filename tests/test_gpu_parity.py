@@ -34,6 +34,13 @@ def run_case(w, seed=0, mode="scripted", impl=B.TD_ATTN_AUTO, steps=None, capaci
     r.dec.close()
 
 
+def test_more_splits_than_one_merge_group(monkeypatch):
+    """12 node splits per unit (a TD_ATTN_SPLITS override): the split merge takes a group
+    of 8 and a group of 4 with a running max, and some splits hold no node."""
+    monkeypatch.setenv("TD_ATTN_SPLITS", "12")
+    run_case(small(steps=6), seed=31)
+
+
 @pytest.mark.parametrize("mode", ["driven", "scripted"])
 def test_tiny_fp32_all_steps(mode):
     run_case(synth.WORKLOADS["tiny"], seed=0, mode=mode)
