@@ -121,7 +121,11 @@ typedef struct {
 
 /* Create a context: validates desc, allocates trie metadata and workspace on the
  * current device (synchronous).  Tries start empty; call td_init_prompt or
- * td_load_state before decoding. */
+ * td_load_state before decoding.  Tuning, read here from the environment:
+ * TD_ATTN_SPLITS = n (1..64) fixes the number of WGs that split one (trie, layer, KV
+ * head) unit's nodes in the decode attention, instead of the built-in choice (which
+ * splits only when there are too few units to fill the chip); a choice whose partials
+ * would not fit the workspace falls back to no split. */
 td_status td_create(const td_desc* desc, td_ctx** out);
 td_status td_destroy(td_ctx* ctx);
 
