@@ -42,11 +42,14 @@ class Run:
 
     def __init__(self, w, seed=0, layers=None, attn_impl=0, capacity=None, mode="scripted",
                  oracle=True, phase_events=False, eos=-1, eos_boost=0.0, length_penalty=1.0,
-                 early_stopping=False, fused=False):
+                 early_stopping=False, fused=False, layer_calls=None):
         import torch
         import paper_2502_00085_amd.binding as B
         self.w, self.seed, self.mode, self.phase_events = w, seed, mode, phase_events
         self.fused = fused  # beam_topk_append instead of beam_logsoftmax_topk + trie_append_prune
+        # attention as several trie_attn_decode calls over layer ranges [c[i], c[i+1]) (as a
+        # model calls it), instead of one call over every layer
+        self.layer_calls = layer_calls
         self.eos, self.eos_boost = eos, eos_boost
         self.layers = list(range(w.n_layers)) if layers is None else list(layers)
         self.cap = capacity or w.capacity
@@ -96,7 +99,14 @@ class Run:
             evs = [B.KernelEvents() for _ in range(4)]
             for ph, e in enumerate(evs):
                 B.td_set_kernel_events(dec.ctx, ph, e.start, e.stop)
-        dec.attn_decode(0, w.n_layers, qd, knd, vnd, out, self.scale)
+        if self.layer_calls:
+            c = list(self.layer_calls)
+            assert c[0] == 0 and c[-1] == w.n_layers and all(x < y for x, y in zip(c, c[1:]))
+            for l0, l1 in zip(c[:-1], c[1:]):
+                dec.attn_decode(l0, l1 - l0, qd[l0:l1], None if knd is None else knd[l0:l1],
+                                None if vnd is None else vnd[l0:l1], out[l0:l1], self.scale)
+        else:
+            dec.attn_decode(0, w.n_layers, qd, knd, vnd, out, self.scale)
         ld = torch.from_numpy(np.ascontiguousarray(logits)).cuda()
         i32 = dict(dtype=torch.int32, device="cuda")
         f32 = dict(dtype=torch.float32, device="cuda")

@@ -34,6 +34,38 @@ def run_case(w, seed=0, mode="scripted", impl=B.TD_ATTN_AUTO, steps=None, capaci
     r.dec.close()
 
 
+def layer_case(w, seed, calls, mode="scripted", fused=False, steps=None, capacity=None):
+    log(f"layer calls {calls}: {w.name} L={w.n_layers} b={w.beam_width} W={w.window} g={w.gc_interval} "
+        f"mode={mode} fused={fused} seed={seed}")
+    r = Run(w, seed, mode=mode, fused=fused, layer_calls=calls, capacity=capacity)
+    for _ in range(steps or w.steps):
+        errs, _ = r.step()
+        assert not errs, "\n".join(errs[:10])
+    assert r.dec.status() == B.TD_OK
+    r.dec.close()
+
+
+@pytest.mark.parametrize("mode", ["driven", "scripted"])
+def test_one_layer_calls(mode):
+    """Attention as one call per layer (a model's order): each call stores its layers' leaf
+    rows and copies their moved rows, and a one-layer call splits the nodes over WGs whose
+    partials the merge launch combines."""
+    layer_case(small(n_layers=4), seed=41, calls=[0, 1, 2, 3, 4], mode=mode)
+
+
+def test_uneven_layer_ranges_with_window_and_deferred_collection():
+    layer_case(small(n_layers=5, window=30, gc_interval=3, steps=14), seed=42, calls=[0, 2, 3, 5])
+
+
+def test_one_layer_calls_fused_selection():
+    layer_case(small(n_layers=3, beam_width=4, steps=8), seed=43, calls=[0, 1, 2, 3], fused=True)
+
+
+def test_one_layer_calls_two_row_blocks():
+    # b * G = 64 rows per KV head: the two-row-block WG, with node splits per one-layer call
+    layer_case(small(n_layers=2, beam_width=16, n_q_heads=16, n_kv_heads=4, steps=6), seed=44, calls=[0, 1, 2])
+
+
 def test_more_splits_than_one_merge_group(monkeypatch):
     """12 node splits per unit (a TD_ATTN_SPLITS override): the split merge takes a group
     of 8 and a group of 4 with a running max, and some splits hold no node."""
