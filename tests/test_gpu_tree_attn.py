@@ -25,7 +25,7 @@ def small(**kw):
     return synth.Workload(**base)
 
 
-def run_tree(w, seed, pick, capacity=None):
+def run_tree(w, seed, pick, capacity=None, layer_calls=None):
     log(f"tree case T={w.n_tries} L={w.n_layers} Hq={w.n_q_heads} Hkv={w.n_kv_heads} d={w.head_dim} "
         f"P={w.prompt_min}-{w.prompt_max} b={w.beam_width} W={w.window} g={w.gc_interval} steps={w.steps} "
         f"seed={seed}")
@@ -52,7 +52,14 @@ def run_tree(w, seed, pick, capacity=None):
                                                   dtype=np.float32))
     qd = to_dev(w, qt)
     ot = torch.full_like(qd, 5.0)
-    r.dec.tree_attn(0, w.n_layers, torch.from_numpy(qs).cuda(), qd, ot, r.scale)
+    qsd = torch.from_numpy(qs).cuda()
+    if layer_calls:  # one call per layer range [c[i], c[i+1])
+        c = list(layer_calls)
+        assert c[0] == 0 and c[-1] == w.n_layers
+        for l0, l1 in zip(c[:-1], c[1:]):
+            r.dec.tree_attn(l0, l1 - l0, qsd, qd[l0:l1], ot[l0:l1], r.scale)
+    else:
+        r.dec.tree_attn(0, w.n_layers, qsd, qd, ot, r.scale)
     torch.cuda.synchronize()
     got = from_dev(ot)
     qf = synth.as_f32(w, qt)
@@ -159,6 +166,18 @@ def test_prefill_d64_g2_tight_window():
 
 def test_prefill_window_deferred_collection_random_order():
     run_tree(small(window=45, gc_interval=4, steps=14), seed=10, pick=shuffled_nodes_with_gaps)
+
+
+def test_prefill_layer_by_layer_calls():
+    # the prefill kernel with layer_begin > 0: one call per layer, then uneven ranges
+    w = small(n_layers=3, steps=6)
+    run_tree(w, 27, every_node, layer_calls=[0, 1, 2, 3])
+    run_tree(w, 28, shuffled_nodes_with_gaps, layer_calls=[0, 2, 3])
+
+
+def test_small_set_decode_layout_layer_by_layer_calls():
+    # fewer than 128 rows: the decode-layout variant, whose one-layer calls split the nodes
+    run_tree(small(n_layers=3, window=20, gc_interval=2, steps=8), 29, few_nodes, layer_calls=[0, 1, 3])
 
 
 def test_tree_attn_rejects_bad_arguments():
