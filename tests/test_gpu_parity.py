@@ -61,6 +61,11 @@ def test_one_layer_calls_fused_selection():
     layer_case(small(n_layers=3, beam_width=4, steps=8), seed=43, calls=[0, 1, 2, 3], fused=True)
 
 
+def test_one_layer_calls_fp32_vector_kernel():
+    # fp32 K/V: the vector-ALU attention kernel, with node splits and the fp32 merge
+    layer_case(small(n_layers=3, head_dim=64, dtype="f32", steps=6), seed=45, calls=[0, 1, 3])
+
+
 def test_one_layer_calls_two_row_blocks():
     # b * G = 64 rows per KV head: the two-row-block WG, with node splits per one-layer call
     layer_case(small(n_layers=2, beam_width=16, n_q_heads=16, n_kv_heads=4, steps=6), seed=44, calls=[0, 1, 2])
