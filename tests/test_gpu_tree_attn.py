@@ -25,7 +25,7 @@ def small(**kw):
     return synth.Workload(**base)
 
 
-def run_tree(w, seed, pick, capacity=None, layer_calls=None):
+def run_tree(w, seed, pick, capacity=None, layer_calls=None, graph_replays=0):
     log(f"tree case T={w.n_tries} L={w.n_layers} Hq={w.n_q_heads} Hkv={w.n_kv_heads} d={w.head_dim} "
         f"P={w.prompt_min}-{w.prompt_max} b={w.beam_width} W={w.window} g={w.gc_interval} steps={w.steps} "
         f"seed={seed}")
@@ -70,6 +70,17 @@ def run_tree(w, seed, pick, capacity=None, layer_calls=None):
         assert err <= ATTN_ABS_TOL and err <= ATTN_REL_TOL * mx + 1e-6, (t, err, mx)
         dead = [j for j, x in enumerate(qs[t]) if x < 0 or tr.alg3_mask()[x] == 0]
         assert np.all(got[:, t, dead] == 0)
+    if graph_replays:  # the same call captured in a HIP graph (as the benchmark times it)
+        og = torch.full_like(qd, 5.0)
+        graph, cs = torch.cuda.CUDAGraph(), torch.cuda.Stream()
+        with torch.cuda.graph(graph, stream=cs):
+            r.dec.tree_attn(0, w.n_layers, qsd, qd, og, r.scale)
+        for _ in range(graph_replays):
+            og.fill_(5.0)
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(og.view(torch.int16), ot.view(torch.int16))
     assert r.dec.status() == 0
     r.dec.close()
     return qs
@@ -166,6 +177,10 @@ def test_prefill_d64_g2_tight_window():
 
 def test_prefill_window_deferred_collection_random_order():
     run_tree(small(window=45, gc_interval=4, steps=14), seed=10, pick=shuffled_nodes_with_gaps)
+
+
+def test_prefill_graph_replays_match_the_eager_call():
+    run_tree(small(steps=6), 30, every_node, graph_replays=3)
 
 
 def test_prefill_layer_by_layer_calls():
