@@ -131,3 +131,61 @@ def test_graph_replay_all_layers_fused():
 def test_graph_replay_layer_calls_window_deferred_collection():
     run_graph_case(small(n_layers=3, window=40, gc_interval=3, steps=14), seed=52, K=14, fused=False,
                    layer_calls=[0, 1, 3])
+
+
+def test_graph_replay_batch_beam_baseline():
+    """The batch-based baseline (Alg 1) as the benchmark times it: attention over per-beam
+    caches, selection, reorder (a full cache gather into the other buffer).  K is even: the
+    buffer holding the current beams is the host's record, which a replay does not advance,
+    and after an even number of steps it is buffer 0 both ways."""
+    import torch
+    w, seed, K = small(steps=10), 53, 10
+    log(f"graph case batch baseline L={w.n_layers} b={w.beam_width} K={K} seed={seed}")
+    src = Steps(w, seed, K, fused=False)  # the same inputs and prompts
+    src.dec.close()
+    dec = B.BatchBeamDecoder(w.n_tries, w.beam_width, w.prompt_max + K + 2, w.vocab, w.n_layers, w.n_q_heads,
+                             w.n_kv_heads, w.head_dim, w.window, w.dtype)
+    kc, vc = dec.prompt_cache()
+    for t in range(w.n_tries):
+        P = int(src.plens[t])
+        _, pk, pv = synth.prompt(w, t, P, seed)
+        kc[t, 0, :, :, :P] = to_dev(w, pk)
+        vc[t, 0, :, :, :P] = to_dev(w, pv)
+
+    def init():
+        dec.init_prompt(src.plens.tolist(), src.tokens)
+        torch.cuda.synchronize()
+
+    def step(i):
+        q, kn, vn, lg, par, tok = src.inp[i]
+        dec.attn_decode(0, w.n_layers, q, kn if i > 0 else None, vn if i > 0 else None, src.out, src.scale)
+        sp, st, ss, sl, lse, ps = src.sel
+        dec.logsoftmax_topk(lg, sp, st, ss, sl, lse, par, tok, ps)
+        dec.reorder(par, tok, ps)
+
+    def snapshot():
+        beams = [dec.read_beams(t) for t in range(w.n_tries)]
+        return beams, [x.clone() for x in [src.out] + src.sel]
+
+    init()
+    for i in range(K):
+        step(i)
+    torch.cuda.synchronize()
+    assert dec.status() == B.TD_OK
+    eager = snapshot()
+    init()
+    g, cs = torch.cuda.CUDAGraph(), torch.cuda.Stream()
+    with torch.cuda.graph(g, stream=cs):
+        for i in range(K):
+            step(i)
+    for rep in range(3):
+        init()
+        x = torch.randn(1 << 16, device="cuda")
+        assert torch.isfinite(x.sum()).item()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        log(f"  replay {rep + 1}")
+        same(eager, snapshot())
+        assert dec.status() == B.TD_OK
+    dec.close()
