@@ -540,7 +540,7 @@ def device_copy_gbs(mib=1024, reps=10):
 
 def tree_prefill_time(bench, K, reps):
     """Multi-query tree attention with every stored node of the step-K/2 trie as a query (the
-    prefill of that serialized trie, Figure 3's square mask), all layers: `reps` launches
+    prefill of that serialized trie, Figure 2's square mask), all layers: `reps` launches
     graph-replayed between events.  Returns (ms per launch, queries, algorithmic flops per
     launch = 4 d Hq L x the keys each query sees, summed over the queries).  Three replays
     warm up first."""
@@ -705,7 +705,7 @@ def main():
         ms, nq, flops = r["tree"]
         out["tree_attention"] = {
             "what": "trie_tree_attn with every stored node of the step-K/2 trie as a query (its "
-                    "prefill, Figure 3's square mask), all layers, one launch",
+                    "prefill, Figure 2's square mask), all layers, one launch",
             "queries": nq, "us_per_launch": round(ms * 1e3, 2), "query_nodes_per_s": round(nq / (ms / 1e3), 1),
             "bound": "mfma", "achieved": round(flops / (ms / 1e3) / 1e12, 2), "peak": 2500.0,
             "unit": "TFLOP/s", "frac": round(flops / (ms / 1e3) / 1e12 / 2500.0, 4),

@@ -150,7 +150,7 @@ td_status trie_attn_decode(td_ctx* ctx, int32_t layer_begin, int32_t n_layers, c
                            hipStream_t stream);
 
 /* Multi-query tree attention (Section 3.3, Alg 3's mask with one row per query node, as
- * in Figure 3): the prefill of a serialized trie, or the verification of draft nodes hung
+ * in Figure 2): the prefill of a serialized trie, or the verification of draft nodes hung
  * under the leaves.  For every trie t and j < q_max, the query of the stored node at
  * logical slot d_qslots[t][j] attends to that node's root path - its ancestors and itself
  * - restricted to keys with depth(q) - depth < W when a window is set:

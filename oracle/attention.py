@@ -8,7 +8,7 @@ that path.  This module computes that definition directly: materialise the
 path, then dense softmax attention over it, in float64.
 
 ``tree_attention`` generalises this to any set of query nodes, several per branch (Alg 3's
-mask with one row per query node, as drawn in Figure 3): the prefill of a serialized trie,
+mask with one row per query node, as drawn in Figure 2): the prefill of a serialized trie,
 or the verification of a draft tree hung under the leaves.
 
 Conventions (standard model attention): query head h reads KV head
@@ -73,7 +73,7 @@ def node_path(trie, node):
 
 
 def tree_attention(trie, slots, q: np.ndarray, scale: float) -> np.ndarray:
-    """Multi-query tree attention (Alg 3's mask with one row per query node, Figure 3): the
+    """Multi-query tree attention (Alg 3's mask with one row per query node, Figure 2): the
     query of stored node ``slots[j]`` attends to that node's visible root path.  A slot of
     -1, or of a node on no live leaf's path (a dead node awaiting collection), has no keys:
     its output is zero.

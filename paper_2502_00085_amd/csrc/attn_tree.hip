@@ -1,6 +1,6 @@
 // Multi-query tree attention over the stored trie, prefill-shaped (gfx950 matrix cores).
 //
-// Alg 3's mask with one row per query node (Figure 3): the query of stored node q attends
+// Alg 3's mask with one row per query node (Figure 2): the query of stored node q attends
 // to the nodes m with depth(m) <= depth(q) and mask(m) containing mask(q), which for nodes
 // on a live path is exactly the ancestor-or-self relation, within the window of depth(q).
 // When many nodes are queries (the prefill of a serialized trie), the decode kernel's

@@ -614,7 +614,7 @@ def pin_ancestry_is_mask_containment(w, seed, steps=8):
 
 def pin_tree_dense_mask(w, seed, steps=6):
     """All live nodes as queries against dense attention (torch SDPA, float64) over every
-    stored node with the square mask of Figure 3 (ancestor-or-self, within the window)."""
+    stored node with the square mask of Figure 2 (ancestor-or-self, within the window)."""
     import torch
     import torch.nn.functional as F
     trie = grown_trie_with_kv(w, seed, steps)
