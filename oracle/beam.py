@@ -20,8 +20,13 @@ import numpy as np
 
 
 def row_lse32(logits: np.ndarray) -> np.ndarray:
-    """logits [R][V] float32 -> lse [R] float32 (float64 log-sum-exp, rounded once)."""
+    """logits [R][V] float32 -> lse [R] float32 (float64 log-sum-exp, rounded once).
+
+    Logits are finite or -inf (a masked token, weight 0); a row needs a finite one: a row
+    without one, or with a NaN or +inf, has no distribution (ValueError)."""
     x = np.asarray(logits, dtype=np.float32).astype(np.float64)
+    if np.any(np.isnan(x) | (x == np.inf)) or not np.all(np.any(np.isfinite(x), axis=1)):
+        raise ValueError("every row needs a finite logit, and none may be NaN or +inf")
     m = x.max(axis=1)
     lse64 = m + np.log(np.exp(x - m[:, None]).sum(axis=1))
     return lse64.astype(np.float32)

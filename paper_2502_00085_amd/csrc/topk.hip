@@ -219,11 +219,17 @@ __global__ __launch_bounds__(kChunkThreads) void k_topb_chunk(DevState s, const 
   for (int w = 1; w < kChunkWaves; ++w) m = fmaxf(m, wm[w]);
   const double md = (double)m;
   double acc = 0.0;
+  bool bad = false;  // a NaN or +inf logit
 #pragma unroll
   for (int i = 0; i < kChunkPer; ++i) {
     const int v = v0 + i * kChunkThreads + (int)threadIdx.x;
-    if (v < V) acc += exp((double)x[i] - md);
+    // (a chunk whose logits are all -inf adds nothing; exp(-inf - -inf) would be NaN)
+    if (v < V && md != -INFINITY) acc += exp((double)x[i] - md);
+    bad |= v < V && !(x[i] < INFINITY);
   }
+  // an invalid logit poisons the chunk's sum: the row's lse is then NaN and the call
+  // reports the row (k_topb_final)
+  if (bad) acc = __builtin_nan("");
   acc = __ockl_wfred_add_f64(acc);
   if (lane == 0) ws[wave] = acc;
   __syncthreads();
@@ -236,14 +242,16 @@ __global__ __launch_bounds__(kChunkThreads) void k_topb_chunk(DevState s, const 
 }
 
 // fp64 log-sum-exp of row r from its chunk partials, computed by one wave (lane-strided
-// partials, fixed-order wave reductions): bit-reproducible.
+// partials, fixed-order wave reductions): bit-reproducible.  Chunks with a zero sum (every
+// logit -inf) are skipped; a row without a finite logit gets -inf, a row holding a NaN or
+// +inf logit NaN.
 __device__ inline float row_lse32_wave(const double* p, int nch) {
   const int lane = threadIdx.x & 63;
   double M = -INFINITY;
   for (int c = lane; c < nch; c += 64) M = fmax(M, p[2 * c]);
   M = __ockl_wfred_max_f64(M);
   double S = 0.0;
-  for (int c = lane; c < nch; c += 64) S += p[2 * c + 1] * exp(p[2 * c] - M);
+  for (int c = lane; c < nch; c += 64) S += p[2 * c + 1] != 0.0 ? p[2 * c + 1] * exp(p[2 * c] - M) : 0.0;
   S = __ockl_wfred_add_f64(S);
   return (float)(M + log(S));
 }
@@ -589,6 +597,12 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
   }
 
   for (int j = threadIdx.x; j < b; j += kFinalThreads) {
+    // a live row without a finite log-sum-exp (no finite logit, or a NaN / +inf one) is
+    // invalid input: reported, and the fused append is given an invalid selection, so
+    // that it leaves the trie as it was
+    bool bad_row = false;
+    for (int r = 0; r < n_live; ++r) bad_row |= !(fabsf(row_lse[r]) < INFINITY);
+    if (bad_row) set_status(s.status, kDevEinval);
     const uint64_t kx = best_c[j];
     uint32_t f = key_flat(kx);
     float x = key_x(kx);
@@ -605,7 +619,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     sel_score[(size_t)t * b + j] = sc;
     sel_logprob[(size_t)t * b + j] = lp;
     if (APPEND && pair_parent == nullptr) {
-      ash.sp[j] = r;
+      ash.sp[j] = bad_row ? -1 : r;
       ash.stok[j] = v;
       ash.ssc[j] = sc;
     }
@@ -621,7 +635,9 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     if (pp >= 0 && pp < n_live && pv >= 0 && pv < V) sc = score_only(pair_x, row_lse[pp], row_score[pp]);
     pair_score[(size_t)t * b + pj] = sc;
     if (APPEND) {
-      ash.sp[pj] = pp;
+      bool bad_row = false;  // (as for the selection above)
+      for (int r = 0; r < n_live; ++r) bad_row |= !(fabsf(row_lse[r]) < INFINITY);
+      ash.sp[pj] = bad_row ? -1 : pp;
       ash.stok[pj] = pv;
       ash.ssc[pj] = sc;
     }

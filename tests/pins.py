@@ -295,6 +295,13 @@ def pin_lse_vs_scipy(seed, rows=2000, vocab=4096):
     got = obeam.row_lse32(x)
     bad = int(np.count_nonzero(got.view(np.uint32) != ref.view(np.uint32)))
     assert bad == 0, f"{bad} of {rows} rows differ from fl32(scipy logsumexp)"
+    # masked tokens (-inf): whole runs of a row, and rows with a handful of finite logits
+    x[::3, 1000:2500] = -np.inf
+    x[1::7, :] = -np.inf
+    x[1::7, g.integers(0, vocab, 5)] = 2.0
+    ref = logsumexp(x.astype(np.float64), axis=1).astype(np.float32)
+    got = obeam.row_lse32(x)
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32)), "rows with -inf logits differ"
 
 
 def _enumerate_topb(logits, scores, b):

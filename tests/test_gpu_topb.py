@@ -142,3 +142,73 @@ def test_entries_beyond_the_register_batch(b):
     logits = g.normal(0, 3, (b, V)).astype(np.float32)
     scores = -np.sort(g.uniform(0, 2, b)).astype(np.float32)
     run_topb(b, logits, scores)
+
+
+def test_minus_inf_chunks_and_mostly_masked_rows():
+    """Masked tokens (-inf logits, as constrained decoding writes them): a whole 4096-logit
+    chunk of one row and its tail chunk, and a row with only five finite logits.  A chunk
+    without a finite logit adds nothing to its row's sum of exponentials."""
+    g = np.random.default_rng(11)
+    b, V = 8, 3 * 4096 + 17
+    logits = g.normal(0, 3, (b, V)).astype(np.float32)
+    logits[1, 4096:2 * 4096] = -np.inf
+    logits[1, 3 * 4096:] = -np.inf
+    keep = g.choice(V, 5, replace=False)
+    row = np.full(V, -np.inf, np.float32)
+    row[keep] = logits[3, keep] + 4.0
+    logits[3] = row
+    logits[5, ::3] = -np.inf
+    scores = -np.sort(g.uniform(0, 4, b)).astype(np.float32)
+    pairs = (np.array([3, 3, 1, 0, 2, 4, 6, 7]), np.concatenate([keep[:2], g.integers(0, 4096, 6)]))
+    run_topb(b, logits, scores, pairs)
+
+
+def test_single_row_all_but_a_few_masked_llama_vocab():
+    """Step 1 (one live beam) at V = 128,256 with all but b + 3 tokens masked: every chunk
+    but a few holds only -inf."""
+    g = np.random.default_rng(12)
+    b, V = 8, 128256
+    row = np.full((1, V), -np.inf, np.float32)
+    keep = g.choice(V, b + 3, replace=False)
+    row[0, keep] = g.normal(0, 3, b + 3).astype(np.float32)
+    run_topb(b, row, np.array([0.0], np.float32))
+
+
+@pytest.mark.parametrize("bad", ["all_masked", "nan", "pos_inf"])
+def test_live_row_without_a_valid_distribution_is_rejected(bad):
+    """A live row with no finite logit, or with a NaN or +inf one, is invalid input: the
+    device status reports TD_EINVAL, and the fused call leaves the trie as it was."""
+    import torch
+    import paper_2502_00085_amd.binding as B
+    b, V, P, n_live = 4, 5000, 5, 3
+    log(f"invalid row case {bad}")
+    dec = B.TrieDecoder(1, b, P + b + 2, V, 1, 1, 1, 64, 0, "bf16")
+    try:
+        st0 = chain_with_leaves(P, n_live, np.array([0.0, -1.0, -2.0], np.float32))
+        dec.load_state(0, st0)
+        g = np.random.default_rng(13)
+        full = g.normal(0, 3, (b, V)).astype(np.float32)
+        if bad == "all_masked":
+            full[1] = -np.inf
+        elif bad == "nan":
+            full[2, 4100] = np.nan
+        else:
+            full[0, 7] = np.inf
+        lg = torch.from_numpy(full).reshape(1, b, V).cuda()
+        i32 = dict(dtype=torch.int32, device="cuda")
+        f32 = dict(dtype=torch.float32, device="cuda")
+        sp, stk = torch.empty((1, b), **i32), torch.empty((1, b), **i32)
+        ss, sl, lse = (torch.empty((1, b), **f32) for _ in range(3))
+        dec.logsoftmax_topk(lg, sp, stk, ss, sl, lse)
+        torch.cuda.synchronize()
+        assert dec.status() == B.TD_EINVAL
+        dec.topk_append(lg, sp, stk, ss, sl, lse)
+        torch.cuda.synchronize()
+        assert dec.status() == B.TD_EINVAL
+        after = dec.read_state(0)
+        assert after["n_nodes"] == P + n_live and after["n_live"] == n_live
+        assert np.array_equal(after["mask"][:P + n_live], st0["mask"])
+        assert np.array_equal(after["leaf_score"][:n_live].view(np.uint32),
+                              st0["leaf_score"].view(np.uint32))
+    finally:
+        dec.close()
