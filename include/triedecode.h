@@ -82,7 +82,8 @@ typedef struct {
   int32_t n_layers;     /* L >= 1                                                         */
   int32_t n_q_heads;    /* Hq, a multiple of Hkv                                          */
   int32_t n_kv_heads;   /* Hkv >= 1                                                       */
-  int32_t head_dim;     /* d in {64, 96, 128}                                             */
+  int32_t head_dim;     /* d: a multiple of 32 in [32, 256] (else TD_EINVAL); the kernels */
+                        /*   implement 64, 96 and 128 (others: TD_EUNSUPPORTED)          */
   int32_t window;       /* sliding window W (0 = dense): key visible iff D - depth < W    */
   int32_t dtype;        /* td_dtype of pools, q, out, k_new, v_new                        */
   int32_t attn_impl;    /* td_attn_impl                                                   */
@@ -196,6 +197,10 @@ td_status td_set_kernel_events(td_ctx* ctx, int32_t phase, hipEvent_t start, hip
  * Optional scoring of caller-chosen pairs (d_pair_parent/d_pair_token [T][b], both
  * NULL or both set): d_pair_score receives s of each pair by the same formula.
  * Reads n_live and leaf scores from the context on the device.
+ * Logits must be finite or -inf (a masked token), with a finite one in every live row;
+ * a live row that breaks this (no finite logit, or a NaN or +inf one) sets the sticky
+ * device status TD_EINVAL, its selection outputs are unspecified, and the fused
+ * beam_topk_append leaves the trie unchanged.
  * With an end-of-sequence token (desc.eos_token >= 0; the paper has none, this is the
  * usual beam-search rule): an EOS candidate ranked better than b in the order above
  * finishes a hypothesis, and the selection (the next beams) is the b best non-EOS
@@ -223,7 +228,8 @@ td_status beam_logsoftmax_topk(td_ctx* ctx, const float* d_logits, int32_t* d_se
  * the appends before the next collection need, the trie is re-packed at slot 0.  The
  * K/V rows of moved survivors are copied to their new slots by the next trie_attn_decode
  * call of each layer, before it reads them (until then the pools hold those rows at their
- * old slots; td_init_prompt and td_load_state drop copies still due).  The new leaves
+ * old slots; td_init_prompt drops every copy still due, td_load_state those of the trie it
+ * loads).  The new leaves
  * become the last b slots in rank j order; their K/V rows are pending until the next
  * trie_attn_decode.
  * Inputs [T][b] device.  Invalid selections / capacity overflow (a trie without room for
@@ -257,7 +263,11 @@ td_status td_read_finished(td_ctx* ctx, int32_t trie, float* h_norm, float* h_sc
 
 /* Copy trie t to the host (synchronises the device). */
 td_status td_read_state(td_ctx* ctx, int32_t trie, td_state* host_out);
-/* Replace trie t by a host state (synchronous).  Slots are placed at base 0.  The state
+/* Replace trie t by a host state (synchronous).  Slots are placed at base 0, and row
+ * copies still due for trie t are dropped; those of the other tries stay due.  With other
+ * initialised tries, kv_pending must equal theirs (else TD_EINVAL), and a state with
+ * kv_pending = 1 is accepted only before the step's first trie_attn_decode (else
+ * TD_ESTATE): the next attention calls then store its leaves' rows too.  The state
  * must be one the method can produce: depth non-decreasing along slots, parents before
  * children with depth + 1, leaves = last n_live slots in rank order with one-hot masks,
  * no all-beam slot after a slot on only some paths (dead slots, mask 0, may lie anywhere

@@ -26,18 +26,24 @@ from typing import Optional
 import numpy as np
 
 from .attention import path_attention
-from .beam import pair_scores, select
+from .beam import pair_scores, row_lse32, select
 from .finished import FinishedPool, select_with_eos
 from .trie import Trie
 
 
 def decode_step(trie: Trie, step: int, q: Optional[np.ndarray], k_new, v_new, logits: np.ndarray,
-                scale: float, script=None, eos: int = -1, pool: Optional[FinishedPool] = None) -> dict:
+                scale: float, script=None, eos: int = -1, pool: Optional[FinishedPool] = None,
+                append: bool = True, full_sort: bool = True, lse=None) -> dict:
     """q / k_new / v_new: [L'][b][..][d] (rows >= n_live unused) or None to skip attention.
 
     logits: [b][V] (rows >= n_live unused).  script: (parent_rank [b], token [b]) or None.
     eos >= 0: the end-of-sequence token (the next beams are the best non-EOS candidates and
-    the finishing EOS candidates go to ``pool``, see ``finished``).
+    the finishing EOS candidates go to ``pool``, see ``finished``).  append=False stops
+    after the selection (the step's append is not applied: the trie keeps its leaves, as
+    when a selection is rejected).  full_sort=False (scripted mode, no EOS) skips the
+    ranking of all n_live x V candidates: only the rows' lse and the pairs' scores are
+    computed (a caller then checks a given selection against ``beam.candidate_scores``).
+    lse: the rows' log-sum-exps when already computed for these logits (``beam.row_lse32``).
     """
     n_live = trie.n_live
     if step > 1 and k_new is not None:
@@ -53,8 +59,12 @@ def decode_step(trie: Trie, step: int, q: Optional[np.ndarray], k_new, v_new, lo
                 leaves = list(trie.leaves)
                 tokens = lambda r: [n.token for n in trie.path(leaves[r])]  # noqa: E731
             pool.process(sel, step, tokens, eos)
-    else:
+    elif full_sort:
         sel = select(logits[:n_live], trie.scores, trie.b)
+    else:
+        if script is None:
+            raise ValueError("full_sort=False needs a script (the selection is not computed)")
+        sel = {"lse": row_lse32(logits[:n_live]) if lse is None else np.asarray(lse, np.float32)}
     out.update(sel)
     if script is None:
         par, tok, sc = sel["sel_parent"], sel["sel_token"], sel["sel_score"]
@@ -63,6 +73,9 @@ def decode_step(trie: Trie, step: int, q: Optional[np.ndarray], k_new, v_new, lo
         sc, lp = pair_scores(logits[:n_live], sel["lse"], trie.scores, par, tok)
         out["pair_score"] = sc
         out["pair_logprob"] = lp
+    if not append:
+        out["state"] = trie.state()
+        return out
     trie.append(par, tok, sc)
     if trie.gc_due():
         trie.garbage_collect()

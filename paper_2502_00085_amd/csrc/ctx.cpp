@@ -102,8 +102,10 @@ td_status td_create(const td_desc* d, td_ctx** out) {
   if (d->n_layers < 1 || d->n_kv_heads < 1 || d->n_q_heads < d->n_kv_heads ||
       d->n_q_heads % d->n_kv_heads != 0)
     return fail(nullptr, TD_EINVAL, "need n_layers >= 1, n_kv_heads >= 1, n_q_heads %% n_kv_heads == 0");
+  if (d->head_dim < 32 || d->head_dim > 256 || d->head_dim % 32 != 0)
+    return fail(nullptr, TD_EINVAL, "head_dim must be a multiple of 32 in [32, 256]");
   if (d->head_dim != 64 && d->head_dim != 96 && d->head_dim != 128)
-    return fail(nullptr, TD_EUNSUPPORTED, "head_dim must be 64, 96 or 128");
+    return fail(nullptr, TD_EUNSUPPORTED, "the kernels implement head_dim 64, 96 and 128");
   if (d->capacity < d->beam_width + 1 || d->capacity > (1 << 30))
     return fail(nullptr, TD_EINVAL, "capacity must be in [beam_width + 1, 2^30]");
   if (d->window < 0) return fail(nullptr, TD_EINVAL, "window must be >= 0");
@@ -515,6 +517,12 @@ td_status td_load_state(td_ctx* c, int32_t trie, const td_state* in) {
   for (int t = 0; t < s.T; ++t) others = others || (t != trie && c->inited[t]);
   if (others && (in->kv_pending != 0) != c->pending)
     return fail(c, TD_EINVAL, "kv_pending must agree with the other initialised tries");
+  if (others && c->pending) {
+    // the loaded leaves' rows are stored by the step's attention calls: none may have run
+    for (int l = 0; l < s.L; ++l)
+      if (c->layer_written[l])
+        return fail(c, TD_ESTATE, "a trie with pending leaves can be loaded only before the step's first trie_attn_decode");
+  }
   hipError_t e = hipDeviceSynchronize();
   const size_t off = (size_t)trie * s.cap;
   const size_t n = (size_t)N;
@@ -538,12 +546,17 @@ td_status td_load_state(td_ctx* c, int32_t trie, const td_state* in) {
   if (e == hipSuccess) e = hipMemcpy(s.hdr + trie, &h, sizeof h, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemset(s.fin_count + trie, 0, sizeof(int32_t));
   if (e == hipSuccess) e = hipMemset(s.fin_done + trie, 0, sizeof(int32_t));
+  // row copies still due for this trie are void (its rows are where the state says);
+  // those of the other tries stay due
+  if (e == hipSuccess) e = hipMemset(s.n_moves + trie, 0, sizeof(int32_t));
   if (e != hipSuccess) return hip_fail(c, e, "td_load_state");
   c->inited[trie] = 1;
   c->leaf_depth[trie] = h.leaf_depth;
-  c->pending = in->kv_pending != 0;
-  c->moves_pending = false;
-  c->layer_written.assign(s.L, 0);
+  if (!others) {  // (with other tries the step's state is theirs, and kv_pending agrees with it)
+    c->pending = in->kv_pending != 0;
+    c->moves_pending = false;
+    c->layer_written.assign(s.L, 0);
+  }
   return TD_OK;
 }
 

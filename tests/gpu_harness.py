@@ -42,10 +42,14 @@ class Run:
 
     def __init__(self, w, seed=0, layers=None, attn_impl=0, capacity=None, mode="scripted",
                  oracle=True, phase_events=False, eos=-1, eos_boost=0.0, length_penalty=1.0,
-                 early_stopping=False, fused=False, layer_calls=None):
+                 early_stopping=False, fused=False, layer_calls=None, input_period=0):
         import torch
         import paper_2502_00085_amd.binding as B
         self.w, self.seed, self.mode, self.phase_events = w, seed, mode, phase_events
+        # q / k_new / v_new / logits of steps 1 .. input_period reused in turn (0: fresh every
+        # step), kept on the host and on the device; the trie growth is drawn every step
+        self.input_period = input_period
+        self._in_host, self._in_dev, self._lse = {}, {}, {}
         self.fused = fused  # beam_topk_append instead of beam_logsoftmax_topk + trie_append_prune
         # attention as several trie_attn_decode calls over layer ranges [c[i], c[i+1]) (as a
         # model calls it), instead of one call over every layer
@@ -76,23 +80,55 @@ class Run:
         self.pending = False
         self.step_no = 0
 
+    def phase(self, s):
+        """The step whose q / k_new / v_new / logits step s uses."""
+        return (s - 1) % self.input_period + 1 if self.input_period > 0 else s
+
     def inputs(self, s):
         w = self.w
-        q, kn, vn = synth.step_qkv(w, s, self.seed)
-        logits = synth.step_logits(w, s, self.seed)
-        if self.eos >= 0 and self.eos_boost:
-            logits[:, :, self.eos] += np.float32(self.eos_boost)  # end-of-sequence candidates rank high
+        ph = self.phase(s)
+        if ph in self._in_host:
+            q, kn, vn, logits = self._in_host[ph]
+        else:
+            q, kn, vn = synth.step_qkv(w, ph, self.seed)
+            logits = synth.step_logits(w, ph, self.seed)
+            if self.eos >= 0 and self.eos_boost:
+                logits[:, :, self.eos] += np.float32(self.eos_boost)  # end-of-sequence candidates rank high
+            if self.input_period > 0:
+                self._in_host[ph] = (q, kn, vn, logits)
         par, tok = synth.step_script(w, s, self.seed) if self.mode == "scripted" else (None, None)
         return q, kn, vn, logits, par, tok
 
-    def gpu_step(self, s, q, kn, vn, logits, par, tok):
+    def row_lse(self, s, t, logits_t, n_live):
+        """oracle.beam.row_lse32 of trie t's rows at step s (memoised per input phase: the
+        same logits give the same values)."""
+        import oracle.beam as obeam
+        if self.input_period <= 0:
+            return obeam.row_lse32(logits_t[:n_live])
+        key = (self.phase(s), t)
+        if key not in self._lse:
+            self._lse[key] = obeam.row_lse32(logits_t)
+        return self._lse[key][:n_live]
+
+    def dev_inputs(self, s, q, kn, vn, logits):
+        import torch
+        ph = self.phase(s)
+        if ph in self._in_dev:
+            return self._in_dev[ph]
+        d = (to_dev(self.w, q), to_dev(self.w, kn), to_dev(self.w, vn),
+             torch.from_numpy(np.ascontiguousarray(logits)).cuda())
+        if self.input_period > 0:
+            self._in_dev[ph] = d
+        return d
+
+    def gpu_step(self, s, q, kn, vn, logits, par, tok, want_o=True):
         import torch
         w, dec = self.w, self.dec
         T, b = w.n_tries, w.beam_width
-        qd = to_dev(w, q)
+        qd, knd, vnd, ld = self.dev_inputs(s, q, kn, vn, logits)
         out = torch.full_like(qd, 7.0)  # garbage: every row must be written
-        knd = to_dev(w, kn) if self.pending else None
-        vnd = to_dev(w, vn) if self.pending else None
+        if not self.pending:
+            knd = vnd = None
         evs = []
         if self.phase_events:
             import paper_2502_00085_amd.binding as B
@@ -107,7 +143,6 @@ class Run:
                                 None if vnd is None else vnd[l0:l1], out[l0:l1], self.scale)
         else:
             dec.attn_decode(0, w.n_layers, qd, knd, vnd, out, self.scale)
-        ld = torch.from_numpy(np.ascontiguousarray(logits)).cuda()
         i32 = dict(dtype=torch.int32, device="cuda")
         f32 = dict(dtype=torch.float32, device="cuda")
         sp, st = torch.empty((T, b), **i32), torch.empty((T, b), **i32)
@@ -129,7 +164,7 @@ class Run:
                 dec.append_prune(sp, st, ss)
         torch.cuda.synchronize()
         self.pending = True
-        res = {"o": from_dev(out), "sel_parent": sp.cpu().numpy(), "sel_token": st.cpu().numpy(),
+        res = {"o": from_dev(out) if want_o else None, "sel_parent": sp.cpu().numpy(), "sel_token": st.cpu().numpy(),
                "sel_score": ss.cpu().numpy(), "sel_logprob": sl.cpu().numpy(), "lse": lse.cpu().numpy()}
         if ps is not None:
             res["pair_score"] = ps.cpu().numpy()
@@ -142,24 +177,38 @@ class Run:
                 e.close()
         return res
 
-    def step(self, check=True, check_attn=True):
-        """Run one step on both sides; return the list of mismatch messages (empty = parity)."""
+    def step(self, check=True, check_attn=True, edit_script=None, rejected=(), full_sort=True):
+        """Run one step on both sides; return the list of mismatch messages (empty = parity).
+
+        edit_script(par, tok) -> (par, tok) changes the step's scripted pairs (both sides);
+        the oracle does not apply the append of the tries in ``rejected`` (pairs the device
+        must reject: it keeps those tries as they were).  full_sort=False (scripted mode):
+        the device's top-b is checked by ``verify_topb`` instead of against the oracle's
+        ranking of every candidate."""
         self.step_no += 1
         s = self.step_no
         w = self.w
         q, kn, vn, logits, par, tok = self.inputs(s)
+        if edit_script is not None:
+            par, tok = edit_script(par.copy(), tok.copy())
         n_live = [tr.n_live for tr in self.tries] if self.tries else None
-        g = self.gpu_step(s, q, kn, vn, logits, par, tok)
+        g = self.gpu_step(s, q, kn, vn, logits, par, tok, want_o=check and check_attn)
         if not check or not self.tries:
             return [], g
         errs = []
-        qf, knf, vnf = (synth.as_f32(w, a[self.layers]) for a in (q, kn, vn))
+        qf = synth.as_f32(w, q[self.layers]) if check_attn else None
+        knf, vnf = (synth.as_f32(w, a[self.layers]) for a in (kn, vn))
         for t, tr in enumerate(self.tries):
             nl = n_live[t]
             script = (par[t], tok[t]) if self.mode == "scripted" else None
+            scores = tr.scores.copy()
+            lse = None if full_sort else self.row_lse(s, t, logits[t], nl)
             ref = odec.decode_step(tr, s, qf[:, t] if check_attn else None, knf[:, t], vnf[:, t],
                                    logits[t], self.scale, script, self.eos,
-                                   self.pools[t] if self.eos >= 0 else None)
+                                   self.pools[t] if self.eos >= 0 else None, append=t not in rejected,
+                                   full_sort=full_sort, lse=lse)
+            if not full_sort:
+                errs += verify_topb(logits[t, :nl], ref["lse"], scores, g, t, w.beam_width, f"step {s} trie {t}")
             errs += compare(w, s, t, nl, self.layers, g, ref, check_attn)
             if self.eos >= 0:
                 errs += compare_finished(s, t, g["finished"][t], self.pools[t])
@@ -181,12 +230,13 @@ def compare(w, s, t, nl, layers, g, ref, check_attn=True):
             errs.append(f"{tag}: attention max err {err:.3e} (max |o_ref| {mx:.3e})")
         if nl < w.beam_width and np.any(og[:, nl:] != 0):
             errs.append(f"{tag}: output rows of beams >= n_live are not zero")
-    for k in ("sel_parent", "sel_token"):
-        if not np.array_equal(g[k][t], ref[k]):
-            errs.append(f"{tag}: {k} {g[k][t].tolist()} != {ref[k].tolist()}")
-    for k in ("sel_score", "sel_logprob"):
-        if not np.array_equal(g[k][t].view(np.uint32), ref[k].view(np.uint32)):
-            errs.append(f"{tag}: {k} bits differ {g[k][t].tolist()} vs {ref[k].tolist()}")
+    if "sel_parent" in ref:  # (else the selection was checked by verify_topb)
+        for k in ("sel_parent", "sel_token"):
+            if not np.array_equal(g[k][t], ref[k]):
+                errs.append(f"{tag}: {k} {g[k][t].tolist()} != {ref[k].tolist()}")
+        for k in ("sel_score", "sel_logprob"):
+            if not np.array_equal(g[k][t].view(np.uint32), ref[k].view(np.uint32)):
+                errs.append(f"{tag}: {k} bits differ {g[k][t].tolist()} vs {ref[k].tolist()}")
     if not np.array_equal(g["lse"][t][:nl].view(np.uint32), ref["lse"].view(np.uint32)):
         errs.append(f"{tag}: lse bits differ {g['lse'][t][:nl]} vs {ref['lse']}")
     if "pair_score" in ref and not np.array_equal(g["pair_score"][t].view(np.uint32),
@@ -203,6 +253,69 @@ def compare(w, s, t, nl, layers, g, ref, check_attn=True):
                 errs.append(f"{tag}: state {k} differs at slots {bad.tolist()}")
         if not np.array_equal(gs["leaf_score"].view(np.uint32), rs["leaf_score"].view(np.uint32)):
             errs.append(f"{tag}: leaf_score bits differ")
+    return errs
+
+
+def _f32_order(x):
+    """float32 array -> int64 keys in the order of the values (-0 below +0)."""
+    u = np.asarray(x, np.float32).view(np.uint32).astype(np.int64)
+    return np.where(u >= 0x80000000, 0xFFFFFFFF - u, u + 0x80000000)
+
+
+def _f32_from_order(o):
+    o = np.asarray(o, np.int64)
+    u = np.where(o >= 0x80000000, o - 0x80000000, 0xFFFFFFFF - o).astype(np.uint32)
+    return u.view(np.float32)
+
+
+def verify_topb(logits, lse, scores, g, t, b, tag):
+    """Checks the device's selection of trie t (g["sel_*"][t]) against the unique top-b of
+    the n_live x V candidates (score s descending, flat index r*V+v ascending), without
+    ranking them all.  Scores come from ``oracle.beam.candidate_scores`` (the oracle's
+    formula) and are compared bit for bit:
+
+    * the selected candidates' s and lp equal the formula's, and their keys decrease;
+    * the candidates whose key is at least the last selected one's are exactly the
+      selection.  They are found row by row with a threshold on the logit: within a row s
+      is a non-decreasing function of x (float32 subtraction and addition round
+      monotonically), so s >= s_b holds exactly for x >= x*_r, the smallest float32 with
+      that property (found by bisection over the float32 order)."""
+    import oracle.beam as obeam
+    errs = []
+    R, V = logits.shape
+    par = g["sel_parent"][t].astype(np.int64)
+    tok = g["sel_token"][t].astype(np.int64)
+    if np.any(par < 0) | np.any(par >= R) | np.any(tok < 0) | np.any(tok >= V):
+        return [f"{tag}: selection outside the candidates: {par.tolist()} {tok.tolist()}"]
+    scores = np.asarray(scores, np.float32)
+    lp1, s1 = obeam.candidate_scores(logits[par, tok][:, None], lse[par], scores[par])
+    lp1, s1 = lp1[:, 0], s1[:, 0]
+    for k, want in (("sel_score", s1), ("sel_logprob", lp1)):
+        if not np.array_equal(g[k][t].view(np.uint32), want.view(np.uint32)):
+            errs.append(f"{tag}: {k} bits differ from the formula")
+    f = par * V + tok
+    if not all(s1[i] > s1[i + 1] or (s1[i] == s1[i + 1] and f[i] < f[i + 1]) for i in range(b - 1)):
+        errs.append(f"{tag}: selection not in key order")
+    sb, fb = s1[-1], f[-1]
+    # x*_r: smallest float32 logit whose score in row r reaches sb
+    lo = np.full(R, int(_f32_order(np.float32(-np.inf))), np.int64)
+    hi = np.full(R, int(_f32_order(np.float32(np.inf))), np.int64)
+    while np.any(lo < hi):
+        mid = (lo + hi) // 2
+        _, sm = obeam.candidate_scores(_f32_from_order(mid)[:, None], lse, scores)
+        ok = sm[:, 0] >= sb
+        hi = np.where(ok, mid, hi)
+        lo = np.where(ok, lo, mid + 1)
+    xstar = _f32_from_order(lo)
+    rr, vv = np.nonzero(logits >= xstar[:, None])
+    lp2, s2 = obeam.candidate_scores(logits[rr, vv][:, None], lse[rr], scores[rr])
+    s2 = s2[:, 0]
+    if np.any(s2 < sb):
+        errs.append(f"{tag}: threshold search broken")
+    f2 = rr * V + vv
+    at_least = (s2 > sb) | ((s2 == sb) & (f2 <= fb))
+    if not np.array_equal(np.sort(f2[at_least]), np.sort(f)):
+        errs.append(f"{tag}: selection is not the top {b}: {int(at_least.sum())} candidates reach its last key")
     return errs
 
 

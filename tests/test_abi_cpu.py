@@ -69,6 +69,22 @@ def test_create_rejects_bad_descriptors(kw, frag):
     assert frag in L.td_error_string(None).decode()
 
 
+@pytest.mark.parametrize("d,want", [(80, "TD_EINVAL"), (16, "TD_EINVAL"), (288, "TD_EINVAL"), (0, "TD_EINVAL"),
+                                    (32, "TD_EUNSUPPORTED"), (160, "TD_EUNSUPPORTED"),
+                                    (192, "TD_EUNSUPPORTED"), (224, "TD_EUNSUPPORTED"),
+                                    (256, "TD_EUNSUPPORTED")])
+def test_head_dim_outside_the_kernels(d, want):
+    """The boundary takes d as a multiple of 32 up to 256; other values are invalid, and the
+    kernels implement 64, 96 and 128 of the valid ones (the rest: unsupported).  Both are
+    rejected by td_create, before anything is allocated."""
+    L = B.lib()
+    ctx = ctypes.c_void_p()
+    st = L.td_create(ctypes.byref(_desc(head_dim=d)), ctypes.byref(ctx))
+    assert st == getattr(B, want), (d, L.td_status_name(st))
+    assert ctx.value is None
+    assert "head_dim" in L.td_error_string(None).decode()
+
+
 def test_null_context_is_rejected_by_every_call():
     L = B.lib()
     assert L.td_destroy(None) == B.TD_EINVAL
