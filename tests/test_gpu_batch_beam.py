@@ -58,22 +58,27 @@ def test_greedy_single_beam():
 
 
 def test_trie_equals_batch_beam_search_on_the_gpu():
-    """Both GPU paths on the same inputs: identical selections and scores at every step,
-    attention outputs within the bf16 rounding of either."""
+    """Both GPU paths on the same inputs, each checked against its own oracle every step
+    (the trie decoder against the oracle trie, the baseline against the oracle's batch beam
+    search), and against each other: identical selections and scores, attention outputs
+    within the bf16 rounding of either."""
     import torch
     w = small(beam_width=8, steps=10, alpha=0.5)
     log("trie vs batch on the GPU")
-    rt = Run(w, seed=6, oracle=False, mode="driven")
+    rt = Run(w, seed=6, mode="driven")
     rb = BatchRun(w, seed=6, mode="driven")
     for s in range(1, w.steps + 1):
-        _, gt = rt.step(check=False)
-        _, gb = rb.step()
+        et, gt = rt.step()
+        eb, gb = rb.step()
+        assert not et, "trie decoder vs oracle: " + "\n".join(et[:10])
+        assert not eb, "batch baseline vs oracle: " + "\n".join(eb[:10])
         for k in ("sel_parent", "sel_token"):
             assert np.array_equal(gt[k], gb[k]), (s, k)
         for k in ("sel_score", "sel_logprob"):
             assert np.array_equal(gt[k].view(np.uint32), gb[k].view(np.uint32)), (s, k)
         nl = 1 if s == 1 else w.beam_width
         assert float(np.max(np.abs(gt["o"][:, :, :nl] - gb["o"][:, :, :nl]))) <= 2e-2
+    assert rt.dec.status() == B.TD_OK and rb.dec.status() == B.TD_OK
     rt.dec.close()
     rb.dec.close()
     torch.cuda.synchronize()

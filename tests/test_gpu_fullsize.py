@@ -1,6 +1,14 @@
-"""GPU parity at the full model shapes, in the launch configuration the benchmark times
-(all layers in one trie_attn_decode call; also one call per layer, as the benchmark's
-layer-by-layer figure), on sampled layers and the first steps."""
+"""GPU parity over whole runs at the full model shapes, in the launch configuration the
+benchmark times: scripted trie growth, attention over all layers in one trie_attn_decode
+call, the selection and the append fused (beam_topk_append), the benchmark's capacity.
+
+Every step of every run: node ids, parent slots, tokens, depths, masks, leaf slots and
+scores, n_nodes, n_live, lse and pair scores bit-exact against the oracle, and the top-b
+exact (the oracle's full ranking, or on the stress run's unsampled steps the exact check
+of ``verify_topb``).  Attention on sampled steps and layers (the oracle's fp64 path
+attention costs seconds per step at these sizes).  Also the layer-by-layer calls a model
+makes, on the first steps.
+"""
 import pytest
 
 import paper_2502_00085_amd.binding as B
@@ -10,41 +18,61 @@ from gpu_harness import Run, log
 pytestmark = pytest.mark.gpu
 
 
-def run_full(name, layers, steps, seed=0, extra_cap=4, layer_calls=None):
+def full_run(name, attn_layers, attn_steps, sort_steps=None, input_period=0, steps=None):
     w = synth.WORKLOADS[name]
-    cap = w.prompt_max + (steps + extra_cap) * w.beam_width
-    log(f"full-size {name}: layers {layers}, {steps} steps, capacity {cap}, layer calls {layer_calls}")
-    r = Run(w, seed, layers=layers, capacity=cap, layer_calls=layer_calls)
-    for s in range(steps):
-        errs, g = r.step()
-        log(f"  step {s + 1}: nodes {[st['n_nodes'] for st in g['state']][:4]} errors {len(errs)}")
+    S = steps or w.steps
+    cap = w.prompt_max + (S + 2) * w.beam_width  # (the benchmark's)
+    log(f"full run {name}: {S} steps, capacity {cap}, attention on layers {attn_layers} at steps "
+        f"{sorted(attn_steps)}, full sort {'every step' if sort_steps is None else sorted(sort_steps)}, "
+        f"input period {input_period}")
+    r = Run(w, 0, layers=attn_layers, capacity=cap, fused=True, input_period=input_period)
+    for s in range(1, S + 1):
+        full = sort_steps is None or s in sort_steps
+        errs, g = r.step(check_attn=s in attn_steps, full_sort=full)
+        if errs or s % 32 == 0 or s in attn_steps:
+            log(f"  step {s}: nodes {[st['n_nodes'] for st in g['state']][:4]} errors {len(errs)}")
         assert not errs, "\n".join(errs[:10])
     assert r.dec.status() == B.TD_OK
     r.dec.close()
 
 
 @pytest.mark.timeout(300)
-def test_llama8b_gqa_full_shape():
-    run_full("llama8b", [0, 15, 31], 4)
+def test_llama8b_gqa_whole_run():
+    full_run("llama8b", [0, 15, 31], {1, 2, 64, 128})
+
+
+@pytest.mark.timeout(300)
+def test_phi35_mha_whole_run():
+    full_run("phi35", [0, 15, 31], {1, 2, 64, 128})
+
+
+@pytest.mark.timeout(400)
+def test_mistral24b_sliding_window_whole_run():
+    # step 1 attends only to the last 4096 prompt nodes, then 4097 prompt nodes are evicted,
+    # then about one per step
+    full_run("mistral24b", [0, 39], {1, 2, 128, 256})
+
+
+@pytest.mark.timeout(600)
+def test_stress_sixteen_tries_whole_run():
+    # 16 tries x 16 beams x 128,256 logits per step: the full ranking on 8 sampled steps,
+    # the exact top-b check on the others; inputs of 16 steps reused in turn (as the
+    # benchmark runs this workload), the trie growth drawn fresh every step
+    full_run("stress", [0, 31], {1, 2, 256, 512}, sort_steps={1, 2, 3, 64, 128, 256, 384, 512},
+             input_period=16)
 
 
 @pytest.mark.timeout(300)
 def test_llama8b_one_layer_calls_full_shape():
     # the layer-by-layer order a model uses: 32 calls per step, each splitting its nodes
-    run_full("llama8b", [0, 31], 3, layer_calls=list(range(33)))
-
-
-@pytest.mark.timeout(300)
-def test_phi35_mha_full_shape():
-    run_full("phi35", [0, 31], 3)
-
-
-@pytest.mark.timeout(400)
-def test_mistral24b_sliding_window_full_shape():
-    # step 1 attends only to the last 4096 prompt nodes, then 4097 prompt nodes are evicted
-    run_full("mistral24b", [0, 39], 3)
-
-
-@pytest.mark.timeout(400)
-def test_stress_sixteen_tries_full_shape():
-    run_full("stress", [0, 31], 2)
+    w = synth.WORKLOADS["llama8b"]
+    steps = 3
+    cap = w.prompt_max + (steps + 4) * w.beam_width
+    log(f"full-size llama8b one-layer calls: {steps} steps, capacity {cap}")
+    r = Run(w, 0, layers=[0, 31], capacity=cap, layer_calls=list(range(33)))
+    for s in range(steps):
+        errs, g = r.step()
+        log(f"  step {s + 1}: nodes {[st['n_nodes'] for st in g['state']]} errors {len(errs)}")
+        assert not errs, "\n".join(errs[:10])
+    assert r.dec.status() == B.TD_OK
+    r.dec.close()

@@ -274,3 +274,17 @@ def test_two_row_blocks_several_tries_without_splits():
 def test_smallest_vocabulary(mode):
     # V = b: at step 1 every candidate is selected; afterwards b of b * b
     run_case(small(n_layers=1, beam_width=4, vocab=4, steps=6), seed=50, mode=mode)
+
+
+@pytest.mark.parametrize("g", [1, 15])
+@pytest.mark.parametrize("layers,splits", [(2, None), (4, "1")])
+def test_thirty_beams_four_row_blocks(monkeypatch, g, layers, splits):
+    """b = 30 at G = 4: 120 query rows per KV head, four 32-row blocks with one WG each (the
+    launch shape of the 30-beam collection measurement).  The row blocks of a node range
+    are grouped onto one XCD; with the built-in node splits (2 layers) and with none (4
+    layers, TD_ATTN_SPLITS = 1)."""
+    if splits:
+        monkeypatch.setenv("TD_ATTN_SPLITS", splits)
+    w = small(name="b30", n_layers=layers, n_q_heads=8, n_kv_heads=2, beam_width=30, steps=8, gc_interval=g,
+              prompt_min=150, prompt_max=150)
+    run_case(w, seed=61 + g)
