@@ -254,6 +254,31 @@ td_status beam_topk_append(td_ctx* ctx, const float* d_logits, int32_t* d_sel_pa
                            const int32_t* d_pair_parent, const int32_t* d_pair_token, float* d_pair_score,
                            hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): the selection of beam_logsoftmax_topk
+ * without a context.  It calls no hipMalloc / hipFree (nor anything that allocates) and
+ * needs no td_create: its workspace is a fixed array in the library's device memory,
+ * one copy per GPU, held until the process ends (2,232,576 bytes; its address is taken
+ * once per device, on the first call made with that device current).
+ * Inputs, all device memory: d_logits [T][b][V] fp32 (rows >= n_live not read);
+ * d_n_live [T] int32, each in [1, b]; d_leaf_score [T][b] fp32, the live beams'
+ * cumulative scores.  Outputs as beam_logsoftmax_topk: d_sel_parent, d_sel_token,
+ * d_sel_score, d_sel_logprob [T][b] in rank order, d_lse [T][b] (may be NULL); the same
+ * arithmetic and order, bit for bit.  No end-of-sequence handling, no pairs, no trie.
+ * d_status (2 int32, may be NULL) receives 0, or TD_EINVAL in [0] when a trie's n_live is
+ * outside [1, b] (that trie's selection is then unspecified) or a live row has no finite
+ * logit (see beam_logsoftmax_topk); it is cleared by each call, in stream order.
+ * Limits, checked on the host before any launch (TD_EINVAL / TD_EUNSUPPORTED, with a
+ * message from td_error_string(NULL)): n_tries <= 128, beam_width in [1, 64],
+ * b * ceil(V / 4096) <= 2048 and n_tries * b * ceil(V / 4096) <= 8192 (Llama-3's
+ * vocabulary: up to 8 tries of 32 beams, or 16 of 16).
+ * Every call on one GPU uses that GPU's one workspace: calls on different streams that
+ * may overlap race and give wrong results; order them on one stream.  Asynchronous. */
+td_status beam_topk_static(int32_t n_tries, int32_t beam_width, int32_t vocab, const float* d_logits,
+                           const int32_t* d_n_live, const float* d_leaf_score, int32_t* d_sel_parent,
+                           int32_t* d_sel_token, float* d_sel_score, float* d_sel_logprob, float* d_lse,
+                           int32_t* d_status, hipStream_t stream);
+
 /* The finished hypotheses of trie t (synchronises the device): *count (<= b) entries, best
  * first - norm, score, step (its length), parent (rank of the live beam it extends at
  * that step; with the selections of steps 1 .. step-1 this names its tokens) - and *done.

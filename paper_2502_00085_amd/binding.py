@@ -89,6 +89,7 @@ def lib() -> ctypes.CDLL:
         L.trie_tree_attn.argtypes = [vp, i32, i32, i32, vp, vp, vp, f32, vp]
         L.td_error_string.argtypes = [vp]
         L.td_error_string.restype = ctypes.c_char_p
+        L.beam_topk_static.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.td_status_name.argtypes = [i32]
         L.td_status_name.restype = ctypes.c_char_p
         L.bbs_create.argtypes = [ctypes.POINTER(BbsDesc), ctypes.POINTER(vp)]
@@ -103,7 +104,8 @@ def lib() -> ctypes.CDLL:
         L.bbs_error_string.argtypes = [vp]
         L.bbs_error_string.restype = ctypes.c_char_p
         for name in ("td_create", "td_destroy", "td_init_prompt", "trie_attn_decode",
-                     "beam_logsoftmax_topk", "trie_append_prune", "td_read_state", "td_load_state",
+                     "beam_logsoftmax_topk", "beam_topk_append", "beam_topk_static", "trie_append_prune",
+                     "td_read_state", "td_load_state",
                      "td_get_status", "td_set_kernel_events", "td_read_finished", "trie_tree_attn", "bbs_create", "bbs_destroy",
                      "bbs_init_prompt", "batch_beam_attn_decode", "batch_beam_logsoftmax_topk",
                      "batch_beam_reorder", "bbs_current_cache", "bbs_read_beams", "bbs_get_status"):
@@ -254,6 +256,22 @@ def beam_logsoftmax_topk(ctx, dims: Dims, logits, sel_parent, sel_token, sel_sco
         _ptr(sel_logprob, torch.float32, tb, "sel_logprob"), _ptr(lse, torch.float32, tb, "lse"),
         _ptr(pair_parent, torch.int32, tb, "pair_parent"), _ptr(pair_token, torch.int32, tb, "pair_token"),
         _ptr(pair_score, torch.float32, tb, "pair_score"), _stream(stream)))
+
+
+def beam_topk_static(n_tries, beam_width, vocab, logits, n_live, leaf_score, sel_parent, sel_token,
+                     sel_score, sel_logprob, lse=None, status=None, stream=None):
+    """beam_topk_static: the selection of beam_logsoftmax_topk without a context, on the
+    library's static device workspace (allocates nothing)."""
+    import torch
+    tb = n_tries * beam_width
+    st = lib().beam_topk_static(
+        int(n_tries), int(beam_width), int(vocab), _ptr(logits, torch.float32, tb * vocab, "logits"),
+        _ptr(n_live, torch.int32, n_tries, "n_live"), _ptr(leaf_score, torch.float32, tb, "leaf_score"),
+        _ptr(sel_parent, torch.int32, tb, "sel_parent"), _ptr(sel_token, torch.int32, tb, "sel_token"),
+        _ptr(sel_score, torch.float32, tb, "sel_score"), _ptr(sel_logprob, torch.float32, tb, "sel_logprob"),
+        _ptr(lse, torch.float32, tb, "lse"), _ptr(status, torch.int32, 2, "status"), _stream(stream))
+    if st != TD_OK:
+        raise TdError(st, td_error_string(None))
 
 
 def beam_topk_append(ctx, dims: Dims, logits, sel_parent, sel_token, sel_score, sel_logprob,

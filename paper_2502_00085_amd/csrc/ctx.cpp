@@ -71,6 +71,12 @@ td_status check_ready(td_ctx* c) {
 
 }  // namespace
 
+namespace td {
+// The message td_error_string(NULL) returns: a failed td_create, or a failed call that
+// has no context (beam_topk_static).
+void set_error_without_context(const char* msg) { g_create_err = msg; }
+}  // namespace td
+
 extern "C" {
 
 const char* td_status_name(int32_t s) {

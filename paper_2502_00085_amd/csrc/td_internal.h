@@ -130,6 +130,7 @@ hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_
                                   float* pair_score, bool append, hipStream_t st, hipEvent_t ev0,
                                   hipEvent_t ev1);
 int topb_max_chunk_lists();  // limit of b * lse_chunks per trie
+void set_error_without_context(const char* msg);
 hipError_t launch_append_prune(const DevState& s, const int32_t* sel_parent,
                                const int32_t* sel_token, const float* sel_score, hipStream_t st,
                                hipEvent_t ev0, hipEvent_t ev1);

@@ -24,6 +24,8 @@
 // scoring >= L lies in a sub-chunk whose best score is >= L: a hot one.
 // (Two launches instead of a last-arriving-WG merge: a device-scope fence costs an L2
 // writeback + invalidate per WG on this multi-XCD part.)
+#include <mutex>
+
 #include "trie_append.h"
 
 namespace td {
@@ -676,4 +678,109 @@ hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_
 
 int topb_max_chunk_lists() { return kMaxEntries; }
 
+// ---------------------------------------------------------------------------------------
+// beam_topk_static: the selection without a context, on a fixed device-resident workspace
+// ---------------------------------------------------------------------------------------
+namespace {
+
+// Workspace of beam_topk_static, one copy per GPU for the life of the process: the status
+// word and per-trie headers (n_live), then the chunk partials and sub-chunk keys of at
+// most kStaticLists (trie, row, chunk) lists.  Host code must not pass this name to a
+// kernel (it is a host-side stand-in): it uses the address hipGetSymbolAddress returns.
+constexpr int kStaticMaxTries = 128;
+constexpr int kStaticLists = 8192;
+constexpr size_t kStaticHdrOff = 256;
+constexpr size_t kStaticLseOff = kStaticHdrOff + kStaticMaxTries * sizeof(TrieHdr);      // 4,352
+constexpr size_t kStaticKeyOff = kStaticLseOff + (size_t)kStaticLists * 2 * sizeof(double);
+constexpr size_t kStaticBytes = kStaticKeyOff + (size_t)kStaticLists * 2 * kSub * sizeof(uint64_t);
+static_assert(kStaticLseOff % 256 == 0 && kStaticKeyOff % 256 == 0, "aligned regions");
+__device__ __align__(256) unsigned char scratch[kStaticBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Clears the status word, then writes each trie's n_live into its header (an n_live
+// outside [1, b] sets TD_EINVAL and becomes 0: that trie gets no candidates).  One block.
+__global__ void k_static_setup(TrieHdr* hdr, int32_t* status, const int32_t* n_live, int T, int b) {
+  if (threadIdx.x == 0) {
+    status[0] = 0;
+    status[1] = 0;
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < T; t += blockDim.x) {
+    int n = n_live[t];
+    if (n < 1 || n > b) {
+      set_status(status, kDevEinval);
+      n = 0;
+    }
+    TrieHdr h{};
+    h.n_live = n;
+    hdr[t] = h;
+  }
+}
+
+td_status static_fail(td_status st, const char* msg) {
+  set_error_without_context(msg);
+  return st;
+}
+
+}  // namespace
+
 }  // namespace td
+
+extern "C" td_status beam_topk_static(int32_t n_tries, int32_t beam_width, int32_t vocab, const float* d_logits,
+                                      const int32_t* d_n_live, const float* d_leaf_score, int32_t* d_sel_parent,
+                                      int32_t* d_sel_token, float* d_sel_score, float* d_sel_logprob, float* d_lse,
+                                      int32_t* d_status, hipStream_t st) {
+  using namespace td;
+  set_error_without_context("");
+  if (n_tries < 1 || beam_width < 1 || beam_width > kMaxBeam || vocab < beam_width)
+    return static_fail(TD_EINVAL, "need n_tries >= 1, beam_width in [1, 64], vocab >= beam_width");
+  if ((int64_t)vocab * beam_width >= (int64_t(1) << 31))
+    return static_fail(TD_EINVAL, "vocab * beam_width must be < 2^31");
+  if (!d_logits || !d_n_live || !d_leaf_score || !d_sel_parent || !d_sel_token || !d_sel_score || !d_sel_logprob)
+    return static_fail(TD_EINVAL, "logits, n_live, leaf scores and the four selection outputs are required");
+  const int nch = (vocab + kLseChunk - 1) / kLseChunk;
+  if ((int64_t)beam_width * nch > kMaxEntries)
+    return static_fail(TD_EUNSUPPORTED, "beam_width * ceil(vocab / 4096) must be <= 2048");
+  if (n_tries > kStaticMaxTries || (int64_t)n_tries * beam_width * nch > kStaticLists)
+    return static_fail(TD_EUNSUPPORTED,
+                       "beyond the static workspace: n_tries <= 128 and n_tries * beam_width * ceil(vocab / 4096) <= 8192");
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return static_fail(TD_EHIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= kMaxDevices) return static_fail(TD_EUNSUPPORTED, "device index beyond 63");
+  unsigned char* base = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+      // this device's copy of the array (the device is current)
+      void* ptr = nullptr;
+      e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !ptr) return static_fail(TD_EHIP, "hipGetSymbolAddress of the static workspace failed");
+      g_scratch[dev] = ptr;
+    }
+    base = static_cast<unsigned char*>(g_scratch[dev]);
+  }
+  DevState s{};
+  s.T = n_tries;
+  s.b = beam_width;
+  s.V = vocab;
+  s.eos = -1;
+  s.lse_chunks = nch;
+  s.topk_half = (size_t)n_tries * beam_width * nch * kSub;
+  s.hdr = reinterpret_cast<TrieHdr*>(base + kStaticHdrOff);
+  s.status = d_status ? d_status : reinterpret_cast<int32_t*>(base);
+  s.leaf_score = const_cast<float*>(d_leaf_score);
+  s.lse_part = reinterpret_cast<double*>(base + kStaticLseOff);
+  s.topk_keys = reinterpret_cast<uint64_t*>(base + kStaticKeyOff);
+  hipLaunchKernelGGL(k_static_setup, dim3(1), dim3(kStaticMaxTries), 0, st, s.hdr, s.status, d_n_live, n_tries,
+                     beam_width);
+  e = hipGetLastError();
+  if (e == hipSuccess)
+    e = launch_logsoftmax_topk(s, d_logits, d_sel_parent, d_sel_token, d_sel_score, d_sel_logprob, d_lse, nullptr,
+                               nullptr, nullptr, false, st, nullptr, nullptr);
+  if (e != hipSuccess) return static_fail(TD_EHIP, "beam_topk_static launch failed");
+  return TD_OK;
+}

@@ -165,3 +165,23 @@ def test_binding_refuses_to_run_without_the_library(monkeypatch):
     monkeypatch.setattr(B, "LIB_PATH", "/nonexistent/libtriedecode.so")
     with pytest.raises(RuntimeError, match="missing"):
         B.lib()
+
+
+@pytest.mark.parametrize("T,b,V,want", [(0, 8, 1000, "TD_EINVAL"), (1, 0, 1000, "TD_EINVAL"), (1, 65, 1000, "TD_EINVAL"),
+                                        (1, 8, 4, "TD_EINVAL"), (129, 1, 1000, "TD_EUNSUPPORTED"),
+                                        (9, 32, 128256, "TD_EUNSUPPORTED"), (1, 64, 200000, "TD_EUNSUPPORTED")])
+def test_static_selection_limits_are_checked_on_the_host(T, b, V, want):
+    """beam_topk_static rejects sizes beyond its fixed workspace (and invalid ones) before
+    touching the device: here with dummy pointers and no GPU."""
+    L = B.lib()
+    p = ctypes.c_void_p(0x10000)
+    st = L.beam_topk_static(T, b, V, p, p, p, p, p, p, p, None, None, None)
+    assert st == getattr(B, want), L.td_status_name(st)
+    assert L.td_error_string(None).decode()
+
+
+def test_static_selection_needs_its_buffers():
+    L = B.lib()
+    p = ctypes.c_void_p(0x10000)
+    assert L.beam_topk_static(1, 8, 1000, None, p, p, p, p, p, p, None, None, None) == B.TD_EINVAL
+    assert L.beam_topk_static(1, 8, 1000, p, p, p, p, p, p, None, None, None, None) == B.TD_EINVAL
