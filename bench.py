@@ -31,18 +31,20 @@ import synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
 
-# HBM traffic of the attention kernel measured by rocprofv3 (separate --pmc FETCH_SIZE and
-# --pmc WRITE_SIZE runs of `bench.py --profile-only --no-batch-baseline --no-tree
-# --copy-ref-mib 512`, llama8b), scaled by what the same counters read for a plain 512 MiB
-# device copy (fetch x 2.0, write x 1.0), per launch for the 64 graph-replayed launches at
-# the step-K/2 trie: the launches `roofline.achieved` is timed on.  Valid only for the
-# kernel sources it was measured on: reported as null once their digest (comments
-# stripped) differs.
+# HBM traffic of the attention kernel measured by rocprofv3: separate --pmc FETCH_SIZE and
+# --pmc WRITE_SIZE runs of the command the record names, scaled by what the same counters
+# read for a plain device copy of known size (the factors), per dispatch of the launches
+# the cold and warm attention figures are timed on.  Reported for a run as bytes per
+# attended node (the record's traffic less its query/output bytes, over its nodes) times
+# the run's attended nodes, plus the run's query/output bytes.  Valid only for the kernel
+# sources it was measured on: null once their digest (comments stripped) differs.
 ATTN_TRAFFIC = {
     "workload": "llama8b",
-    "sources_sha256": "09aa57105a6a520fc0223222b71c87f2a896f5893d3085cca6a631a329bc5264",
-    "bytes_per_launch": 283743804,             # 2.0 x FETCH_SIZE + 1.0 x WRITE_SIZE
-    "algorithmic_bytes_per_launch": 283377664,  # unique K+V rows, q, out
+    "profile": "profiles/k_attn_mfma_llama8b_hbm_traffic.md",
+    "sources_sha256": "3319b2134f645d21d21ef29632c736eb4a2593c341a060cad24bede59a5f2d62",
+    "bytes_per_launch": 275850036,    # 2.0 x 133,679.97 KiB FETCH_SIZE + 1.0 x 2,048 KiB WRITE_SIZE
+    "nodes_per_launch": 2070,         # attended nodes of the profiled (step-10) trie
+    "qo_bytes_per_launch": 4194304,   # queries + outputs of the profiled launch
 }
 ATTN_SOURCES = ("attn_mfma.hip", "attn_common.h", "td_internal.h")
 
@@ -77,6 +79,10 @@ def parse():
     p.add_argument("--profile-only", action="store_true",
                    help="run warmup + timed steps only (for rocprofv3), no CPU baseline")
     p.add_argument("--attn-reps", type=int, default=32, help="launches in the attention timing graph")
+    p.add_argument("--cold-reps", type=int, default=16,
+                   help="attention launches timed after the last-level cache is cleared (median)")
+    p.add_argument("--timed-runs", type=int, default=5,
+                   help="timed runs of the K steps (each from the same initial state); the median is reported")
     p.add_argument("--copy-ref-mib", type=int, default=0,
                    help="also run one plain device copy of this many MiB (reference for HBM counters)")
     p.add_argument("--unfused", action="store_true",
@@ -266,23 +272,27 @@ def gpu_bench(args, w, K):
         except Exception as e:  # graph capture unavailable: fall back to eager launches
             log(f"[bench] graph capture failed ({e}); timing eager launches")
             mode, graph = "eager", None
-    # the timed region: exactly K decode steps
-    bench.init()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    if graph is not None:
-        graph.replay()
-    else:
-        for i in range(K):
-            bench.step(i, stream)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    # the timed region: exactly K decode steps, bracketed by synchronisations; run
+    # `timed_runs` times from the same initial state (re-initialised between runs, outside
+    # the timed region), the median reported
+    run_s = []
+    for _ in range(args.timed_runs):
+        bench.init()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        if graph is not None:
+            graph.replay()
+        else:
+            for i in range(K):
+                bench.step(i, stream)
+        torch.cuda.synchronize()
+        run_s.append(time.perf_counter() - t0)
     status = bench.dec.status()
     if status != 0:
         raise RuntimeError(f"device status {status} after the timed run")
     finished = [bench.dec.read_finished(t) for t in range(w.n_tries)] if args.eos >= 0 else None
     attn_graph_ms, attn_graph_nodes = attn_graph_time(bench, K, args.attn_reps)
-    attn_cold_ms = attn_cold_time(bench, max(4, args.attn_reps // 4))
+    attn_cold_ms = attn_cold_time(bench, args.cold_reps)
     per_layer_ms = attn_per_layer_time(bench, max(4, args.attn_reps // 4))
     copy_gbs = device_copy_gbs()
     tree = None if args.no_tree or w.dtype != "bf16" else tree_prefill_time(bench, K, 8)
@@ -291,7 +301,8 @@ def gpu_bench(args, w, K):
     collects = np.array([bench.collects(i) for i in range(K)])
     bench.dec.close()
     batch = None if args.no_batch_baseline else batch_bench(bench, K, args.warmup)
-    return dict(mode=mode, seconds=t1 - t0, eager_seconds=eager_s, attn_ms=attn_ms, nodes=nodes,
+    return dict(mode=mode, seconds=float(np.median(run_s)), run_seconds=run_s, eager_seconds=eager_s,
+                attn_ms=attn_ms, nodes=nodes,
                 attn_graph_ms=attn_graph_ms, attn_graph_nodes=attn_graph_nodes, phase_ms=phase_ms,
                 attn_cold_ms=attn_cold_ms, per_layer_ms=per_layer_ms, copy_gbs=copy_gbs,
                 collects=collects, stored=bench.stored, batch=batch, finished=finished, tree=tree,
@@ -457,19 +468,22 @@ def attn_graph_time(bench, K, reps):
         raise RuntimeError(bench.B.td_error_string(ctx))
     graph.replay()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    graph.replay()
-    e1.record()
-    torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / reps, nodes
+    ms = []
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1) / reps)
+    return float(np.median(ms)), nodes
 
 
 def attn_cold_time(bench, reps):
     """The same launch as attn_graph_time (the trie it leaves: nothing pending), with the
     last-level cache cleared first: before each launch a 1 GiB buffer is read (four times
-    the 256 MB cache), then the kernel alone is timed by kernel-timestamp events.  Returns
-    the mean ms per launch."""
+    the 256 MB cache), then the kernel alone is timed by kernel-timestamp events on the
+    stream it runs on.  Returns the median ms per launch over `reps` launches."""
     import torch
     stream = torch.cuda.current_stream().cuda_stream
     L, ctx, w = bench.B.lib(), bench.dec.ctx, bench.w
@@ -486,7 +500,7 @@ def attn_cold_time(bench, reps):
         ms.append(ev.elapsed_ms())
     ev.close()
     del flush
-    return float(np.mean(ms))
+    return float(np.median(ms))
 
 
 def attn_per_layer_time(bench, reps):
@@ -599,16 +613,11 @@ def tree_prefill_time(bench, K, reps):
     return e0.elapsed_time(e1) / reps, int(sum(int(bench.dec.read_state(t)["n_nodes"]) for t in range(w.n_tries))), flops
 
 
-def cpu_baseline(w, seed, budget_s):
+def oracle_rate(w, seed, budget_s):
     """The CPU oracle on the same workload: decode steps from the start, all layers, until
-    the time budget is used; steps/s over the completed steps."""
+    the time budget is used (at least one step).  Returns (steps/s, steps, prompt setup s)."""
     import oracle.decode as odec
     import oracle.trie as otrie
-    try:
-        import threadpoolctl
-        blas_threads = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
-    except Exception:
-        blas_threads = 1
     scale = 1.0 / float(np.sqrt(w.head_dim))
     t_setup = time.time()
     plens = synth.prompt_lengths(w, seed)
@@ -630,10 +639,33 @@ def cpu_baseline(w, seed, budget_s):
         done += 1
         if spent >= budget_s:
             break
-    return {"value": done / spent, "unit": "steps/s", "cores": int(blas_threads), "kind": "oracle",
+    return done / spent, done, setup
+
+
+def cpu_baseline(w, seed, budget_s):
+    """The oracle timed on this host's cores: with the BLAS threads NumPy uses by default
+    (its matrix products; the Python loop itself is one thread), and with one thread."""
+    affinity = len(os.sched_getaffinity(0))
+    try:
+        import threadpoolctl
+        blas_threads = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
+    except Exception:
+        threadpoolctl, blas_threads = None, 1
+    rate, done, setup = oracle_rate(w, seed, budget_s)
+    single = None
+    if threadpoolctl is not None:
+        with threadpoolctl.threadpool_limits(1):
+            r1, d1, _ = oracle_rate(w, seed, budget_s / 3)
+        single = {"value": r1, "steps": d1}
+    return {"value": rate, "unit": "steps/s", "cores": int(blas_threads), "kind": "oracle",
             "sample": f"first {done} decode steps of the same workload (all {w.n_layers} layers, "
-                      f"{w.n_tries} trie(s)), prompt setup {setup:.1f}s excluded; python is "
-                      f"single-threaded, cores = BLAS threads"}
+                      f"{w.n_tries} trie(s), fp64 path attention for every beam), prompt setup {setup:.1f}s "
+                      f"excluded; cores = the BLAS threads of NumPy's matrix products, the Python loop is "
+                      f"single-threaded",
+            "affinity_cores": affinity, "blas_threads": int(blas_threads),
+            "single_thread_value": None if single is None else single["value"],
+            "single_thread_sample": None if single is None else f"first {single['steps']} decode steps, "
+                                                               f"BLAS limited to 1 thread"}
 
 
 def main():
@@ -653,18 +685,23 @@ def main():
     ms_per_step = r["seconds"] * 1e3 / K
     kv_bytes = r["nodes"].sum(axis=1).astype(np.float64) * w.node_bytes  # per step, all tries
     attn_s = r["attn_ms"] / 1e3
-    graph_bytes = float(sum(r["attn_graph_nodes"])) * w.node_bytes
-    achieved = graph_bytes / (r["attn_graph_ms"] / 1e3) / 1e9
+    graph_nodes = float(sum(r["attn_graph_nodes"]))
+    graph_bytes = graph_nodes * w.node_bytes
+    warm = graph_bytes / (r["attn_graph_ms"] / 1e3) / 1e9
+    cold = graph_bytes / (r["attn_cold_ms"] / 1e3) / 1e9
     traffic = None
     if (ATTN_TRAFFIC["workload"] == w.name and ATTN_TRAFFIC["bytes_per_launch"] is not None
             and ATTN_TRAFFIC["sources_sha256"] == attn_sources_digest()):
-        traffic = ATTN_TRAFFIC["bytes_per_launch"]
+        per_node = (ATTN_TRAFFIC["bytes_per_launch"] - ATTN_TRAFFIC["qo_bytes_per_launch"]) / \
+            ATTN_TRAFFIC["nodes_per_launch"]
+        traffic = int(round(per_node * graph_nodes + r["qo_bytes"]))
     out = {
         "metric": "trie-decode steps/s and achieved HBM GB/s (% of peak) at Llama-8B GQA shape, b=8",
         "value": round(K / r["seconds"], 2),
         "unit": "steps/s",
         "n_gpus": 1, "steps": K, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
+        "timed_runs_ms_per_step": [round(x * 1e3 / K, 5) for x in r["run_seconds"]],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "layers": w.n_layers, "q_heads": w.n_q_heads,
@@ -675,21 +712,24 @@ def main():
                    "growth": f"scripted, parent rank ~ (r+1)^-{w.alpha}", "launch": r["mode"],
                    "step_calls": "trie_attn_decode, beam_logsoftmax_topk, trie_append_prune" if args.unfused
                    else "trie_attn_decode, beam_topk_append"},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+        "roofline": {"bound": "hbm", "achieved": round(cold, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(cold / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": "k_attn_mfma (trie_attn_decode, all layers, one launch)",
-                     "attn_us_per_launch": round(r["attn_graph_ms"] * 1e3, 2),
+                     "timing": f"unique trie K/V bytes of one launch at the step-{K // 2} trie over the median "
+                               f"duration of {args.cold_reps} launches, each after a 1 GiB read has cleared the "
+                               f"256 MB last-level cache, timed by kernel-timestamp events on the launch stream",
+                     "attn_us_llc_cold": round(r["attn_cold_ms"] * 1e3, 2),
                      "unique_kv_bytes_per_launch": int(graph_bytes),
                      "algorithmic_bytes_per_launch": int(graph_bytes) + r["qo_bytes"],
-                     "timing": f"{args.attn_reps} back-to-back launches at the step-{K // 2} trie, "
-                               f"graph-replayed between events",
+                     "traffic_source": (ATTN_TRAFFIC["profile"] + ", per attended node, scaled to this trie")
+                     if traffic is not None else "no counter record for these kernel sources",
+                     "achieved_warm": round(warm, 1), "frac_warm": round(warm / HBM_PEAK_GBS, 4),
+                     "attn_us_warm": round(r["attn_graph_ms"] * 1e3, 2),
+                     "warm": f"the same launch repeated back to back ({args.attn_reps} per graph replay, median "
+                             f"of 5 replays): part of the K/V can stay in the last-level cache",
                      "attn_us_eager_events_mean": round(float(attn_s.mean() * 1e6), 2),
-                     "attn_us_llc_cold": round(r["attn_cold_ms"] * 1e3, 2),
-                     "achieved_llc_cold": round(graph_bytes / (r["attn_cold_ms"] / 1e3) / 1e9, 1),
-                     "llc_cold": "the same launch with the 256 MB last-level cache cleared before it "
-                                 "(a 1 GiB read), timed alone by kernel-timestamp events",
                      "device_copy_gbs": round(r["copy_gbs"], 1),
-                     "frac_of_device_copy": round(achieved / r["copy_gbs"], 4),
+                     "frac_of_device_copy": round(cold / r["copy_gbs"], 4),
                      "device_copy": "a plain 1 GiB device-to-device copy (torch copy_), read + write bytes "
                                     "over time, on the same GPU in the same run",
                      "attn_us_per_step_layer_calls": round(r["per_layer_ms"] * 1e3, 2),
