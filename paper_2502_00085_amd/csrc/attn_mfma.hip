@@ -26,6 +26,8 @@
 // with max/sum rescaling through LDS; node splits over WGs write partials that a second
 // launch merges (attn_combine.hip).  Template variants: TREE (rows are arbitrary query
 // nodes) and RB = 2 (one WG over two 32-row blocks).
+#include <type_traits>
+
 #include "attn_common.h"
 #include "mfma_tile.h"
 
@@ -185,7 +187,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     mt0 = lane < nmoves ? mv[lane].x - base : 0;
     mt1 = lane + 64 < nmoves ? mv[lane + 64].x - base : 0;
   }
-  auto table = [&](int k) -> int {  // source of moved row k < kRegMoves (all lanes active)
+  auto table = [&](int k) __attribute__((always_inline)) -> int {  // source of moved row k < kRegMoves (all lanes active)
     const int a0 = __builtin_amdgcn_ds_bpermute((k & 63) << 2, mt0);
     const int a1 = __builtin_amdgcn_ds_bpermute((k & 63) << 2, mt1);
     return k < 64 ? a0 : a1;
@@ -226,17 +228,33 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   // physical chunk p % CPR.  K rows are rotated by one chunk per row (the MFMA-layout
   // reads of 16 consecutive rows then hit 16 different bank groups); V rows by one
   // 64-byte block per row (transposed reads of 4 consecutive rows use 4 bank groups).
-  // koff / voff: element offset, inside the row, of the logical chunk this lane loads.
-  auto tile_geom = [&](int i, int ln, int& row, int& ko, int& vo) {
+  // ko / vo: element offset, inside the row, of the logical chunk this lane loads.
+  auto tile_geom = [&](int i, int ln, int& row, int& ko, int& vo) __attribute__((always_inline)) {
     const int p = 64 * i + ln;
     const int pc = p % C::CPR;
     row = p / C::CPR;
     ko = (pc + C::CPR - row % C::CPR) % C::CPR * 8;
     vo = (pc + C::CPR - 4 * (row % C::NBLK)) % C::CPR * 8;
   };
-  int vrow[C::VINST], koff[C::VINST], voff[C::VINST];
+  // The common tile is 32 consecutive pool rows from its first node: this lane's element
+  // offset inside them, K and V, for each load, kept in registers by the one-row-block
+  // decode kernel (the others, short of registers, recompute the geometry per load).
+  constexpr bool kOfsRegs = !TREE && RB == 1;
+  int kofs[kOfsRegs ? C::VINST : 1], vofs[kOfsRegs ? C::VINST : 1];
+  if constexpr (kOfsRegs) {
 #pragma unroll
-  for (int i = 0; i < C::VINST; ++i) tile_geom(i, lane, vrow[i], koff[i], voff[i]);
+    for (int i = 0; i < C::VINST; ++i) {
+      int vr, ko, vo;
+      tile_geom(i, lane, vr, ko, vo);
+      kofs[i] = vr * D + ko;
+      vofs[i] = vr * D + vo;
+    }
+  }
+  auto geom = [&](int i, int& vr, int& ko, int& vo) __attribute__((always_inline)) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));  // (keeps the geometry from being hoisted into registers)
+    tile_geom(i, ln, vr, ko, vo);
+  };
   // this lane's K operand chunks for the 32x32x16 steps: row col, logical chunk
   // hh * CPR / 2 + t, rotated by col
   int kread[C::KSTEPS];
@@ -252,23 +270,44 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   // gathers a lane's 16 nodes from them by lane permutes)
   int tdep = 0;
   uint64_t tmk = 0;
-  auto issue = [&](int tile) {
+  // KPART: the K rows of a tile, else its V rows
+  auto issue_part = [&](int tile, auto kpart) __attribute__((always_inline)) {
+    constexpr bool KP = decltype(kpart)::value;
     const int tb = n0 + tile * 32;
     const bool full = tb + 32 <= n1;
     const bool any_moved = tb + 32 > first_moved && tb < moved_end;  // wave-uniform
-    if constexpr (TREE) {
+    if constexpr (KP) {
       const int nn = min(tb + col, n1 - 1);
-      tdep = depthp[nn];
-      tmk = maskp[nn];
+      if constexpr (TREE) {
+        tdep = depthp[nn];
+        tmk = maskp[nn];
+      } else if (tb + 32 > n1 || tb + 32 > h.n_shared) {
+        tmk = maskp[nn];  // (a tile that needs the ancestor bits: one coalesced load)
+      }
+    }
+    unsigned char* dst = KP ? kbuf : vbuf;
+    if (full && tb + 32 <= leaf0 && !any_moved) {
+      // every row of the tile is a pool row in place: one add per load
+      const __bf16* base = (KP ? kpool : vpool) + (size_t)tb * D;
+#pragma unroll
+      for (int i = 0; i < C::VINST; ++i) {
+        int o;
+        if constexpr (kOfsRegs) {
+          o = KP ? kofs[i] : vofs[i];
+        } else {
+          int vr, ko, vo;
+          geom(i, vr, ko, vo);
+          o = vr * D + (KP ? ko : vo);
+        }
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(base + o),
+                                         (__attribute__((address_space(3))) void*)(dst + i * 1024), 16, 0, NT ? 2 : 0);
+      }
+      return;
     }
 #pragma unroll
     for (int i = 0; i < C::VINST; ++i) {
-      int vr = vrow[i], ko = koff[i], vo = voff[i];
-      if constexpr (RB == 2) {  // (recomputed per call: registers are short with two row blocks)
-        int ln = lane;
-        asm volatile("" : "+v"(ln));
-        tile_geom(i, ln, vr, ko, vo);
-      }
+      int vr, ko, vo;
+      geom(i, vr, ko, vo);
       const int nv = full ? tb + vr : min(tb + vr, n1 - 1);
       const bool leaf = nv >= leaf0;
       int src = nv;
@@ -283,13 +322,14 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
         }
       }
       const size_t kr = leaf ? (size_t)(nv - leaf0) * leaf_stride : (size_t)src * D;
-      const __bf16* ks = (leaf ? knew : kpool) + kr + ko;
-      const __bf16* vs = (leaf ? vnew : vpool) + kr + vo;
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)ks,
-                                       (__attribute__((address_space(3))) void*)(kbuf + i * 1024), 16, 0, kTileCpol);
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)vs,
-                                       (__attribute__((address_space(3))) void*)(vbuf + i * 1024), 16, 0, kTileCpol);
+      const __bf16* sp = KP ? (leaf ? knew : kpool) + kr + ko : (leaf ? vnew : vpool) + kr + vo;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)sp,
+                                       (__attribute__((address_space(3))) void*)(dst + i * 1024), 16, 0, NT ? 2 : 0);
     }
+  };
+  auto issue = [&](int tile) __attribute__((always_inline)) {
+    issue_part(tile, std::true_type{});
+    issue_part(tile, std::false_type{});
   };
 
   const float scale = a.scale_log2;
@@ -356,7 +396,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     const int tile = wave + NW * k;
     const int tb = n0 + tile * 32;
     __builtin_amdgcn_s_waitcnt(kWaitVmAll);  // this tile's K and V rows have landed in LDS
-    const int cdep = tdep;  // (TREE) this tile's node depth and mask of lane % 32
+    const int cdep = tdep;  // this tile's node depth (TREE) and mask of lane % 32
     const uint64_t cmk = tmk;
     // all LDS reads of the tile first: K operands (MFMA layout) and V^T operands (two
     // transposed reads per 16 nodes x 32 d, giving this lane column d = 32 dt + col at 4
@@ -441,12 +481,16 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[v] = (vis >> v) & 1u ? acc[v] : -INFINITY;
       } else if (tb + 32 > n1 || tb + 32 > h.n_shared) {
+        // the ancestor mask of tile node i was loaded with the tile by lane i
+        const int mlo = (int)(uint32_t)cmk, mhi = (int)(uint32_t)(cmk >> 32);
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int n = tb + 8 * (v >> 2) + 4 * hh + (v & 3);
-          bool ok = n < n1;
-          if (ok && n >= h.n_shared) ok = (maskp[n] >> beam_bit[rbk]) & 1ull;
-          if (!ok) acc[v] = -INFINITY;
+          const int i = 8 * (v >> 2) + 4 * hh + (v & 3);
+          const uint32_t lo_ = (uint32_t)__builtin_amdgcn_ds_bpermute(i << 2, mlo);
+          const uint32_t hi_ = (uint32_t)__builtin_amdgcn_ds_bpermute(i << 2, mhi);
+          const uint32_t word = beam_bit[rbk] < 32 ? lo_ : hi_;
+          const bool ok = (tb + i < n1) & ((tb + i < h.n_shared) | ((word >> (beam_bit[rbk] & 31)) & 1u));
+          acc[v] = ok ? acc[v] : -INFINITY;
         }
       }
       float tmax = acc[0];

@@ -25,6 +25,8 @@ __device__ inline int phys_chunk(int r, int c) {
 // s_waitcnt immediates (gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14,
 // expcnt in 6:4, lgkmcnt in 11:8)
 constexpr int kWaitVmAll = 0 | (7 << 4) | (15 << 8);                // vmcnt(0)
+// vmcnt(n), 0 <= n < 64: at most n vector memory operations of this wave outstanding
+constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 constexpr int kWaitLgkmAll = 15 | (3 << 14) | (7 << 4) | (0 << 8);  // lgkmcnt(0)
 
 }  // namespace td
