@@ -258,7 +258,7 @@ td_status beam_topk_append(td_ctx* ctx, const float* d_logits, int32_t* d_sel_pa
  * serving loops, harnesses that forbid hipMalloc): the selection of beam_logsoftmax_topk
  * without a context.  It calls no hipMalloc / hipFree (nor anything that allocates) and
  * needs no td_create: its workspace is a fixed array in the library's device memory,
- * one copy per GPU, held until the process ends (2,232,576 bytes; its address is taken
+ * one copy per GPU, held until the process ends (2,236,672 bytes; its address is taken
  * once per device, on the first call made with that device current).
  * Inputs, all device memory: d_logits [T][b][V] fp32 (rows >= n_live not read);
  * d_n_live [T] int32, each in [1, b]; d_leaf_score [T][b] fp32, the live beams'

@@ -165,8 +165,10 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   constexpr int kQBytes = RB == 2 ? RB * kRows * D * 2 : 0;
   constexpr int kMove0 = C::MOVE0 + kQBytes, kMoveLds = C::MOVE_LDS - kQBytes;
   static_assert(kMoveLds > 0, "LDS for the staging area");
-  const int nmoves = a.moves ? s.n_moves[u.t] : 0;
-  const int first_moved = nmoves > 0 ? s.moves[(size_t)u.t * s.cap].y - base : INT_MAX;
+  // (the count and the first destination come with the header: no dependent loads before
+  // the first tile)
+  const int nmoves = a.moves ? h.n_moves : 0;
+  const int first_moved = nmoves > 0 ? h.first_moved : INT_MAX;
   // The pending leaves' rows of a WG whose range holds them are staged the same way (from
   // k_new / v_new), ahead of the moved rows, unless the moved rows are copied through the
   // same LDS at the start or the end.

@@ -90,7 +90,7 @@ __global__ __launch_bounds__(256) void k_bbs_meta(BbsState s, const int32_t* sel
   h.n_shared = len + 1;
   h.leaf_depth = len;
   h.next_id = 0;
-  h.step = h.pad1 = 0;
+  h.step = h.n_moves = h.first_moved = 0;
   s.chain[(size_t)t * b + j] = h;
   if (j == 0) {
     TrieHdr r = s.req[t];

@@ -548,7 +548,8 @@ td_status td_load_state(td_ctx* c, int32_t trie, const td_state* in) {
   h.leaf_depth = in->depth[N - 1];
   h.next_id = in->next_id;
   h.step = in->step;
-  h.pad1 = 0;
+  h.n_moves = 0;
+  h.first_moved = 0;
   if (e == hipSuccess) e = hipMemcpy(s.hdr + trie, &h, sizeof h, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemset(s.fin_count + trie, 0, sizeof(int32_t));
   if (e == hipSuccess) e = hipMemset(s.fin_done + trie, 0, sizeof(int32_t));

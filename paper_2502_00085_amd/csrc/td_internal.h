@@ -10,7 +10,7 @@
 namespace td {
 
 // Per-trie header kept in device memory (one per trie).
-struct TrieHdr {
+struct alignas(16) TrieHdr {
   int32_t n_nodes;     // stored nodes N
   int32_t base;        // physical slot of logical slot 0
   int32_t n_live;      // live leaves (last n_live logical slots, rank order)
@@ -19,8 +19,13 @@ struct TrieHdr {
   int32_t leaf_depth;  // depth D of every live leaf
   int32_t next_id;     // id given to the next appended node of rank 0
   int32_t step;        // appends so far (the next selection is step + 1)
-  int32_t pad1;
+  int32_t n_moves;     // K/V rows the last append's collection moved (0: none, or copied
+                       //   already as far as the header knows; also in DevState::n_moves)
+  int32_t first_moved; // logical slot of the first moved row's destination (n_moves > 0);
+                       //   the destinations are consecutive
+  int32_t pad[7];
 };
+static_assert(sizeof(TrieHdr) == 64, "one 64-byte header per trie");
 
 // Device-side pointers of one context.  Node arrays are [T][cap], indexed by physical slot.
 struct DevState {

@@ -690,7 +690,7 @@ namespace {
 constexpr int kStaticMaxTries = 128;
 constexpr int kStaticLists = 8192;
 constexpr size_t kStaticHdrOff = 256;
-constexpr size_t kStaticLseOff = kStaticHdrOff + kStaticMaxTries * sizeof(TrieHdr);      // 4,352
+constexpr size_t kStaticLseOff = kStaticHdrOff + kStaticMaxTries * sizeof(TrieHdr);      // 8,448
 constexpr size_t kStaticKeyOff = kStaticLseOff + (size_t)kStaticLists * 2 * sizeof(double);
 constexpr size_t kStaticBytes = kStaticKeyOff + (size_t)kStaticLists * 2 * kSub * sizeof(uint64_t);
 static_assert(kStaticLseOff % 256 == 0 && kStaticKeyOff % 256 == 0, "aligned regions");

@@ -213,6 +213,7 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
         set_status(s.status, err ? kDevEinval : kDevEcapacity);
         s.status[1] = 1;
         s.n_moves[t] = 0;
+        s.hdr[t].n_moves = 0;  // (the trie is unchanged: nothing more to move)
       }
       return;
     }
@@ -241,7 +242,8 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
         nh.leaf_depth = d_new;
         nh.next_id = h.next_id + b;
         nh.step = h.step + 1;
-        nh.pad1 = 0;
+        nh.n_moves = 0;
+        nh.first_moved = 0;
         s.hdr[t] = nh;
         s.n_moves[t] = 0;
       }
@@ -303,7 +305,10 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
       nh.leaf_depth = d_new;
       nh.next_id = h.next_id + b;
       nh.step = h.step + 1;
-      nh.pad1 = 0;
+      nh.n_moves = n_moved;
+      // the first move's destination: the start of the re-packed trie, or the survivor that
+      // follows the first dead slot (every slot before it survived)
+      nh.first_moved = rebase ? 0 : (r0 - e) + first_dead;
       s.hdr[t] = nh;
       s.n_moves[t] = n_moved;
     }
@@ -329,6 +334,7 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
       set_status(s.status, err ? kDevEinval : kDevEcapacity);
       s.status[1] = 1;
       s.n_moves[t] = 0;
+      s.hdr[t].n_moves = 0;  // (the trie is unchanged: nothing more to move)
     }
     return;
   }
@@ -366,7 +372,8 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
       nh.leaf_depth = d_new;
       nh.next_id = h.next_id + b;
       nh.step = h.step + 1;
-      nh.pad1 = 0;
+      nh.n_moves = 0;
+      nh.first_moved = 0;
       s.hdr[t] = nh;
       s.n_moves[t] = 0;
     }
@@ -397,6 +404,7 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
       set_status(s.status, kDevEcapacity);
       s.status[1] = 1;
       s.n_moves[t] = 0;
+      s.hdr[t].n_moves = 0;  // (the trie is unchanged: nothing more to move)
     }
     return;
   }
@@ -483,7 +491,8 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
     nh.leaf_depth = d_new;
     nh.next_id = h.next_id + b;
     nh.step = h.step + 1;
-    nh.pad1 = 0;
+    nh.n_moves = mv_run;
+    nh.first_moved = mv_run > 0 ? s.moves[off].y - nb : 0;  // (written before the last barrier)
     s.hdr[t] = nh;
     s.n_moves[t] = mv_run;
   }

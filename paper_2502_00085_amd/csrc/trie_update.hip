@@ -28,7 +28,8 @@ __global__ __launch_bounds__(256) void k_init_prompt(DevState s, const int32_t* 
     h.leaf_depth = P - 1;
     h.next_id = P;
     h.step = 0;
-    h.pad1 = 0;
+    h.n_moves = 0;
+    h.first_moved = 0;
     s.hdr[t] = h;
   }
 }
