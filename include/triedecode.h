@@ -124,9 +124,11 @@ typedef struct {
  * current device (synchronous).  Tries start empty; call td_init_prompt or
  * td_load_state before decoding.  Tuning, read here from the environment:
  * TD_ATTN_SPLITS = n (1..64) fixes the number of WGs that split one (trie, layer, KV
- * head) unit's nodes in the decode attention, instead of the built-in choice (which
- * splits only when there are too few units to fill the chip); a choice whose partials
- * would not fit the workspace falls back to no split. */
+ * head) unit's nodes in the decode attention, each taking a share, instead of the
+ * built-in choice (which splits only when there are too few units to fill the chip, up
+ * to 16 ways, and gives nodes to only as many of those WGs as keep each of their waves to
+ * one 32-node tile); a choice whose partials would not fit the workspace falls back to no
+ * split. */
 td_status td_create(const td_desc* desc, td_ctx** out);
 td_status td_destroy(td_ctx* ctx);
 

@@ -26,10 +26,11 @@ __device__ inline void store8(__bf16* p, const float* v) {
 }
 
 // Grid: (trie, layer, KV head, row block) units x parts; each thread one (row, 8-element
-// chunk of d).  The splits are taken in groups of 8: every load of a group (maxima, sums
-// and 8-element O chunks) is issued before any is used, so a merge of up to 8 splits is
-// one memory round; groups are merged with a running max.
-template <typename T>
+// chunk of d).  The splits are taken in groups of GS (8 or 16): every load of a group
+// (maxima, sums and 8-element O chunks) is issued before any is used, so a merge of up to
+// GS splits is one memory round; groups are merged with a running max.  A split that
+// attended no node (sum 0: an empty range, or every node hidden) weighs nothing.
+template <typename T, int GS>
 __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(DevState s, AttnArgs a, int R, int parts) {
   const int unit = blockIdx.x / parts;  // ((t * nl + li) * Hkv + g) * row_blocks + rb
   const int item = (blockIdx.x % parts) * kCombineThreads + (int)threadIdx.x;
@@ -43,22 +44,22 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(DevState s, At
   const int G = s.Hq / s.Hkv;
   const int D = s.D;
   const int CH = D / 8;
+  const int n_live = s.hdr[t].n_live;
   if (item >= R * CH) return;
   const int i = item / CH, c = (item % CH) * 8;
   const int rr = rb * R + i;
   const int nrows = a.tree ? a.qmax : s.b;  // row owners per trie in out
   if (rr >= nrows * G) return;
-  const int n_live = s.hdr[t].n_live;
   const size_t stride = (size_t)R * (D + 2);  // one split's records
   const float* rec = s.attn_part + (size_t)unit * a.splits * stride + (size_t)i * (D + 2);
   float M = -1.0e30f, L = 0.0f, O[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) O[e] = 0.0f;
-  for (int s0 = 0; s0 < a.splits; s0 += 8) {
-    float mv[8], lv[8];
-    float2 ov[8][4];
+  for (int s0 = 0; s0 < a.splits; s0 += GS) {
+    float mv[GS], lv[GS];
+    float2 ov[GS][4];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < GS; ++k) {
       // (a split past the last reads the group's first again; its weight is zero)
       const float* pp = rec + (size_t)(s0 + k < a.splits ? s0 + k : s0) * stride;
       mv[k] = pp[D];
@@ -69,19 +70,20 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(DevState s, At
     }
     float Mg = M;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) Mg = s0 + k < a.splits ? fmaxf(Mg, mv[k]) : Mg;
+    for (int k = 0; k < GS; ++k) Mg = s0 + k < a.splits && lv[k] > 0.0f ? fmaxf(Mg, mv[k]) : Mg;
     const float fo = exp2f(M - Mg);
     L *= fo;
 #pragma unroll
     for (int e = 0; e < 8; ++e) O[e] *= fo;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const float f = s0 + k < a.splits ? exp2f(mv[k] - Mg) : 0.0f;
-      L += lv[k] * f;
+    for (int k = 0; k < GS; ++k) {
+      const bool use = s0 + k < a.splits && lv[k] > 0.0f;
+      const float f = use ? exp2f(mv[k] - Mg) : 0.0f;
+      L += use ? lv[k] * f : 0.0f;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        O[2 * e] += ov[k][e].x * f;
-        O[2 * e + 1] += ov[k][e].y * f;
+        O[2 * e] += use ? ov[k][e].x * f : 0.0f;
+        O[2 * e + 1] += use ? ov[k][e].y * f : 0.0f;
       }
     }
     M = Mg;
@@ -100,12 +102,14 @@ hipError_t launch_attn_combine(const DevState& s, const AttnArgs& a, int rows_pe
                                hipEvent_t ev0, hipEvent_t ev1) {
   const int parts = (rows_per_block * (s.D / 8) + kCombineThreads - 1) / kCombineThreads;
   const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * parts);
-  if (s.dtype == TD_F32)
-    hipExtLaunchKernelGGL(k_attn_combine<float>, grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a,
-                          rows_per_block, parts);
-  else
-    hipExtLaunchKernelGGL(k_attn_combine<__bf16>, grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a,
-                          rows_per_block, parts);
+  const bool wide = a.splits > 8;  // (one memory round for up to 16 splits)
+  if (s.dtype == TD_F32) {
+    if (wide) hipExtLaunchKernelGGL((k_attn_combine<float, 16>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
+    else hipExtLaunchKernelGGL((k_attn_combine<float, 8>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
+  } else {
+    if (wide) hipExtLaunchKernelGGL((k_attn_combine<__bf16, 16>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
+    else hipExtLaunchKernelGGL((k_attn_combine<__bf16, 8>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
+  }
   return hipGetLastError();
 }
 

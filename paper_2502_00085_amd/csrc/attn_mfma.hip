@@ -39,6 +39,18 @@ constexpr int kRows = 32;
 constexpr float kNegBig = -1.0e30f;
 constexpr int kRegMoves = 128;  // moved rows whose sources each wave keeps in registers
 
+// Nodes per split of a span split `splits` ways: whole 32-node tiles, and (unless `all`)
+// only as many splits as give each of the NW waves at most one tile round (when fewer
+// suffice, the WGs of the remaining splits get an empty range and their partials weigh
+// nothing).
+__device__ inline int split_range(int span, int splits, int NW, bool all) {
+  if (splits <= 1) return span;
+  const int tiles = (span + 31) / 32;
+  const int need = (tiles + NW - 1) / NW;
+  const int act = all ? splits : (need < 1 ? 1 : (need < splits ? need : splits));
+  return (tiles + act - 1) / act * 32;
+}
+
 template <int D, int NW>
 struct MfmaCfg {
   static constexpr int KSTEPS = D / 16;       // 32x32x16 steps of S^T
@@ -125,13 +137,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     const int hi = qrange[0];
     lo = hi > 0 ? window_lo(s, u.t, base, N, qrange[1]) : 0;
     const int span = max(0, hi - lo);
-    const int per = (span + a.splits - 1) / a.splits;
+    const int per = split_range(span, a.splits, NW, a.all_splits);
     n0 = lo + u.split * per;
     n1 = min(lo + span, n0 + per);
   } else {
     row_ok = r < s.b * G && owner < n_live;
     lo = window_lo(s, u.t, base, N, Dq);
-    const int per = (N - lo + a.splits - 1) / a.splits;
+    const int per = split_range(N - lo, a.splits, NW, a.all_splits);
     n0 = lo + u.split * per;
     n1 = min(N, n0 + per);
   }
@@ -652,12 +664,12 @@ int attn_mfma_rows_per_block() { return kRows; }
 
 // Node splits per (trie, layer, KV head, row block): one WG per unit once there are enough
 // units to occupy most CUs (a split costs partial writes and a combine launch); small
-// launches are split so that the node axis still spreads over the chip.
+// launches are split so that the node axis still spreads over the chip, up to 16 ways.
 int attn_choose_splits(const DevState& s, int n_layers, int row_blocks) {
   const int units = s.T * n_layers * s.Hkv * row_blocks;
   if (units >= 192) return 1;
   int sp = (256 + units - 1) / units;
-  return sp > 8 ? 8 : sp;
+  return sp > 16 ? 16 : sp;  // (the kernel activates only the splits its node span needs)
 }
 
 hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,

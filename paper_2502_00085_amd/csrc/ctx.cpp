@@ -257,6 +257,7 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
     a.row_blocks = 1;
   }
   a.splits = c->splits_override > 0 ? c->splits_override : td::attn_choose_splits(s, n_layers, a.row_blocks);
+  a.all_splits = c->splits_override > 0 ? 1 : 0;
   const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks32;  // (partials per 32-row block)
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;
   a.xcd_group = a.row_blocks > 1 && ((long)s.T * n_layers * s.Hkv * a.splits) % 8 == 0 ? 1 : 0;
@@ -353,6 +354,7 @@ td_status trie_tree_attn(td_ctx* c, int32_t layer_begin, int32_t n_layers, int32
   a.row_blocks = (q_max * (s.Hq / s.Hkv) + rpb - 1) / rpb;
   a.row_blocks32 = a.row_blocks;
   a.splits = c->splits_override > 0 ? c->splits_override : td::attn_choose_splits(s, n_layers, a.row_blocks);
+  a.all_splits = c->splits_override > 0 ? 1 : 0;
   const long units = (long)s.T * n_layers * s.Hkv * a.row_blocks;
   if (units * a.splits > s.attn_pairs_max && a.splits > 1) a.splits = 1;
   a.xcd_group = a.row_blocks > 1 && ((long)s.T * n_layers * s.Hkv * a.splits) % 8 == 0 ? 1 : 0;

@@ -111,6 +111,8 @@ struct AttnArgs {
   int rb_per_wg = 1;               // (matrix-core decode) 32-row blocks per WG: 1 or 2
   int row_blocks32 = 0;            // 32-row blocks per unit (partials and the combine); the
                                    // grid's row_blocks counts WGs, of rb_per_wg blocks each
+  int all_splits = 0;              // (matrix-core kernel) 1: every split WG takes a share of the
+                                   // nodes (a forced split count); 0: only as many as needed
 };
 
 hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const int32_t* d_tokens,

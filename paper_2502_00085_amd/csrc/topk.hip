@@ -11,8 +11,8 @@
 //
 // Two launches:
 //   k_topb_chunk  grid (chunks of 4096 logits, rows, tries): the chunk's max and its fp64
-//                 sum of exp(x - max), and the largest logit (key, with its index) of each
-//                 of its 16 sub-chunks (the 256 logits of one wave: 4 runs of 64);
+//                 sum of exp(x - max), and the two largest logit keys of each of its 16
+//                 sub-chunks (256 logits: 4 runs of 64, 1024 apart);
 //   k_topb_final  grid (tries): every row's lse from its chunk partials; the score of each
 //                 sub-chunk's largest logit; a bound L at most the b-th largest of those
 //                 (the b-th largest of the maxima of disjoint groups of sub-chunks);
@@ -35,6 +35,7 @@ namespace {
 constexpr int kChunkThreads = 1024;
 constexpr int kChunkPer = kLseChunk / kChunkThreads;  // logits per thread
 constexpr int kChunkWaves = kChunkThreads / 64;
+constexpr long kManyChunks = 512;                     // chunk WGs beyond which they have 4 waves
 constexpr int kFinalThreads = 1024;
 constexpr int kFinalWaves = kFinalThreads / 64;
 constexpr int kCandMax = 4096;
@@ -174,61 +175,84 @@ __device__ inline void rank_topb(const uint64_t* cand, const uint64_t* comp, int
 }
 
 // One chunk of one row: max, fp64 sum of exp(x - max), the two largest logit keys of each
-// wave (sub-chunk).
-__global__ __launch_bounds__(kChunkThreads) void k_topb_chunk(DevState s, const float* logits) {
+// 256-logit sub-chunk.  Sub-chunk w of the chunk holds logits v0 + i*1024 + 64w + lane
+// (i < 4); a WG of NWC waves gives each wave 16/NWC consecutive sub-chunks (16 waves: one
+// each; 4 waves, for launches of many chunks: four each, so that the wave-wide and
+// block-wide steps are paid once per 1,024 logits).
+template <int NWC>
+__global__ __launch_bounds__(NWC * 64) void k_topb_chunk(DevState s, const float* logits) {
+  constexpr int SPW = kSub / NWC;  // sub-chunks per wave
   const int c = blockIdx.x, r = blockIdx.y, t = blockIdx.z;
   const int V = s.V, b = s.b;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const float* row = logits + ((size_t)t * b + r) * V;
   const int v0 = c * kLseChunk;
-  __shared__ float wm[kChunkWaves];
-  __shared__ double ws[kChunkWaves];
+  __shared__ float wm[NWC];
+  __shared__ double ws[NWC];
 
   // the loads go out before n_live is known (every row of the [T][b][V] block exists)
-  float x[kChunkPer];
+  float x[SPW][kChunkPer];
 #pragma unroll
-  for (int i = 0; i < kChunkPer; ++i) {
-    const int v = v0 + i * kChunkThreads + (int)threadIdx.x;
-    x[i] = v < V ? row[v] : -INFINITY;
-  }
+  for (int q = 0; q < SPW; ++q)
+#pragma unroll
+    for (int i = 0; i < kChunkPer; ++i) {
+      const int v = v0 + i * kChunkThreads + (wave * SPW + q) * 64 + lane;
+      x[q][i] = v < V ? row[v] : -INFINITY;
+    }
   if (r >= s.hdr[t].n_live) return;
-  float m = -INFINITY;
-  uint64_t k1 = 0, k2 = 0;  // this lane's two largest keys
-  const uint32_t flat0 = (uint32_t)r * (uint32_t)V + (uint32_t)v0 + threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < kChunkPer; ++i) {
-    const int v = v0 + i * kChunkThreads + (int)threadIdx.x;
-    m = fmaxf(m, x[i]);
-    // (the end-of-sequence token, if any, is not a candidate for the next beams)
-    const uint64_t k = v < V && v != s.eos ? x_key(x[i], flat0 + (uint32_t)(i * kChunkThreads)) : 0;
-    k2 = k > k1 ? k1 : (k > k2 ? k : k2);
-    k1 = k > k1 ? k : k1;
-  }
-  m = __ockl_wfred_max_f32(m);
-  // the wave's largest key, and its second largest (the owner of the largest offers its
-  // own second; keys are unique)
-  const uint64_t km = wave_max_u64(k1);
-  const uint64_t km2 = wave_max_u64(k1 == km ? k2 : k1);
   const size_t list = ((size_t)t * b + r) * s.lse_chunks + c;
   const size_t lists = (size_t)s.T * b * s.lse_chunks;
-  if (lane == 0) {
-    wm[wave] = m;
-    s.topk_keys[wave * lists + list] = km;  // 0 when the wave holds no logit
-    s.topk_keys[s.topk_half + wave * lists + list] = km2;
+  float m = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < SPW; ++q) {
+    const int sw = wave * SPW + q;
+    // this lane's two largest logits of the sub-chunk, by order of value (a later logit
+    // replaces an equal one only if larger: the lower flat index wins ties)
+    uint32_t o1 = 0, o2 = 0;
+    int i1 = 0, i2 = 0;
+#pragma unroll
+    for (int i = 0; i < kChunkPer; ++i) {
+      const int v = v0 + i * kChunkThreads + sw * 64 + lane;
+      m = fmaxf(m, x[q][i]);
+      // (the end-of-sequence token, if any, is not a candidate for the next beams;
+      // order 0 = no candidate)
+      const uint32_t o = v < V && v != s.eos ? ord_raw(x[q][i]) : 0u;
+      const bool gt1 = o > o1, gt2 = o > o2;
+      o2 = gt1 ? o1 : (gt2 ? o : o2);
+      i2 = gt1 ? i1 : (gt2 ? i : i2);
+      o1 = gt1 ? o : o1;
+      i1 = gt1 ? i : i1;
+    }
+    const uint32_t flat = (uint32_t)r * (uint32_t)V + (uint32_t)(v0 + sw * 64 + lane);
+    const uint64_t k1 = o1 ? ((uint64_t)o1 << 32) | (uint64_t)(0xffffffffu - (flat + (uint32_t)(i1 * kChunkThreads))) : 0;
+    const uint64_t k2 = o2 ? ((uint64_t)o2 << 32) | (uint64_t)(0xffffffffu - (flat + (uint32_t)(i2 * kChunkThreads))) : 0;
+    // the sub-chunk's largest key, and its second largest (the owner of the largest offers
+    // its own second; keys are unique)
+    const uint64_t km = wave_max_u64(k1);
+    const uint64_t km2 = wave_max_u64(k1 == km ? k2 : k1);
+    if (lane == 0) {
+      s.topk_keys[sw * lists + list] = km;  // 0 when the sub-chunk holds no candidate
+      s.topk_keys[s.topk_half + sw * lists + list] = km2;
+    }
   }
+  m = __ockl_wfred_max_f32(m);
+  if (lane == 0) wm[wave] = m;
   __syncthreads();
   m = wm[0];
-  for (int w = 1; w < kChunkWaves; ++w) m = fmaxf(m, wm[w]);
+#pragma unroll
+  for (int w = 1; w < NWC; ++w) m = fmaxf(m, wm[w]);
   const double md = (double)m;
   double acc = 0.0;
   bool bad = false;  // a NaN or +inf logit
 #pragma unroll
-  for (int i = 0; i < kChunkPer; ++i) {
-    const int v = v0 + i * kChunkThreads + (int)threadIdx.x;
-    // (a chunk whose logits are all -inf adds nothing; exp(-inf - -inf) would be NaN)
-    if (v < V && md != -INFINITY) acc += exp((double)x[i] - md);
-    bad |= v < V && !(x[i] < INFINITY);
-  }
+  for (int q = 0; q < SPW; ++q)
+#pragma unroll
+    for (int i = 0; i < kChunkPer; ++i) {
+      const int v = v0 + i * kChunkThreads + (wave * SPW + q) * 64 + lane;
+      // (a chunk whose logits are all -inf adds nothing; exp(-inf - -inf) would be NaN)
+      if (v < V && md != -INFINITY) acc += exp((double)x[q][i] - md);
+      bad |= v < V && !(x[q][i] < INFINITY);
+    }
   // an invalid logit poisons the chunk's sum: the row's lse is then NaN and the call
   // reports the row (k_topb_final)
   if (bad) acc = __builtin_nan("");
@@ -237,7 +261,7 @@ __global__ __launch_bounds__(kChunkThreads) void k_topb_chunk(DevState s, const 
   __syncthreads();
   if (threadIdx.x == 0) {
     double tot = 0.0;
-    for (int w = 0; w < kChunkWaves; ++w) tot += ws[w];
+    for (int w = 0; w < NWC; ++w) tot += ws[w];
     s.lse_part[list * 2] = md;
     s.lse_part[list * 2 + 1] = tot;
   }
@@ -654,8 +678,13 @@ hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_
                                   float* lse, const int32_t* pair_parent, const int32_t* pair_token,
                                   float* pair_score, bool append, hipStream_t st, hipEvent_t ev0,
                                   hipEvent_t ev1) {
-  hipExtLaunchKernelGGL(k_topb_chunk, dim3(s.lse_chunks, s.b, s.T), dim3(kChunkThreads), 0, st, ev0,
-                        nullptr, 0, s, logits);
+  // (many chunks, more than about two WGs of 16 waves per CU: WGs of 4 waves)
+  if ((long)s.T * s.b * s.lse_chunks > kManyChunks)
+    hipExtLaunchKernelGGL(k_topb_chunk<4>, dim3(s.lse_chunks, s.b, s.T), dim3(4 * 64), 0, st, ev0, nullptr, 0, s,
+                          logits);
+  else
+    hipExtLaunchKernelGGL(k_topb_chunk<kChunkWaves>, dim3(s.lse_chunks, s.b, s.T), dim3(kChunkThreads), 0, st, ev0,
+                          nullptr, 0, s, logits);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // entries per wave: b * chunks (every wave covers every row); up to 256 of them fit the

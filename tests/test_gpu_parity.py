@@ -71,11 +71,20 @@ def test_one_layer_calls_two_row_blocks():
     layer_case(small(n_layers=2, beam_width=16, n_q_heads=16, n_kv_heads=4, steps=6), seed=44, calls=[0, 1, 2])
 
 
-def test_more_splits_than_one_merge_group(monkeypatch):
-    """12 node splits per unit (a TD_ATTN_SPLITS override): the split merge takes a group
-    of 8 and a group of 4 with a running max, and some splits hold no node."""
-    monkeypatch.setenv("TD_ATTN_SPLITS", "12")
+@pytest.mark.parametrize("splits", ["12", "21"])
+def test_more_splits_than_one_merge_group(monkeypatch, splits):
+    """12 and 21 node splits per unit (a TD_ATTN_SPLITS override, every split WG given a
+    share): the split merge takes one group of 16, or a group of 16 and one of 5 with a
+    running max, and some splits hold no node."""
+    monkeypatch.setenv("TD_ATTN_SPLITS", splits)
     run_case(small(steps=6), seed=31)
+
+
+def test_one_layer_calls_with_spare_split_wgs():
+    """One-layer calls of a wider trie: 16 split WGs per unit are launched and only as many
+    as give each wave one tile take nodes (the rest hold empty ranges, weighing nothing in
+    the merge)."""
+    layer_case(small(n_layers=2, prompt_min=700, prompt_max=700, steps=5), seed=46, calls=[0, 1, 2])
 
 
 @pytest.mark.parametrize("mode", ["driven", "scripted"])
