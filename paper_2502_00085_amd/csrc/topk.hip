@@ -40,7 +40,7 @@ constexpr int kFinalThreads = 1024;
 constexpr int kFinalWaves = kFinalThreads / 64;
 constexpr int kCandMax = 4096;
 constexpr int kSub = kChunkWaves;                     // sub-chunks (waves) per chunk
-constexpr int kPer = 16;                              // entries per lane held in registers
+constexpr int kPer = 8;                               // entries per lane held in registers
 constexpr int kMaxEntries = 2048;                     // entries per wave (b * chunks per row)
 static_assert(kSub == kFinalThreads / 64, "the final merge maps sub-chunk w of a chunk to wave w");
 static_assert(kAppThreads == kFinalThreads, "the fused merge runs the append with its own block");
@@ -386,29 +386,31 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
   const uint64_t* ekey2 = ekey + s.topk_half;                                 // second largest
   const int e_all = b * nch;
 
-  // Independent loads first: the first batch of this wave's entries (rows >= n_live are
-  // dropped once n_live is known), pair logits, leaf scores, every row's lse, then n_live.
+  // Independent loads first, in one batch (no load waits on another, except the pair
+  // logits and the append's fields on the header): the first batch of this wave's entries
+  // (rows >= n_live are dropped once n_live is known), the chunk partials of the row this
+  // wave reduces, the leaf scores, the pairs, the EOS logits, the append's fields.
   constexpr int PRE2 = PER <= 4 ? PER : 0;  // second-largest keys held in registers
   uint64_t km0[PER], km20[PRE2 > 0 ? PRE2 : 1];
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
-    const int j = q * 64 + lane;
-    km0[q] = 0;
-    if (PRE2 > 0) km20[q < PRE2 ? q : 0] = 0;
-    if (q * 64 < e_all) {  // (wave-uniform)
-      km0[q] = j < e_all ? ekey[j] : 0;
-      if (PRE2 > 0) km20[q < PRE2 ? q : 0] = j < e_all ? ekey2[j] : 0;
-    }
+    const int j = min(q * 64 + lane, e_all - 1);  // (clamped: every lane loads)
+    km0[q] = ekey[j];
+    if (PRE2 > 0) km20[q < PRE2 ? q : 0] = ekey2[j];
   }
-  // pairs: the last b threads (their wave has no row below; the dependent logit load
-  // waits there)
+  // one row per wave (b <= 16 and nch <= 64: wave r, lane c holds chunk c's max and sum)
+  const bool lse_fast = b <= kFinalWaves && nch <= 64;
+  double2 part = make_double2(-INFINITY, 0.0);
+  if (lse_fast)
+    part = reinterpret_cast<const double2*>(s.lse_part)[((size_t)t * b + min(wave, b - 1)) * nch + min(lane, nch - 1)];
+  const float lsc = s.leaf_score[(size_t)t * b + min(lane, b - 1)];  // leaf score of row `lane`
+  // pairs: the last b threads (their wave has no row below); the dependent logit load comes
+  // after the log-sum-exp
   const int pj = (int)threadIdx.x - (kFinalThreads - b);
-  float pair_x = 0.0f;
   int pp = -1, pv = -1;
   if (pair_parent != nullptr && pj >= 0) {
     pp = pair_parent[(size_t)t * b + pj];
     pv = pair_token[(size_t)t * b + pj];
-    if (pp >= 0 && pp < b && pv >= 0 && pv < V) pair_x = lrow[(size_t)pp * V + pv];
   }
   // end of sequence: every row's EOS logit (thread r), and the pool's state (thread 0)
   float eos_x = 0.0f;
@@ -421,24 +423,41 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
       pool_step = s.hdr[t].step + 1;
     }
   }
-  for (int r = threadIdx.x; r < b; r += kFinalThreads) row_score[r] = s.leaf_score[(size_t)t * b + r];
   __shared__ AppShared ash;
   AppPre pre;
   if constexpr (APPEND) append_prefetch(s, t, s.hdr[t], false, ash, pre);
-  for (int r = wave; r < b; r += kFinalWaves) {
-    const float l = row_lse32_wave(s.lse_part + ((size_t)t * b + r) * nch * 2, nch);
-    if (lane == 0) row_lse[r] = l;
-  }
   const int n_live = APPEND ? pre.h.n_live : s.hdr[t].n_live;
+
+  // every row's lse (fp64 from the chunk partials, then fl32): row r by wave r (with
+  // lse_fast; else by the lane-strided loop)
+  if (lse_fast) {
+    if (wave < b) {
+      const double M = __ockl_wfred_max_f64(lane < nch ? part.x : -INFINITY);
+      const double S = __ockl_wfred_add_f64(lane < nch && part.y != 0.0 ? part.y * exp(part.x - M) : 0.0);
+      if (lane == 0) row_lse[wave] = (float)(M + log(S));
+    }
+  } else {
+    for (int r = wave; r < b; r += kFinalWaves) {
+      const float l = row_lse32_wave(s.lse_part + ((size_t)t * b + r) * nch * 2, nch);
+      if (lane == 0) row_lse[r] = l;
+    }
+  }
+  if (wave == 0 && lane < b) row_score[lane] = lsc;
   if (threadIdx.x == 0) ncand = nhot = 0;
+  float pair_x = 0.0f;
+  if (pair_parent != nullptr && pj >= 0 && pp >= 0 && pp < b && pv >= 0 && pv < V)
+    pair_x = lrow[(size_t)pp * V + pv];
   __syncthreads();
   const int e_live = n_live * nch;
   const float inv_nch = 1.0f / (float)nch;
+  // a live row without a finite log-sum-exp (no finite logit, or a NaN / +inf one)
+  const bool bad_row = __ballot(lane < n_live && !(fabsf(row_lse[min(lane, b - 1)]) < INFINITY)) != 0ull;
 
   // score ord of an entry's largest logit (0: no entry / no logit); the first batch is
-  // kept in registers, a second one (more than 1024 entries per wave) is read again later
+  // kept in registers (its row lookups go out together), a second one (more than 64 PER
+  // entries per wave) is read again later
   auto entry_ord = [&](int j, uint64_t km) -> uint32_t {
-    const int r = div_small(j, inv_nch);
+    const int r = min(div_small(j, inv_nch), b - 1);
     return km != 0 ? ord_score(score_only(key_x(km), row_lse[r], row_score[r])) : 0u;
   };
   uint32_t o0[PER];
@@ -446,11 +465,8 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
     const int j = q * 64 + lane;
-    o0[q] = 0;
-    if (q * 64 < e_live) {  // (wave-uniform)
-      o0[q] = entry_ord(j, j < e_live ? km0[q] : 0);
-      lmax = o0[q] > lmax ? o0[q] : lmax;
-    }
+    o0[q] = entry_ord(j, j < e_live ? km0[q] : 0);
+    lmax = o0[q] > lmax ? o0[q] : lmax;
   }
   for (int j = PER * 64 + lane; j < e_live; j += 64) {
     const uint32_t oj = entry_ord(j, ekey[j]);
@@ -626,8 +642,6 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     // a live row without a finite log-sum-exp (no finite logit, or a NaN / +inf one) is
     // invalid input: reported, and the fused append is given an invalid selection, so
     // that it leaves the trie as it was
-    bool bad_row = false;
-    for (int r = 0; r < n_live; ++r) bad_row |= !(fabsf(row_lse[r]) < INFINITY);
     if (bad_row) set_status(s.status, kDevEinval);
     const uint64_t kx = best_c[j];
     uint32_t f = key_flat(kx);
@@ -661,9 +675,7 @@ __global__ __launch_bounds__(kFinalThreads) void k_topb_final(DevState s, const 
     if (pp >= 0 && pp < n_live && pv >= 0 && pv < V) sc = score_only(pair_x, row_lse[pp], row_score[pp]);
     pair_score[(size_t)t * b + pj] = sc;
     if (APPEND) {
-      bool bad_row = false;  // (as for the selection above)
-      for (int r = 0; r < n_live; ++r) bad_row |= !(fabsf(row_lse[r]) < INFINITY);
-      ash.sp[pj] = bad_row ? -1 : pp;
+      ash.sp[pj] = bad_row ? -1 : pp;  // (as for the selection above)
       ash.stok[pj] = pv;
       ash.ssc[pj] = sc;
     }

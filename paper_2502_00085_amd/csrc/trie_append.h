@@ -39,9 +39,11 @@ __device__ inline int block_rank(bool flag, int* wave_cnt, int* total) {
   return before + in_wave;
 }
 
-__device__ inline uint64_t remap_mask(uint64_t m, const int* sp, int b) {
+// New mask of a node with old mask m: bit j = old bit sel_parent[j].  spl holds sel_parent[j]
+// in lane j (j < b) of every wave: the ranks are read across lanes, not from LDS.
+__device__ inline uint64_t remap_mask(uint64_t m, int spl, int b) {
   uint64_t r = 0;
-  for (int j = 0; j < b; ++j) r |= ((m >> (sp[j] & 63)) & 1ull) << j;  // (ranks are checked)
+  for (int j = 0; j < b; ++j) r |= ((m >> (__builtin_amdgcn_readlane(spl, j) & 63)) & 1ull) << j;  // (ranks are checked)
   return r;
 }
 
@@ -81,7 +83,7 @@ struct AppShared {
   float ssc[kMaxBeam];               // and score
   int err, wave_cnt[kAppWaves], wave_cnt2[kAppWaves];
   int full_cnt, first_nf;
-  int wa[kAppWaves], wf[kAppWaves], wd[kAppWaves], wp[kAppWaves];
+  int4 winfo[kAppWaves];  // per wave: survivors, all-beam survivors, first dead, first not all-beam
   int lpos[kAppThreads];
 };
 
@@ -100,6 +102,7 @@ struct AppPre {
 // is left, with the loads, to append_apply.  Call from uniform control flow.
 __device__ inline void append_prefetch(const DevState& s, int t, const TrieHdr& h, bool search_window,
                                        AppShared& sh, AppPre& pre) {
+  if (threadIdx.x == 0) sh.err = 0;  // (append_apply's first barrier orders it)
   pre.h = h;
   const size_t off = (size_t)t * s.cap;
   const int N = h.n_nodes, base = h.base;
@@ -142,16 +145,16 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
   int& first_nf = sh.first_nf;
   int* const wave_cnt = sh.wave_cnt;
   int* const wave_cnt2 = sh.wave_cnt2;
-  int* const wa = sh.wa;
-  int* const wf = sh.wf;
-  int* const wd = sh.wd;
-  int* const wp = sh.wp;
+  int4* const winfo = sh.winfo;
   int* const lpos = sh.lpos;
   if (!pre.searched) append_prefetch(s, t, pre.h, true, sh, pre);  // (uniform) a deferred window search
   __syncthreads();  // the selection is in sh
+  const int lane = tid & 63, wave = tid >> 6;
+  // every wave: selection j's parent rank in lane j (read across lanes by remap_mask)
+  const int spl = lane < b ? sp[lane] : 0;
   int p = 0, v = 0;
   if (tid < b) {
-    p = sp[tid];
+    p = spl;
     v = stok[tid];
   }
   const TrieHdr h = pre.h;
@@ -170,8 +173,6 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
     const bool in = n < N;
     const uint64_t m = pre.m;
     const int id = pre.id, tk = pre.tk, dp = pre.dp, pp = pre.pp;
-    if (tid == 0) err = 0;
-    __syncthreads();
     // invalid selections: a parent rank outside the live leaves, a token outside the
     // vocabulary, the same (parent, token) twice
     bool bad = tid < b && (p < 0 || p >= n_live || v < 0 || v >= s.V);
@@ -182,26 +183,25 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
     if (bad) atomicOr(&err, 1);
     // survivors (new mask != 0), the all-beam ones, the first dead and the first
     // not-all-beam slot: one exchange
-    const uint64_t nm = in ? remap_mask(m, sp, b) : 0ull;
+    const uint64_t nm = in ? remap_mask(m, spl, b) : 0ull;
     const bool alive = in && nm != 0ull;
-    const int lane = tid & 63, wave = tid >> 6;
     const uint64_t ba = __ballot(alive), bd = __ballot(in && !alive);
     const uint64_t bf = __ballot(alive && nm == full_b), bp = __ballot(in && nm != full_b);
-    if (lane == 0) {
-      wa[wave] = __popcll(ba);
-      wf[wave] = __popcll(bf);
-      wd[wave] = bd ? wave * 64 + __ffsll((unsigned long long)bd) - 1 : kAppThreads;
-      wp[wave] = bp ? wave * 64 + __ffsll((unsigned long long)bp) - 1 : kAppThreads;
-    }
+    if (lane == 0)
+      winfo[wave] = make_int4(__popcll(ba), __popcll(bf),
+                              bd ? wave * 64 + __ffsll((unsigned long long)bd) - 1 : kAppThreads,
+                              bp ? wave * 64 + __ffsll((unsigned long long)bp) - 1 : kAppThreads);
     __syncthreads();
     int rank = __popcll(ba & ((1ull << lane) - 1ull)), n_alive = 0, n_full = 0, first_dead = kAppThreads;
     int first_part = kAppThreads;
-    for (int w = 0; w < kAppWaves; ++w) {
-      rank += w < wave ? wa[w] : 0;
-      n_alive += wa[w];
-      n_full += wf[w];
-      first_dead = min(first_dead, wd[w]);
-      first_part = min(first_part, wp[w]);
+#pragma unroll
+    for (int w = 0; w < kAppWaves; ++w) {  // (independent reads: they go out together)
+      const int4 wi = winfo[w];
+      rank += w < wave ? wi.x : 0;
+      n_alive += wi.x;
+      n_full += wi.y;
+      first_dead = min(first_dead, wi.z);
+      first_part = min(first_part, wi.w);
     }
     const int n_new = gc ? (r0 - e) + n_alive + b : N + b;
     // a collection re-packs at slot 0 when the room after the trie is short of the appends
@@ -345,7 +345,7 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
     for (int c0 = r0; c0 < N; c0 += kAppThreads) {
       const int n = c0 + tid;
       if (n < N) {
-        const uint64_t nm = remap_mask(s.mask[off + base + n], sp, b);
+        const uint64_t nm = remap_mask(s.mask[off + base + n], spl, b);
         s.mask[off + base + n] = nm;
         if (nm != full_b) atomicMin(&first_nf, n);
       }
@@ -387,7 +387,7 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
     bool alive = false;
     uint64_t nm = 0;
     if (n < N) {
-      nm = remap_mask(s.mask[off + base + n], sp, b);
+      nm = remap_mask(s.mask[off + base + n], spl, b);
       alive = nm != 0ull;
       if (alive && nm == full_b) atomicAdd(&full_cnt, 1);
     }
@@ -424,7 +424,7 @@ __device__ inline void append_apply(const DevState& s, int t, AppPre& pre, AppSh
         id = s.node_id[off + base + n];
         tk = s.token[off + base + n];
         dp = s.depth[off + base + n];
-        nm = remap_mask(s.mask[off + base + n], sp, b);
+        nm = remap_mask(s.mask[off + base + n], spl, b);
         const int pp = s.parent[off + base + n];
         if (pp >= 0) {
           const int lp = pp - base;
