@@ -127,8 +127,8 @@ typedef struct {
  * head) unit's nodes in the decode attention, each taking a share, instead of the
  * built-in choice (which splits only when there are too few units to fill the chip, up
  * to 16 ways, and gives nodes to only as many of those WGs as keep each of their waves to
- * one 32-node tile); a choice whose partials would not fit the workspace falls back to no
- * split. */
+ * one 32-node tile, or, up to 8 WGs, to half a tile); a choice whose partials would not
+ * fit the workspace falls back to no split. */
 td_status td_create(const td_desc* desc, td_ctx** out);
 td_status td_destroy(td_ctx* ctx);
 

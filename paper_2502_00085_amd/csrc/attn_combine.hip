@@ -11,7 +11,7 @@ namespace td {
 
 namespace {
 
-constexpr int kCombineThreads = 256;
+constexpr int kCombineThreads = 64;
 
 __device__ inline void store8(float* p, const float* v) {
   reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
@@ -25,15 +25,20 @@ __device__ inline void store8(__bf16* p, const float* v) {
   *reinterpret_cast<bf16x8_t*>(p) = y;
 }
 
-// Grid: (trie, layer, KV head, row block) units x parts; each thread one (row, 8-element
-// chunk of d).  The splits are taken in groups of GS (8 or 16): every load of a group
-// (maxima, sums and 8-element O chunks) is issued before any is used, so a merge of up to
-// GS splits is one memory round; groups are merged with a running max.  A split that
-// attended no node (sum 0: an empty range, or every node hidden) weighs nothing.
-template <typename T, int GS>
+// Grid: (trie, layer, KV head, row block) units x parts; each (row, 8-element chunk of d)
+// is merged by TP adjacent lanes (TP = 2 beyond 8 splits), lane j taking the groups of 8
+// splits j, j + TP, ...: every load of a group (maxima, sums and 8-element O chunks) is
+// issued before any is used, so a merge of up to 8 TP splits is one memory round; groups
+// are merged with a running max, and the TP lanes' states with one lane exchange.  WGs of
+// one wave: a CU issues vector loads at a limited rate, small WGs spread the merge's reads
+// over more CUs.  A split that attended no node (sum 0: an empty range, every node
+// hidden, or a split the span did not need) weighs nothing.
+template <typename T, int TP>
 __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(DevState s, AttnArgs a, int R, int parts) {
+  constexpr int GS = 8;
   const int unit = blockIdx.x / parts;  // ((t * nl + li) * Hkv + g) * row_blocks + rb
-  const int item = (blockIdx.x % parts) * kCombineThreads + (int)threadIdx.x;
+  const int lin = (blockIdx.x % parts) * kCombineThreads + (int)threadIdx.x;
+  const int item = lin / TP, sub = lin % TP;  // (the TP lanes of an item are adjacent)
   int x = unit;
   const int rb = x % a.row_blocks;
   x /= a.row_blocks;
@@ -45,6 +50,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(DevState s, At
   const int D = s.D;
   const int CH = D / 8;
   const int n_live = s.hdr[t].n_live;
+  // (both lanes of an item leave together, or neither)
   if (item >= R * CH) return;
   const int i = item / CH, c = (item % CH) * 8;
   const int rr = rb * R + i;
@@ -55,7 +61,7 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(DevState s, At
   float M = -1.0e30f, L = 0.0f, O[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) O[e] = 0.0f;
-  for (int s0 = 0; s0 < a.splits; s0 += GS) {
+  for (int s0 = sub * GS; s0 < a.splits; s0 += TP * GS) {
     float mv[GS], lv[GS];
     float2 ov[GS][4];
 #pragma unroll
@@ -88,6 +94,21 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(DevState s, At
     }
     M = Mg;
   }
+  if constexpr (TP == 2) {
+    // the other lane's state (its groups), rescaled to the common max; the same order on
+    // both lanes
+    const float M2 = __shfl_xor(M, 1), L2 = __shfl_xor(L, 1);
+    float O2[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) O2[e] = __shfl_xor(O[e], 1);
+    const float Mn = fmaxf(M, M2);
+    const float f0 = exp2f((sub == 0 ? M : M2) - Mn), f1 = exp2f((sub == 0 ? M2 : M) - Mn);
+    const float La = sub == 0 ? L : L2, Lb = sub == 0 ? L2 : L;
+    L = La * f0 + Lb * f1;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) O[e] = (sub == 0 ? O[e] : O2[e]) * f0 + (sub == 0 ? O2[e] : O[e]) * f1;
+    if (sub != 0) return;
+  }
   const int bm = rr / G;
   const float inv = ((a.tree || bm < n_live) && L > 0.0f) ? 1.0f / L : 0.0f;
 #pragma unroll
@@ -100,15 +121,15 @@ __global__ __launch_bounds__(kCombineThreads) void k_attn_combine(DevState s, At
 
 hipError_t launch_attn_combine(const DevState& s, const AttnArgs& a, int rows_per_block, hipStream_t st,
                                hipEvent_t ev0, hipEvent_t ev1) {
-  const int parts = (rows_per_block * (s.D / 8) + kCombineThreads - 1) / kCombineThreads;
+  const int tp = a.splits > 8 ? 2 : 1;  // (two lanes per output chunk beyond 8 splits)
+  const int parts = (rows_per_block * (s.D / 8) * tp + kCombineThreads - 1) / kCombineThreads;
   const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * parts);
-  const bool wide = a.splits > 8;  // (one memory round for up to 16 splits)
   if (s.dtype == TD_F32) {
-    if (wide) hipExtLaunchKernelGGL((k_attn_combine<float, 16>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
-    else hipExtLaunchKernelGGL((k_attn_combine<float, 8>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
+    if (tp == 2) hipExtLaunchKernelGGL((k_attn_combine<float, 2>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
+    else hipExtLaunchKernelGGL((k_attn_combine<float, 1>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
   } else {
-    if (wide) hipExtLaunchKernelGGL((k_attn_combine<__bf16, 16>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
-    else hipExtLaunchKernelGGL((k_attn_combine<__bf16, 8>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
+    if (tp == 2) hipExtLaunchKernelGGL((k_attn_combine<__bf16, 2>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
+    else hipExtLaunchKernelGGL((k_attn_combine<__bf16, 1>), grid, dim3(kCombineThreads), 0, st, ev0, ev1, 0, s, a, rows_per_block, parts);
   }
   return hipGetLastError();
 }

@@ -40,15 +40,20 @@ constexpr float kNegBig = -1.0e30f;
 constexpr int kRegMoves = 128;  // moved rows whose sources each wave keeps in registers
 
 // Nodes per split of a span split `splits` ways: whole 32-node tiles, and (unless `all`)
-// only as many splits as give each of the NW waves at most one tile round (when fewer
-// suffice, the WGs of the remaining splits get an empty range and their partials weigh
-// nothing).
-__device__ inline int split_range(int span, int splits, int NW, bool all) {
-  if (splits <= 1) return span;
+// only as many splits as give each of the NW waves at most one tile round, or, up to 8
+// splits (one group of the merge), half a round; *act = the splits that get nodes (the
+// WGs of the others leave at once, their partials marked empty).  (Measured: fewer tiles
+// per WG shorten its load issue, more splits lengthen the merge.)
+__device__ inline int split_range(int span, int splits, int NW, bool all, int* act) {
+  if (splits <= 1) {
+    *act = 1;
+    return span;
+  }
   const int tiles = (span + 31) / 32;
-  const int need = (tiles + NW - 1) / NW;
-  const int act = all ? splits : (need < 1 ? 1 : (need < splits ? need : splits));
-  return (tiles + act - 1) / act * 32;
+  const int half = min(8, (tiles + NW / 2 - 1) / (NW / 2));
+  const int need = max((tiles + NW - 1) / NW, half);
+  *act = all ? splits : (need < 1 ? 1 : (need < splits ? need : splits));
+  return (tiles + *act - 1) / *act * 32;
 }
 
 template <int D, int NW>
@@ -112,7 +117,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   bool row_ok;
   uint64_t qmask = 0;
   int qdepth = -1;  // (TREE) no key is visible to a row without a live query node
-  int lo, n0, n1;
+  int lo, n0, n1, act;
   if constexpr (TREE) {
     __shared__ int qrange[2];  // the block's key range end, its shallowest query depth
     int slot = r < a.qmax * G ? a.qslots[(size_t)u.t * a.qmax + owner] : -1;
@@ -137,15 +142,30 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     const int hi = qrange[0];
     lo = hi > 0 ? window_lo(s, u.t, base, N, qrange[1]) : 0;
     const int span = max(0, hi - lo);
-    const int per = split_range(span, a.splits, NW, a.all_splits);
+    const int per = split_range(span, a.splits, NW, a.all_splits, &act);
     n0 = lo + u.split * per;
     n1 = min(lo + span, n0 + per);
   } else {
     row_ok = r < s.b * G && owner < n_live;
     lo = window_lo(s, u.t, base, N, Dq);
-    const int per = split_range(N - lo, a.splits, NW, a.all_splits);
+    const int per = split_range(N - lo, a.splits, NW, a.all_splits, &act);
     n0 = lo + u.split * per;
     n1 = min(N, n0 + per);
+  }
+  if (u.split >= act) {
+    // a split the span does not need: its partials are marked empty (sum 0) for the
+    // combine; nothing else is due from it (moves come with single-split launches, leaf
+    // rows with the range that holds them)
+    if (threadIdx.x < kRows) {
+#pragma unroll
+      for (int rbk = 0; rbk < RB; ++rbk) {
+        const int unit = RB == 1 ? u.unit : (u.unit / a.row_blocks) * a.row_blocks32 + u.rb * RB + rbk;
+        float* pp = s.attn_part + (((size_t)unit * a.splits + u.split) * kRows + threadIdx.x) * (D + 2);
+        pp[D] = kNegBig;
+        pp[D + 1] = 0.0f;
+      }
+    }
+    return;
   }
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform (SGPR)
   // (two row blocks: every wave waits for the query rows at a barrier, so wave 0 loads them
