@@ -174,6 +174,29 @@ __device__ inline void rank_topb(const uint64_t* cand, const uint64_t* comp, int
   }
 }
 
+// exp(d) in fp64 for d = x - max <= 0 (x and max fp32 values, so d is exact): 2^(k/64)
+// from a table of the 64 values 2^(j/64) (tab, computed per WG) times e^r for the reduced
+// argument r = d - k ln2/64, |r| <= ln2/128, by its Taylor polynomial of degree 5
+// (truncation below 4e-17 relative; ln2/64 split in two parts (Cody-Waite) so that k times
+// the first is exact).  Error within 2 ulp; the chunk sum only needs fp64 accuracy far
+// below the fp32 rounding of the log-sum-exp.  d < -708 (or -inf) gives 0: such a term
+// is below the ulp of a sum that holds exp(0) = 1.  About a third of the instructions of
+// the library exp, which dominates the VALU-bound chunk pass.
+__device__ inline double exp_nonpos(double d, const double* tab) {
+  const double k = __builtin_rint(d * 92.33248261689366);  // 64 / ln 2
+  double r = __builtin_fma(k, -0x1.62e42fefa0000p-7, d);     // ln2/64, leading 36 bits
+  r = __builtin_fma(k, -2.572804622327669e-14, r);           // and the rest
+  double p = __builtin_fma(r, 1.0 / 120.0, 1.0 / 24.0);
+  p = __builtin_fma(r, p, 1.0 / 6.0);
+  p = __builtin_fma(r, p, 0.5);
+  p = __builtin_fma(r, p, 1.0);
+  p *= r;  // e^r - 1
+  const int ki = (int)k;
+  const double t = tab[ki & 63];
+  const double e = __builtin_ldexp(__builtin_fma(t, p, t), ki >> 6);
+  return d < -708.0 ? 0.0 : e;
+}
+
 // One chunk of one row: max, fp64 sum of exp(x - max), the two largest logit keys of each
 // 256-logit sub-chunk.  Sub-chunk w of the chunk holds logits v0 + i*1024 + 64w + lane
 // (i < 4); a WG of NWC waves gives each wave 16/NWC consecutive sub-chunks (16 waves: one
@@ -189,6 +212,7 @@ __global__ __launch_bounds__(NWC * 64) void k_topb_chunk(DevState s, const float
   const int v0 = c * kLseChunk;
   __shared__ float wm[NWC];
   __shared__ double ws[NWC];
+  __shared__ double exp_tab[64];  // 2^(j/64)
 
   // the loads go out before n_live is known (every row of the [T][b][V] block exists)
   float x[SPW][kChunkPer];
@@ -200,6 +224,7 @@ __global__ __launch_bounds__(NWC * 64) void k_topb_chunk(DevState s, const float
       x[q][i] = v < V ? row[v] : -INFINITY;
     }
   if (r >= s.hdr[t].n_live) return;
+  if (wave == 0) exp_tab[lane] = exp2((double)lane * 0.015625);  // (read after the barrier below)
   const size_t list = ((size_t)t * b + r) * s.lse_chunks + c;
   const size_t lists = (size_t)s.T * b * s.lse_chunks;
   float m = -INFINITY;
@@ -250,7 +275,7 @@ __global__ __launch_bounds__(NWC * 64) void k_topb_chunk(DevState s, const float
     for (int i = 0; i < kChunkPer; ++i) {
       const int v = v0 + i * kChunkThreads + (wave * SPW + q) * 64 + lane;
       // (a chunk whose logits are all -inf adds nothing; exp(-inf - -inf) would be NaN)
-      if (v < V && md != -INFINITY) acc += exp((double)x[q][i] - md);
+      if (v < V && md != -INFINITY) acc += exp_nonpos((double)x[q][i] - md, exp_tab);
       bad |= v < V && !(x[q][i] < INFINITY);
     }
   // an invalid logit poisons the chunk's sum: the row's lse is then NaN and the call
