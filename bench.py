@@ -294,6 +294,7 @@ def gpu_bench(args, w, K):
     attn_graph_ms, attn_graph_nodes = attn_graph_time(bench, K, args.attn_reps)
     attn_cold_ms = attn_cold_time(bench, args.cold_reps)
     per_layer_ms = attn_per_layer_time(bench, max(4, args.attn_reps // 4))
+    probe = read_probe_cold(bench.B, float(sum(attn_graph_nodes)) * w.node_bytes, args.cold_reps)
     copy_gbs = device_copy_gbs()
     tree = None if args.no_tree or w.dtype != "bf16" else tree_prefill_time(bench, K, 8)
     phase_ms = phase_times(bench, K)
@@ -304,7 +305,7 @@ def gpu_bench(args, w, K):
     return dict(mode=mode, seconds=float(np.median(run_s)), run_seconds=run_s, eager_seconds=eager_s,
                 attn_ms=attn_ms, nodes=nodes,
                 attn_graph_ms=attn_graph_ms, attn_graph_nodes=attn_graph_nodes, phase_ms=phase_ms,
-                attn_cold_ms=attn_cold_ms, per_layer_ms=per_layer_ms, copy_gbs=copy_gbs,
+                attn_cold_ms=attn_cold_ms, per_layer_ms=per_layer_ms, copy_gbs=copy_gbs, probe=probe,
                 collects=collects, stored=bench.stored, batch=batch, finished=finished, tree=tree,
                 qo_bytes=int(bench.q[0].numel() * bench.q[0].element_size() +
                              bench.out.numel() * bench.out.element_size()))
@@ -501,6 +502,32 @@ def attn_cold_time(bench, reps):
     ev.close()
     del flush
     return float(np.median(ms))
+
+
+def read_probe_cold(B, nbytes, reps):
+    """This GPU's cold read rate in the same run (td_read_probe): a span of `nbytes` (the
+    attention launch's unique K/V bytes) read by the attention's own tile stream (method 0:
+    256 WGs of 8 waves, 16 KiB direct-to-LDS non-temporal loads per wave in flight) and by
+    plain non-temporal register loads (method 1: 1024 WGs of 512 threads, 8 loads per
+    thread in flight), each launch after the same 1 GiB read as the cold attention
+    launches, timed by kernel-timestamp events.  Returns {method: GB/s of the median launch}."""
+    import torch
+    n16 = (int(nbytes) + 15) // 16
+    buf = torch.ones(n16 * 4, dtype=torch.int32, device="cuda")
+    flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    ev = B.KernelEvents()
+    out = {}
+    for method, wgs in ((0, 256), (1, 1024)):
+        sink = torch.zeros(wgs, dtype=torch.int32, device="cuda")
+        ms = []
+        for _ in range(reps):
+            float(flush.sum())
+            B.td_read_probe(buf, method, wgs, sink, ev.start, ev.stop)
+            ms.append(ev.elapsed_ms())
+        out[method] = n16 * 16 / (float(np.median(ms)) / 1e3) / 1e9
+    ev.close()
+    del buf, flush
+    return out
 
 
 def attn_per_layer_time(bench, reps):
@@ -728,6 +755,15 @@ def main():
                      "warm": f"the same launch repeated back to back ({args.attn_reps} per graph replay, median "
                              f"of 5 replays): part of the K/V can stay in the last-level cache",
                      "attn_us_eager_events_mean": round(float(attn_s.mean() * 1e6), 2),
+                     "read_probe_cold_gbs": round(max(r["probe"].values()), 1),
+                     "frac_of_read_probe": round(cold / max(r["probe"].values()), 4),
+                     "read_probe_cold_gbs_by_method": {"tile_stream_lds": round(r["probe"][0], 1),
+                                                       "register_loads": round(r["probe"][1], 1)},
+                     "read_probe": "td_read_probe over a span of the launch's unique K/V bytes, each launch "
+                                   "after the same 1 GiB read (median of the cold launches): the attention's "
+                                   "own tile stream (256 WGs x 8 waves, 16 KiB per wave in flight) and plain "
+                                   "non-temporal register loads (1024 WGs x 512 threads x 8 in flight); the "
+                                   "faster is the measured cold ceiling",
                      "device_copy_gbs": round(r["copy_gbs"], 1),
                      "frac_of_device_copy": round(cold / r["copy_gbs"], 4),
                      "device_copy": "a plain 1 GiB device-to-device copy (torch copy_), read + write bytes "

@@ -312,6 +312,21 @@ const char* td_error_string(const td_ctx* ctx);
 /* Symbolic name of a td_status value. */
 const char* td_status_name(int32_t status);
 
+/* Measurement only (not a step of the decode path): streams `bytes` bytes from d_buf (a
+ * device buffer, 16-byte aligned, bytes a positive multiple of 16) over n_wgs WGs (1 ..
+ * 65536), so that a benchmark can measure this GPU's read rate beside the attention's.
+ * method 0 reads the way the decode attention streams its K/V tiles (WGs of 8 waves, one
+ * contiguous span per WG, 16 KiB per wave in flight as 16-byte direct global -> LDS loads
+ * with the non-temporal policy); method 1 with plain 16-byte non-temporal register loads
+ * (512-thread WGs striding over the buffer, eight loads in flight per thread).  WG g
+ * writes to d_sink[g] (device, n_wgs words) the XOR of the 32-bit words it read; every
+ * word is read once, so the XOR of the sink is the XOR of the buffer.  Optional
+ * kernel-timestamp events (hipExtLaunchKernel): ev_start at the dispatch, ev_stop at the
+ * completion.  Invalid arguments: TD_EINVAL before any HIP call (message in
+ * td_error_string(NULL)).  Asynchronous on `stream`. */
+td_status td_read_probe(const void* d_buf, size_t bytes, int32_t method, int32_t n_wgs, uint32_t* d_sink,
+                        hipEvent_t ev_start, hipEvent_t ev_stop, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -90,6 +90,7 @@ def lib() -> ctypes.CDLL:
         L.td_error_string.argtypes = [vp]
         L.td_error_string.restype = ctypes.c_char_p
         L.beam_topk_static.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.td_read_probe.argtypes = [vp, ctypes.c_size_t, i32, i32, vp, vp, vp, vp]
         L.td_status_name.argtypes = [i32]
         L.td_status_name.restype = ctypes.c_char_p
         L.bbs_create.argtypes = [ctypes.POINTER(BbsDesc), ctypes.POINTER(vp)]
@@ -104,7 +105,7 @@ def lib() -> ctypes.CDLL:
         L.bbs_error_string.argtypes = [vp]
         L.bbs_error_string.restype = ctypes.c_char_p
         for name in ("td_create", "td_destroy", "td_init_prompt", "trie_attn_decode",
-                     "beam_logsoftmax_topk", "beam_topk_append", "beam_topk_static", "trie_append_prune",
+                     "beam_logsoftmax_topk", "beam_topk_append", "beam_topk_static", "td_read_probe", "trie_append_prune",
                      "td_read_state", "td_load_state",
                      "td_get_status", "td_set_kernel_events", "td_read_finished", "trie_tree_attn", "bbs_create", "bbs_destroy",
                      "bbs_init_prompt", "batch_beam_attn_decode", "batch_beam_logsoftmax_topk",
@@ -270,6 +271,19 @@ def beam_topk_static(n_tries, beam_width, vocab, logits, n_live, leaf_score, sel
         _ptr(sel_parent, torch.int32, tb, "sel_parent"), _ptr(sel_token, torch.int32, tb, "sel_token"),
         _ptr(sel_score, torch.float32, tb, "sel_score"), _ptr(sel_logprob, torch.float32, tb, "sel_logprob"),
         _ptr(lse, torch.float32, tb, "lse"), _ptr(status, torch.int32, 2, "status"), _stream(stream))
+    if st != TD_OK:
+        raise TdError(st, td_error_string(None))
+
+
+def td_read_probe(buf, method, n_wgs, sink, ev_start=None, ev_stop=None, stream=None):
+    """td_read_probe: streams all of `buf` (a contiguous device tensor, its byte size a
+    multiple of 16) by `method` (0: the attention's direct-to-LDS tile stream, 1: register
+    loads) over n_wgs WGs; sink: int32 device tensor of n_wgs words (XOR of the words each WG
+    read).  ev_start / ev_stop: raw hipEvent_t handles (KernelEvents) or None."""
+    import torch
+    st = lib().td_read_probe(_ptr(buf, None, None, "buf"), int(buf.numel() * buf.element_size()), int(method),
+                             int(n_wgs), _ptr(sink, torch.int32, int(n_wgs), "sink"), ev_start, ev_stop,
+                             _stream(stream))
     if st != TD_OK:
         raise TdError(st, td_error_string(None))
 

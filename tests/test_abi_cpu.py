@@ -185,3 +185,22 @@ def test_static_selection_needs_its_buffers():
     p = ctypes.c_void_p(0x10000)
     assert L.beam_topk_static(1, 8, 1000, None, p, p, p, p, p, p, None, None, None) == B.TD_EINVAL
     assert L.beam_topk_static(1, 8, 1000, p, p, p, p, p, p, None, None, None, None) == B.TD_EINVAL
+
+
+@pytest.mark.parametrize("buf,nbytes,method,wgs,sink", [
+    (None, 1024, 0, 1, 0x20000),            # no buffer
+    (0x10000, 1024, 0, 1, None),            # no sink
+    (0x10008, 1024, 0, 1, 0x20000),         # buffer not 16-byte aligned
+    (0x10000, 0, 0, 1, 0x20000),            # nothing to read
+    (0x10000, 1000, 0, 1, 0x20000),         # not a multiple of 16 bytes
+    (0x10000, 1024, 2, 1, 0x20000),         # no such method
+    (0x10000, 1024, 1, 0, 0x20000),         # no WG
+    (0x10000, 1024, 1, 65537, 0x20000)])    # too many WGs
+def test_read_probe_checks_its_arguments_on_the_host(buf, nbytes, method, wgs, sink):
+    """td_read_probe (measurement only) rejects invalid arguments before any HIP call: here
+    with dummy pointers and no GPU."""
+    L = B.lib()
+    st = L.td_read_probe(None if buf is None else ctypes.c_void_p(buf), nbytes, method, wgs,
+                         None if sink is None else ctypes.c_void_p(sink), None, None, None)
+    assert st == B.TD_EINVAL, L.td_status_name(st)
+    assert L.td_error_string(None).decode().startswith("td_read_probe")
