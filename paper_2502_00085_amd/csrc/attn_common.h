@@ -84,6 +84,47 @@ __device__ inline void move_rows_block(const DevState& s, int t, int l, int g, u
   }
 }
 
+// The same copy in batches of 4 16-byte chunks per thread held in registers (for a block
+// whose LDS and registers are free, at the end of its work): every load of a batch goes
+// out before any is used (two dependent round trips per batch: the move table, then the
+// rows), every read of a batch completes (barrier) before its writes, and a later batch
+// reads only slots above every slot an earlier batch wrote.  Ends with a barrier when there
+// is anything to move.  Call from uniform control flow.
+template <typename T>
+__device__ inline void move_rows_regs(const DevState& s, int t, int l, int g) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));  // (a vector: kept in registers)
+  constexpr int C = 4;
+  const int nm = s.n_moves[t];
+  if (nm == 0) return;
+  const int cpr = s.D * (int)sizeof(T) / 16;  // 16-byte chunks per row
+  const int per_row = 2 * cpr;                // K and V
+  u32x4* kp = reinterpret_cast<u32x4*>(static_cast<T*>(s.k_pool) + pool_row(s, t, l, g, 0));
+  u32x4* vp = reinterpret_cast<u32x4*>(static_cast<T*>(s.v_pool) + pool_row(s, t, l, g, 0));
+  const int2* mv = s.moves + (size_t)t * s.cap;
+  const int total = nm * per_row;
+  const int nt = (int)blockDim.x;
+  for (int c0 = 0; c0 < total; c0 += C * nt) {
+    int ss[C], ds[C], ch[C];  // source and destination slot, chunk of the row (K then V)
+    u32x4 v[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      // (past the end: the batch's last chunk again, read and not written)
+      const int idx = min(c0 + c * nt + (int)threadIdx.x, total - 1);
+      const int2 m = mv[idx / per_row];
+      ss[c] = m.x;
+      ds[c] = m.y;
+      ch[c] = idx % per_row;
+    }
+#pragma unroll
+    for (int c = 0; c < C; ++c) v[c] = (ch[c] < cpr ? kp : vp)[(size_t)ss[c] * cpr + ch[c] % cpr];
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+      if (c0 + c * nt + (int)threadIdx.x < total) (ch[c] < cpr ? kp : vp)[(size_t)ds[c] * cpr + ch[c] % cpr] = v[c];
+  }
+  __syncthreads();
+}
+
 // Stores the pending leaves' K/V rows of one (trie, layer, KV head) into the pools
 // (16-byte chunks, whole block).
 template <typename T>

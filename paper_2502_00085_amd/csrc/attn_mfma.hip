@@ -152,18 +152,16 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     n0 = lo + u.split * per;
     n1 = min(N, n0 + per);
   }
-  if (u.split >= act) {
+  if (RB == 1 && u.split >= act) {
     // a split the span does not need: its partials are marked empty (sum 0) for the
     // combine; nothing else is due from it (moves come with single-split launches, leaf
-    // rows with the range that holds them)
+    // rows with the range that holds them).  (Two row blocks: such a WG runs on with an
+    // empty range and stores empty partials the usual way; an early exit there costs the
+    // main loop registers.)
     if (threadIdx.x < kRows) {
-#pragma unroll
-      for (int rbk = 0; rbk < RB; ++rbk) {
-        const int unit = RB == 1 ? u.unit : (u.unit / a.row_blocks) * a.row_blocks32 + u.rb * RB + rbk;
-        float* pp = s.attn_part + (((size_t)unit * a.splits + u.split) * kRows + threadIdx.x) * (D + 2);
-        pp[D] = kNegBig;
-        pp[D + 1] = 0.0f;
-      }
+      float* pp = s.attn_part + (((size_t)u.unit * a.splits + u.split) * kRows + threadIdx.x) * (D + 2);
+      pp[D] = kNegBig;
+      pp[D + 1] = 0.0f;
     }
     return;
   }
@@ -670,8 +668,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   // the moved rows to their new slots (every read of this call is done), then the pending
   // leaves' rows into the pool, for later calls (this call read them from k_new / v_new)
   if (late_copy) {
-    __syncthreads();  // the merge buffers are free
-    move_rows_block<__bf16>(s, u.t, lab, u.g, reinterpret_cast<uint4*>(lds), C::LDS / 16);
+    __syncthreads();  // every wave's reads of this call are done
+    // register batches where there is room; the two-row-block kernel, at its register
+    // limit, stages through the (now free) LDS instead
+    if constexpr (RB == 1)
+      move_rows_regs<__bf16>(s, u.t, lab, u.g);
+    else
+      move_rows_block<__bf16>(s, u.t, lab, u.g, reinterpret_cast<uint4*>(lds), C::LDS / 16);
   }
   if (leaves_here && !leaves_staged) store_leaf_kv<__bf16>(s, a, u, base, N, n_live);
 }

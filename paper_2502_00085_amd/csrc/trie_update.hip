@@ -55,37 +55,44 @@ __global__ __launch_bounds__(kAppThreads) void k_append_prune(DevState s, const 
 }
 
 // The paper's index_select compaction of the KV cache, restricted to rows that move.
-// One WG per (trie, layer, KV head, K|V); moves are staged through LDS in ascending-source
-// batches so that in-place copies never overwrite an unread source.
+// One WG per (trie, layer, KV head, K|V); the moves go in ascending-source batches of 8
+// 16-byte chunks per thread held in registers (every load of a batch issued before any is
+// used), all reads of a batch before its writes, so that in-place copies never overwrite
+// an unread source.
 constexpr int kMoveThreads = 256;
-constexpr int kMoveLdsBytes = 64 * 1024;
+constexpr int kMoveBatch = 8;
 
 __global__ __launch_bounds__(kMoveThreads) void k_move_rows(DevState s, int layer_begin, int n_layers) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));  // (a vector: kept in registers)
   const int which = blockIdx.x & 1;
   const int x = blockIdx.x >> 1;              // (t * n_layers + li) * Hkv + g
   const int g = x % s.Hkv, li = (x / s.Hkv) % n_layers, t = x / (s.Hkv * n_layers);
   const int pair = (t * s.L + layer_begin + li) * s.Hkv + g;
   const int nm = s.n_moves[t];
   if (nm == 0) return;
-  extern __shared__ uint4 stage[];
   const int esz = s.dtype == TD_F32 ? 4 : 2;
   const int row_chunks = s.D * esz / 16;      // 16-byte chunks per row
-  const int rows_per_batch = kMoveLdsBytes / (row_chunks * 16);
-  uint4* pool = reinterpret_cast<uint4*>(which ? s.v_pool : s.k_pool) +
-                (size_t)pair * s.cap * row_chunks;
+  u32x4* pool = reinterpret_cast<u32x4*>(which ? s.v_pool : s.k_pool) + (size_t)pair * s.cap * row_chunks;
   const int2* mv = s.moves + (size_t)t * s.cap;
-  for (int i0 = 0; i0 < nm; i0 += rows_per_batch) {
-    const int cnt = min(rows_per_batch, nm - i0);
-    for (int c = threadIdx.x; c < cnt * row_chunks; c += kMoveThreads) {
-      const int r = c / row_chunks, k = c % row_chunks;
-      stage[c] = pool[(size_t)mv[i0 + r].x * row_chunks + k];
+  const int total = nm * row_chunks;
+  for (int c0 = 0; c0 < total; c0 += kMoveBatch * kMoveThreads) {
+    int ss[kMoveBatch], ds[kMoveBatch], ch[kMoveBatch];  // source, destination slot; chunk
+    u32x4 v[kMoveBatch];
+#pragma unroll
+    for (int c = 0; c < kMoveBatch; ++c) {
+      // (past the end: the batch's last chunk again, read and not written)
+      const int idx = min(c0 + c * kMoveThreads + (int)threadIdx.x, total - 1);
+      const int2 m = mv[idx / row_chunks];
+      ss[c] = m.x;
+      ds[c] = m.y;
+      ch[c] = idx % row_chunks;
     }
+#pragma unroll
+    for (int c = 0; c < kMoveBatch; ++c) v[c] = pool[(size_t)ss[c] * row_chunks + ch[c]];
     __syncthreads();
-    for (int c = threadIdx.x; c < cnt * row_chunks; c += kMoveThreads) {
-      const int r = c / row_chunks, k = c % row_chunks;
-      pool[(size_t)mv[i0 + r].y * row_chunks + k] = stage[c];
-    }
-    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < kMoveBatch; ++c)
+      if (c0 + c * kMoveThreads + (int)threadIdx.x < total) pool[(size_t)ds[c] * row_chunks + ch[c]] = v[c];
   }
 }
 
@@ -107,7 +114,7 @@ hipError_t launch_append_prune(const DevState& s, const int32_t* sel_parent,
 
 hipError_t launch_move_rows(const DevState& s, int layer_begin, int n_layers, hipStream_t st,
                             hipEvent_t ev0, hipEvent_t ev1) {
-  hipExtLaunchKernelGGL(k_move_rows, dim3(s.T * n_layers * s.Hkv * 2), dim3(kMoveThreads), kMoveLdsBytes,
+  hipExtLaunchKernelGGL(k_move_rows, dim3(s.T * n_layers * s.Hkv * 2), dim3(kMoveThreads), 0,
                         st, ev0, ev1, 0, s, layer_begin, n_layers);
   return hipGetLastError();
 }
