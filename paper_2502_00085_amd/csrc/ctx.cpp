@@ -33,6 +33,8 @@ namespace {
 
 thread_local std::string g_create_err;
 
+constexpr long kOneRoundWgs = 256;  // attention WGs that run at once (one per CU)
+
 td_status fail(td_ctx* c, td_status st, const char* fmt, ...) {
   char buf[512];
   va_list ap;
@@ -268,7 +270,13 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   // Rows moved by the last compaction are copied before the layer's first attention: by
   // the attention WGs themselves when each owns a whole (layer, KV head) and every layer
   // of the call is still due (unless the copy is being timed), else by a copy launch per
-  // due layer range.
+  // due layer range.  The two-row-block kernel has room to stage only a few moved rows
+  // with its first tile; more are copied by each WG after its output, a latency that a
+  // launch of several WG rounds pays once per round on every CU.  There the copy launch
+  // is cheaper (measured with 16 tries of 16 beams at the Llama shape, 31 moved rows per
+  // trie on average: 32 us for the launch against about 140 us inside the attention).
+  const long attn_wgs = (long)s.T * n_layers * s.Hkv * a.row_blocks * a.splits;
+  const bool fuse_moves = a.rb_per_wg == 1 || attn_wgs <= kOneRoundWgs;
   a.moves = 0;
   std::vector<std::pair<int, int>> due;
   if (c->pending && c->moves_pending) {
@@ -282,7 +290,8 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
       due.emplace_back(l, j - l);
       l = j;
     }
-    if (due.size() == 1 && due[0].second == n_layers && a.splits == 1 && a.row_blocks == 1 && !mv0) {
+    if (due.size() == 1 && due[0].second == n_layers && a.splits == 1 && a.row_blocks == 1 && !mv0 &&
+        fuse_moves) {
       a.moves = 1;
       due.clear();
     }
