@@ -41,10 +41,13 @@ __device__ inline AttnUnit attn_unit(const DevState& s, const AttnArgs& a) {
 // First logical slot inside the sliding window of a query at depth D (depth is
 // non-decreasing along the slots): the smallest n with D - depth[n] < W, i.e. with
 // depth[n] > D - W.  Block-parallel (call from uniform control flow, every thread).
-__device__ inline int window_lo(const DevState& s, int t, int base, int N, int D) {
-  __shared__ int scratch[16];
+__device__ inline int window_lo(const DevState& s, int t, int base, int N, int D, int* scratch) {
   if (s.W <= 0) return 0;
   return block_first_above(s.depth + (size_t)t * s.cap + base, N, D - s.W, scratch);
+}
+__device__ inline int window_lo(const DevState& s, int t, int base, int N, int D) {
+  __shared__ int scratch[16];
+  return window_lo(s, t, base, N, D, scratch);
 }
 
 // Pool row of (trie t, absolute layer l, KV head g, physical slot p), in elements.

@@ -69,7 +69,8 @@ struct MfmaCfg {
   static constexpr int O_LDS = NW * kRows * OS * 4 + 3 * NW * kRows * 4 + 2 * kRows * 4;
   // past both the tiles and the merge buffers: the moved rows' sources and staged copies
   static constexpr int MOVE0 = V_LDS > O_LDS ? V_LDS : O_LDS;
-  static constexpr int LDS = 160 * 1024 - 256;  // (the rest: the window search's scratch)
+  // 8 waves: one WG per CU (the rest: the window search's scratch); 4 waves: two per CU
+  static constexpr int LDS = NW == 8 ? 160 * 1024 - 256 : 80 * 1024;
   static constexpr int MOVE_LDS = LDS - MOVE0;
   static constexpr int ROW_BYTES = 4 * D;      // K + V of one node row
 };
@@ -86,6 +87,11 @@ struct MfmaCfg {
 // at G = 4) one WG takes both blocks: each wave's tile serves 64 rows, instead of two WGs
 // streaming the same nodes side by side.
 //
+// NW = 4 (two-row-block decode only): WGs of 4 waves, two per CU, with tiles and Q alone in
+// their LDS (no staging of moved or leaf rows, no fused row copy).  A launch of many WG
+// rounds then overlaps one WG's prologue and merge, when it streams nothing, with the other
+// WG's tile stream.
+//
 // NT: the K/V tile loads carry the non-temporal cache policy.  A decode launch whose node
 // range is streamed by one WG reads each row once per call, and the streaming policy
 // reads a span that the last-level cache cannot hold markedly faster (measured on this
@@ -93,8 +99,9 @@ struct MfmaCfg {
 // sibling WGs of other row blocks read the same range again from L2 (xcd_group) and for
 // the tree kernel, whose row blocks share the keys the same way.
 template <int D, int NW, bool TREE, int RB, bool NT>
-__global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
+__global__ __launch_bounds__(NW * 64, 2) void k_attn_mfma(DevState s, AttnArgs a) {
   static_assert(RB == 1 || (RB == 2 && !TREE), "two row blocks per WG: decode only");
+  static_assert(NW == 8 || (NW == 4 && RB == 2), "4-wave WGs: two-row-block decode only");
   static_assert(!(NT && TREE), "tree launches share keys between row blocks");
   constexpr int kTileCpol = NT ? 2 : 0;  // cache-policy bits of the tile loads (2: nt)
   using C = MfmaCfg<D, NW>;
@@ -147,7 +154,10 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     n1 = min(lo + span, n0 + per);
   } else {
     row_ok = r < s.b * G && owner < n_live;
-    lo = window_lo(s, u.t, base, N, Dq);
+    if constexpr (NW == 4)
+      lo = window_lo(s, u.t, base, N, Dq, reinterpret_cast<int*>(lds));  // (before any tile load)
+    else
+      lo = window_lo(s, u.t, base, N, Dq);
     const int per = split_range(N - lo, a.splits, NW, a.all_splits, &act);
     n0 = lo + u.split * per;
     n1 = min(N, n0 + per);
@@ -191,13 +201,16 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   // issued with the first tile, then written after the main loop.  More: the table goes to
   // LDS (one block barrier) and the rows are copied at the end.  More than that table
   // holds: copied first.  The leaf store, whose slots may be sources of moves, follows.
-  // (two row blocks: their query rows sit in LDS, ahead of the staging area)
+  // (two row blocks: their query rows sit in LDS, ahead of the staging area; with 4 waves
+  // right after the tiles, inside the merge buffers, which are used only after the loop)
   constexpr int kQBytes = RB == 2 ? RB * kRows * D * 2 : 0;
-  constexpr int kMove0 = C::MOVE0 + kQBytes, kMoveLds = C::MOVE_LDS - kQBytes;
-  static_assert(kMoveLds > 0, "LDS for the staging area");
+  constexpr int kQ0 = NW == 4 ? C::V_LDS : C::MOVE0;
+  constexpr int kMove0 = kQ0 + kQBytes, kMoveLds = C::LDS - kMove0;
+  static_assert(kMoveLds >= 0 && (NW == 4 || kMoveLds > 0), "LDS for the staging area");
   // (the count and the first destination come with the header: no dependent loads before
-  // the first tile)
-  const int nmoves = a.moves ? h.n_moves : 0;
+  // the first tile; 4-wave WGs have no room to stage and never copy: the host launches
+  // the row copy separately)
+  const int nmoves = kMoveLds > 0 && a.moves ? h.n_moves : 0;
   const int first_moved = nmoves > 0 ? h.first_moved : INT_MAX;
   // The pending leaves' rows of a WG whose range holds them are staged the same way (from
   // k_new / v_new), ahead of the moved rows, unless the moved rows are copied through the
@@ -289,9 +302,22 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   };
   // this lane's K operand chunks for the 32x32x16 steps: row col, logical chunk
   // hh * CPR / 2 + t, rotated by col
-  int kread[C::KSTEPS];
+  // (held in registers by the one-row-block kernels; the two-row-block kernel, short of
+  // registers, recomputes them per tile)
+  int kread[RB == 1 ? C::KSTEPS : 1];
+  if constexpr (RB == 1) {
 #pragma unroll
-  for (int t = 0; t < C::KSTEPS; ++t) kread[t] = col * (2 * D) + (hh * (C::CPR / 2) + t + col) % C::CPR * 16;
+    for (int t = 0; t < C::KSTEPS; ++t) kread[t] = col * (2 * D) + (hh * (C::CPR / 2) + t + col) % C::CPR * 16;
+  }
+  auto kaddr = [&](int t) __attribute__((always_inline)) -> int {
+    if constexpr (RB == 1) {
+      return kread[t];
+    } else {
+      int c = col;
+      asm volatile("" : "+v"(c));  // (keeps the offsets from being hoisted into registers)
+      return c * (2 * D) + (hh * (C::CPR / 2) + t + c) % C::CPR * 16;
+    }
+  };
 
   // K and V rows of a tile -> the wave's LDS buffers (coalesced 16-byte direct loads; the
   // pending leaves' rows come from k_new / v_new, moved rows from their sources); in the
@@ -398,7 +424,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
   // this lane's query row of each row block (B operand of S^T): half hh of its d range
   int beam_bit[RB];
   bool rok[RB];
-  unsigned char* qlds = lds + C::MOVE0;  // (two row blocks) [64 rows][D], chunks rotated by row
+  unsigned char* qlds = lds + kQ0;  // (two row blocks) [64 rows][D], chunks rotated by row
 #pragma unroll
   for (int k = 0; k < RB; ++k) {
     const int rk = r + k * kRows, ok_ = k == 0 ? row_ok : (rk < s.b * G && rk / G < n_live);
@@ -435,14 +461,15 @@ __global__ __launch_bounds__(NW * 64) void k_attn_mfma(DevState s, AttnArgs a) {
     // nodes 16uu + 8 half + 4hh + tm')
     bf16x8 kv[C::KSTEPS];
 #pragma unroll
-    for (int t = 0; t < C::KSTEPS; ++t) kv[t] = *reinterpret_cast<const bf16x8*>(kbuf + kread[t]);
+    for (int t = 0; t < C::KSTEPS; ++t) kv[t] = *reinterpret_cast<const bf16x8*>(kbuf + kaddr(t));
     // (two row blocks: both blocks' scores first, so that the K operands are dead before the
     // V operands are read; the query rows come from LDS)
     f32x16 acc2[RB];
     if constexpr (RB == 2) {
 #pragma unroll
       for (int rbk = 0; rbk < RB; ++rbk) {
-        const int row = rbk * kRows + col;
+        int row = rbk * kRows + col;
+        asm volatile("" : "+v"(row));  // (the read offsets are recomputed per tile, not held)
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc2[rbk][v] = 0.0f;
 #pragma unroll
@@ -704,9 +731,12 @@ hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st
   if (a.rb_per_wg < 1 || a.rb_per_wg > 2 || (a.rb_per_wg == 2 && a.tree) ||
       a.row_blocks32 > a.row_blocks * a.rb_per_wg || a.row_blocks32 <= (a.row_blocks - 1) * a.rb_per_wg)
     return hipErrorInvalidValue;
-  const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * a.splits), block(kNW * 64);
+  if (a.half_wgs && (a.rb_per_wg != 2 || a.moves)) return hipErrorInvalidValue;  // (no staging room)
+  const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * a.splits), block(kNW * 64), half(kNW * 32);
 #define LAUNCH_MFMA(DD)                                                                                      \
   (a.tree ? hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW, true, 1, false>), grid, block, 0, st, ev0, ev1, 0, s, a) \
+   : a.half_wgs                                                                                                \
+       ? hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW / 2, false, 2, true>), grid, half, 0, st, ev0, ev1, 0, s, a) \
    : a.rb_per_wg == 2                                                                                          \
        ? hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW, false, 2, true>), grid, block, 0, st, ev0, ev1, 0, s, a)  \
    : a.xcd_group                                                                                               \

@@ -113,6 +113,8 @@ struct AttnArgs {
                                    // grid's row_blocks counts WGs, of rb_per_wg blocks each
   int all_splits = 0;              // (matrix-core kernel) 1: every split WG takes a share of the
                                    // nodes (a forced split count); 0: only as many as needed
+  int half_wgs = 0;                // (two-row-block decode) 1: 4-wave WGs, two per CU; no fused
+                                   // row copy (moves == 0)
 };
 
 hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const int32_t* d_tokens,

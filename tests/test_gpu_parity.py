@@ -279,6 +279,23 @@ def test_two_row_blocks_several_tries_without_splits():
                    prompt_min=20, prompt_max=70, vocab=500, alpha=0.0, steps=6), seed=42)
 
 
+# more than one WG round of two-row-block units: 4-wave WGs, two per CU, and the moved rows
+# copied by their own launch before the attention
+@pytest.mark.parametrize("d", [64, 96, 128])
+def test_two_row_blocks_half_wgs_several_rounds(d):
+    # 5 tries x 4 layers x 16 KV heads = 320 units
+    run_case(small(n_tries=5, n_layers=4, n_q_heads=64, n_kv_heads=16, head_dim=d, beam_width=16,
+                   prompt_min=20, prompt_max=90, vocab=500, alpha=0.0, qkv_std=1.0 / np.sqrt(d), steps=6),
+             seed=70 + d, impl=B.TD_ATTN_MFMA)
+
+
+def test_two_row_blocks_half_wgs_window_deferred_collection():
+    # 3 tries x 6 layers x 16 KV heads = 288 units, a window and collection every 3 positions
+    run_case(small(n_tries=3, n_layers=6, n_q_heads=64, n_kv_heads=16, head_dim=64, beam_width=16,
+                   prompt_min=30, prompt_max=60, vocab=500, window=24, gc_interval=3, alpha=0.3, steps=12),
+             seed=75)
+
+
 @pytest.mark.parametrize("mode", ["driven", "scripted"])
 def test_smallest_vocabulary(mode):
     # V = b: at step 1 every candidate is selected; afterwards b of b * b
