@@ -87,10 +87,11 @@ struct MfmaCfg {
 // at G = 4) one WG takes both blocks: each wave's tile serves 64 rows, instead of two WGs
 // streaming the same nodes side by side.
 //
-// NW = 4 (two-row-block decode only): WGs of 4 waves, two per CU, with tiles and Q alone in
-// their LDS (no staging of moved or leaf rows, no fused row copy).  A launch of many WG
-// rounds then overlaps one WG's prologue and merge, when it streams nothing, with the other
-// WG's tile stream.
+// NW = 4 (decode only): WGs of 4 waves, two per CU.  With two row blocks, tiles and Q alone
+// fill their LDS (no staging of moved or leaf rows, no fused row copy), and a launch of many
+// WG rounds overlaps one WG's prologue and merge, when it streams nothing, with the other
+// WG's tile stream.  With one row block (12 KiB left to stage rows), a launch of 257 to 512
+// WGs runs in one round instead of two.
 //
 // NT: the K/V tile loads carry the non-temporal cache policy.  A decode launch whose node
 // range is streamed by one WG reads each row once per call, and the streaming policy
@@ -101,7 +102,7 @@ struct MfmaCfg {
 template <int D, int NW, bool TREE, int RB, bool NT>
 __global__ __launch_bounds__(NW * 64, 2) void k_attn_mfma(DevState s, AttnArgs a) {
   static_assert(RB == 1 || (RB == 2 && !TREE), "two row blocks per WG: decode only");
-  static_assert(NW == 8 || (NW == 4 && RB == 2), "4-wave WGs: two-row-block decode only");
+  static_assert(NW == 8 || (NW == 4 && !TREE), "4-wave WGs: decode only");
   static_assert(!(NT && TREE), "tree launches share keys between row blocks");
   constexpr int kTileCpol = NT ? 2 : 0;  // cache-policy bits of the tile loads (2: nt)
   using C = MfmaCfg<D, NW>;
@@ -204,9 +205,9 @@ __global__ __launch_bounds__(NW * 64, 2) void k_attn_mfma(DevState s, AttnArgs a
   // (two row blocks: their query rows sit in LDS, ahead of the staging area; with 4 waves
   // right after the tiles, inside the merge buffers, which are used only after the loop)
   constexpr int kQBytes = RB == 2 ? RB * kRows * D * 2 : 0;
-  constexpr int kQ0 = NW == 4 ? C::V_LDS : C::MOVE0;
+  constexpr int kQ0 = NW == 4 && RB == 2 ? C::V_LDS : C::MOVE0;
   constexpr int kMove0 = kQ0 + kQBytes, kMoveLds = C::LDS - kMove0;
-  static_assert(kMoveLds >= 0 && (NW == 4 || kMoveLds > 0), "LDS for the staging area");
+  static_assert(kMoveLds >= 0 && (NW == 4 && RB == 2 || kMoveLds > 0), "LDS for the staging area");
   // (the count and the first destination come with the header: no dependent loads before
   // the first tile; 4-wave WGs have no room to stage and never copy: the host launches
   // the row copy separately)
@@ -731,12 +732,14 @@ hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st
   if (a.rb_per_wg < 1 || a.rb_per_wg > 2 || (a.rb_per_wg == 2 && a.tree) ||
       a.row_blocks32 > a.row_blocks * a.rb_per_wg || a.row_blocks32 <= (a.row_blocks - 1) * a.rb_per_wg)
     return hipErrorInvalidValue;
-  if (a.half_wgs && (a.rb_per_wg != 2 || a.moves)) return hipErrorInvalidValue;  // (no staging room)
+  if (a.half_wgs && (a.tree || a.xcd_group || (a.rb_per_wg == 2 && a.moves))) return hipErrorInvalidValue;
   const dim3 grid(s.T * a.n_layers * s.Hkv * a.row_blocks * a.splits), block(kNW * 64), half(kNW * 32);
 #define LAUNCH_MFMA(DD)                                                                                      \
   (a.tree ? hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW, true, 1, false>), grid, block, 0, st, ev0, ev1, 0, s, a) \
-   : a.half_wgs                                                                                                \
+   : a.half_wgs && a.rb_per_wg == 2                                                                            \
        ? hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW / 2, false, 2, true>), grid, half, 0, st, ev0, ev1, 0, s, a) \
+   : a.half_wgs                                                                                                \
+       ? hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW / 2, false, 1, true>), grid, half, 0, st, ev0, ev1, 0, s, a) \
    : a.rb_per_wg == 2                                                                                          \
        ? hipExtLaunchKernelGGL((k_attn_mfma<DD, kNW, false, 2, true>), grid, block, 0, st, ev0, ev1, 0, s, a)  \
    : a.xcd_group                                                                                               \

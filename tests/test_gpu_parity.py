@@ -296,6 +296,23 @@ def test_two_row_blocks_half_wgs_window_deferred_collection():
              seed=75)
 
 
+# one row block and 257..512 units: 4-wave WGs, two per CU, in one round (rows moved by the
+# collection staged and copied by the attention WGs themselves)
+@pytest.mark.parametrize("d", [64, 128])
+def test_one_row_block_half_wgs_one_round(d):
+    # 5 tries x 4 layers x 16 KV heads = 320 units of b G = 32 rows
+    run_case(small(n_tries=5, n_layers=4, n_q_heads=64, n_kv_heads=16, head_dim=d, beam_width=8,
+                   prompt_min=20, prompt_max=90, vocab=500, alpha=0.0, qkv_std=1.0 / np.sqrt(d), steps=6),
+             seed=80 + d, impl=B.TD_ATTN_MFMA)
+
+
+def test_one_row_block_half_wgs_window_deferred_collection_fused():
+    # 3 tries x 6 layers x 16 heads (MHA) = 288 units, a window, collection every 3 positions
+    run_case(small(n_tries=3, n_layers=6, n_q_heads=16, n_kv_heads=16, head_dim=96, beam_width=4,
+                   prompt_min=30, prompt_max=60, vocab=500, window=20, gc_interval=3, alpha=0.3,
+                   qkv_std=1.0 / np.sqrt(96.0), steps=12), seed=85, fused=True)
+
+
 @pytest.mark.parametrize("mode", ["driven", "scripted"])
 def test_smallest_vocabulary(mode):
     # V = b: at step 1 every candidate is selected; afterwards b of b * b
