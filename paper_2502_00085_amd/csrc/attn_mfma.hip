@@ -87,11 +87,10 @@ struct MfmaCfg {
 // at G = 4) one WG takes both blocks: each wave's tile serves 64 rows, instead of two WGs
 // streaming the same nodes side by side.
 //
-// NW = 4 (decode only): WGs of 4 waves, two per CU.  With two row blocks, tiles and Q alone
-// fill their LDS (no staging of moved or leaf rows, no fused row copy), and a launch of many
-// WG rounds overlaps one WG's prologue and merge, when it streams nothing, with the other
-// WG's tile stream.  With one row block (12 KiB left to stage rows), a launch of 257 to 512
-// WGs runs in one round instead of two.
+// NW = 4 (decode launches of more WGs than CUs): WGs of 4 waves, two per CU, so that one
+// WG's prologue and merge, when it streams nothing, overlap the other WG's tile stream.
+// With two row blocks, tiles and Q alone fill their LDS (no staging of moved or leaf rows,
+// no fused row copy); with one row block 12 KiB are left to stage rows.
 //
 // NT: the K/V tile loads carry the non-temporal cache policy.  A decode launch whose node
 // range is streamed by one WG reads each row once per call, and the streaming policy
@@ -209,8 +208,8 @@ __global__ __launch_bounds__(NW * 64, 2) void k_attn_mfma(DevState s, AttnArgs a
   constexpr int kMove0 = kQ0 + kQBytes, kMoveLds = C::LDS - kMove0;
   static_assert(kMoveLds >= 0 && (NW == 4 && RB == 2 || kMoveLds > 0), "LDS for the staging area");
   // (the count and the first destination come with the header: no dependent loads before
-  // the first tile; 4-wave WGs have no room to stage and never copy: the host launches
-  // the row copy separately)
+  // the first tile; 4-wave WGs over two row blocks have no room to stage and never copy:
+  // the host launches the row copy separately)
   const int nmoves = kMoveLds > 0 && a.moves ? h.n_moves : 0;
   const int first_moved = nmoves > 0 ? h.first_moved : INT_MAX;
   // The pending leaves' rows of a WG whose range holds them are staged the same way (from
@@ -725,8 +724,6 @@ int attn_choose_splits(const DevState& s, int n_layers, int row_blocks) {
 
 hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
                             hipEvent_t ev1) {
-  // (4-wave WGs, two per CU, measured slower than 8-wave WGs one per CU on every shape
-  // here, also for launches of several WG rounds)
   // (32-row blocks: row_blocks32 = row_blocks WGs of rb_per_wg blocks each, the last
   // possibly half used)
   if (a.rb_per_wg < 1 || a.rb_per_wg > 2 || (a.rb_per_wg == 2 && a.tree) ||
