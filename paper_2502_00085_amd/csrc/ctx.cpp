@@ -277,11 +277,9 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   // trie on average: 32 us for the launch against about 140 us inside the attention).
   const long attn_wgs = (long)s.T * n_layers * s.Hkv * a.row_blocks * a.splits;
   const bool fuse_moves = a.rb_per_wg == 1 || attn_wgs <= kOneRoundWgs;
-  // (a launch of several WG rounds runs 4-wave WGs, two per CU: one WG's prologue and merge
-  // overlap the other's tile stream)
-  a.half_wgs = mfma && ((a.rb_per_wg == 2 && attn_wgs > kOneRoundWgs) ||
-                        (a.rb_per_wg == 1 && a.row_blocks == 1 && a.splits == 1 && attn_wgs > kOneRoundWgs))
-                   ? 1 : 0;
+  // (an unsplit launch of several WG rounds, one WG per unit, runs 4-wave WGs, two per CU:
+  // one WG's prologue and merge overlap the other's tile stream)
+  a.half_wgs = mfma && a.splits == 1 && a.row_blocks == 1 && attn_wgs > kOneRoundWgs ? 1 : 0;
   a.moves = 0;
   std::vector<std::pair<int, int>> due;
   if (c->pending && c->moves_pending) {
