@@ -25,6 +25,7 @@
 // (Two launches instead of a last-arriving-WG merge: a device-scope fence costs an L2
 // writeback + invalidate per WG on this multi-XCD part.)
 #include <mutex>
+#include <type_traits>
 
 #include "trie_append.h"
 
@@ -227,57 +228,76 @@ __global__ __launch_bounds__(NWC * 64) void k_topb_chunk(DevState s, const float
   if (wave == 0) exp_tab[lane] = exp2((double)lane * 0.015625);  // (read after the barrier below)
   const size_t list = ((size_t)t * b + r) * s.lse_chunks + c;
   const size_t lists = (size_t)s.T * b * s.lse_chunks;
+  // PLAIN: a full chunk without the end-of-sequence token, the common case: no per-logit
+  // range or token test, and no per-logit test for a NaN or +inf logit (either makes the
+  // sum NaN by itself: x - max is then NaN for that logit; only a chunk whose maximum is
+  // -inf, i.e. every logit -inf or NaN, needs the explicit test)
+  auto body = [&](auto plain_t, float& m, double& acc, bool& bad) __attribute__((always_inline)) {
+    constexpr bool PLAIN = decltype(plain_t)::value;
+#pragma unroll
+    for (int q = 0; q < SPW; ++q) {
+      const int sw = wave * SPW + q;
+      // this lane's two largest logits of the sub-chunk, by order of value (a later logit
+      // replaces an equal one only if larger: the lower flat index wins ties)
+      uint32_t o1 = 0, o2 = 0;
+      int i1 = 0, i2 = 0;
+#pragma unroll
+      for (int i = 0; i < kChunkPer; ++i) {
+        const int v = v0 + i * kChunkThreads + sw * 64 + lane;
+        m = fmaxf(m, x[q][i]);
+        // (the end-of-sequence token, if any, is not a candidate for the next beams;
+        // order 0 = no candidate)
+        const uint32_t o = PLAIN || (v < V && v != s.eos) ? ord_raw(x[q][i]) : 0u;
+        const bool gt1 = o > o1, gt2 = o > o2;
+        o2 = gt1 ? o1 : (gt2 ? o : o2);
+        i2 = gt1 ? i1 : (gt2 ? i : i2);
+        o1 = gt1 ? o : o1;
+        i1 = gt1 ? i : i1;
+      }
+      const uint32_t flat = (uint32_t)r * (uint32_t)V + (uint32_t)(v0 + sw * 64 + lane);
+      const uint64_t k1 = o1 ? ((uint64_t)o1 << 32) | (uint64_t)(0xffffffffu - (flat + (uint32_t)(i1 * kChunkThreads))) : 0;
+      const uint64_t k2 = o2 ? ((uint64_t)o2 << 32) | (uint64_t)(0xffffffffu - (flat + (uint32_t)(i2 * kChunkThreads))) : 0;
+      // the sub-chunk's largest key, and its second largest (the owner of the largest offers
+      // its own second; keys are unique)
+      const uint64_t km = wave_max_u64(k1);
+      const uint64_t km2 = wave_max_u64(k1 == km ? k2 : k1);
+      if (lane == 0) {
+        s.topk_keys[sw * lists + list] = km;  // 0 when the sub-chunk holds no candidate
+        s.topk_keys[s.topk_half + sw * lists + list] = km2;
+      }
+    }
+    m = __ockl_wfred_max_f32(m);
+    if (lane == 0) wm[wave] = m;
+    __syncthreads();
+    m = wm[0];
+#pragma unroll
+    for (int w = 1; w < NWC; ++w) m = fmaxf(m, wm[w]);
+    const double md = (double)m;
+    if (PLAIN && md != -INFINITY) {
+#pragma unroll
+      for (int q = 0; q < SPW; ++q)
+#pragma unroll
+        for (int i = 0; i < kChunkPer; ++i) acc += exp_nonpos((double)x[q][i] - md, exp_tab);
+    } else {
+#pragma unroll
+      for (int q = 0; q < SPW; ++q)
+#pragma unroll
+        for (int i = 0; i < kChunkPer; ++i) {
+          const int v = v0 + i * kChunkThreads + (wave * SPW + q) * 64 + lane;
+          // (a chunk whose logits are all -inf adds nothing; exp(-inf - -inf) would be NaN)
+          if (v < V && md != -INFINITY) acc += exp_nonpos((double)x[q][i] - md, exp_tab);
+          bad |= v < V && !(x[q][i] < INFINITY);
+        }
+    }
+  };
   float m = -INFINITY;
-#pragma unroll
-  for (int q = 0; q < SPW; ++q) {
-    const int sw = wave * SPW + q;
-    // this lane's two largest logits of the sub-chunk, by order of value (a later logit
-    // replaces an equal one only if larger: the lower flat index wins ties)
-    uint32_t o1 = 0, o2 = 0;
-    int i1 = 0, i2 = 0;
-#pragma unroll
-    for (int i = 0; i < kChunkPer; ++i) {
-      const int v = v0 + i * kChunkThreads + sw * 64 + lane;
-      m = fmaxf(m, x[q][i]);
-      // (the end-of-sequence token, if any, is not a candidate for the next beams;
-      // order 0 = no candidate)
-      const uint32_t o = v < V && v != s.eos ? ord_raw(x[q][i]) : 0u;
-      const bool gt1 = o > o1, gt2 = o > o2;
-      o2 = gt1 ? o1 : (gt2 ? o : o2);
-      i2 = gt1 ? i1 : (gt2 ? i : i2);
-      o1 = gt1 ? o : o1;
-      i1 = gt1 ? i : i1;
-    }
-    const uint32_t flat = (uint32_t)r * (uint32_t)V + (uint32_t)(v0 + sw * 64 + lane);
-    const uint64_t k1 = o1 ? ((uint64_t)o1 << 32) | (uint64_t)(0xffffffffu - (flat + (uint32_t)(i1 * kChunkThreads))) : 0;
-    const uint64_t k2 = o2 ? ((uint64_t)o2 << 32) | (uint64_t)(0xffffffffu - (flat + (uint32_t)(i2 * kChunkThreads))) : 0;
-    // the sub-chunk's largest key, and its second largest (the owner of the largest offers
-    // its own second; keys are unique)
-    const uint64_t km = wave_max_u64(k1);
-    const uint64_t km2 = wave_max_u64(k1 == km ? k2 : k1);
-    if (lane == 0) {
-      s.topk_keys[sw * lists + list] = km;  // 0 when the sub-chunk holds no candidate
-      s.topk_keys[s.topk_half + sw * lists + list] = km2;
-    }
-  }
-  m = __ockl_wfred_max_f32(m);
-  if (lane == 0) wm[wave] = m;
-  __syncthreads();
-  m = wm[0];
-#pragma unroll
-  for (int w = 1; w < NWC; ++w) m = fmaxf(m, wm[w]);
-  const double md = (double)m;
   double acc = 0.0;
   bool bad = false;  // a NaN or +inf logit
-#pragma unroll
-  for (int q = 0; q < SPW; ++q)
-#pragma unroll
-    for (int i = 0; i < kChunkPer; ++i) {
-      const int v = v0 + i * kChunkThreads + (wave * SPW + q) * 64 + lane;
-      // (a chunk whose logits are all -inf adds nothing; exp(-inf - -inf) would be NaN)
-      if (v < V && md != -INFINITY) acc += exp_nonpos((double)x[q][i] - md, exp_tab);
-      bad |= v < V && !(x[q][i] < INFINITY);
-    }
+  if (v0 + kLseChunk <= V && (s.eos < v0 || s.eos >= v0 + kLseChunk))
+    body(std::true_type{}, m, acc, bad);
+  else
+    body(std::false_type{}, m, acc, bad);
+  const double md = (double)m;  // (the chunk's maximum)
   // an invalid logit poisons the chunk's sum: the row's lse is then NaN and the call
   // reports the row (k_topb_final)
   if (bad) acc = __builtin_nan("");
