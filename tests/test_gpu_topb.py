@@ -174,10 +174,13 @@ def test_single_row_all_but_a_few_masked_llama_vocab():
     run_topb(b, row, np.array([0.0], np.float32))
 
 
-@pytest.mark.parametrize("bad", ["all_masked", "nan", "pos_inf"])
+@pytest.mark.parametrize("bad", ["all_masked", "nan", "pos_inf", "nan_full_chunk", "neg_nan_full_chunk",
+                                 "nan_only_chunk"])
 def test_live_row_without_a_valid_distribution_is_rejected(bad):
     """A live row with no finite logit, or with a NaN or +inf one, is invalid input: the
-    device status reports TD_EINVAL, and the fused call leaves the trie as it was."""
+    device status reports TD_EINVAL, and the fused call leaves the trie as it was.  The bad
+    logit sits in the full first chunk (4096 logits, the chunk pass's fast path) or in the
+    tail chunk; a chunk of NaNs only has no finite maximum."""
     import torch
     import paper_2502_00085_amd.binding as B
     b, V, P, n_live = 4, 5000, 5, 3
@@ -192,6 +195,12 @@ def test_live_row_without_a_valid_distribution_is_rejected(bad):
             full[1] = -np.inf
         elif bad == "nan":
             full[2, 4100] = np.nan
+        elif bad == "nan_full_chunk":
+            full[2, 100] = np.nan
+        elif bad == "neg_nan_full_chunk":
+            full[1, 3000] = np.array([0xFFC00000], np.uint32).view(np.float32)[0]
+        elif bad == "nan_only_chunk":
+            full[0, :4096] = np.nan
         else:
             full[0, 7] = np.inf
         lg = torch.from_numpy(full).reshape(1, b, V).cuda()
