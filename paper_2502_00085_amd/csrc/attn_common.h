@@ -43,7 +43,11 @@ __device__ inline AttnUnit attn_unit(const DevState& s, const AttnArgs& a) {
 // depth[n] > D - W.  Block-parallel (call from uniform control flow, every thread).
 __device__ inline int window_lo(const DevState& s, int t, int base, int N, int D, int* scratch) {
   if (s.W <= 0) return 0;
-  return block_first_above(s.depth + (size_t)t * s.cap + base, N, D - s.W, scratch);
+  const int32_t* dep = s.depth + (size_t)t * s.cap + base;
+  // (the first slot holds the smallest depth: when it is inside the window, as after a
+  // collection that evicted every node outside it, so is every slot; one load, no search)
+  if (N == 0 || dep[0] > D - s.W) return 0;
+  return block_first_above(dep, N, D - s.W, scratch);
 }
 __device__ inline int window_lo(const DevState& s, int t, int base, int N, int D) {
   __shared__ int scratch[16];
