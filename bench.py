@@ -41,8 +41,8 @@ HBM_PEAK_GBS = 8000.0
 ATTN_TRAFFIC = {
     "workload": "llama8b",
     "profile": "profiles/k_attn_mfma_llama8b_hbm_traffic.md",
-    "sources_sha256": "0f36f0e8151a803254c5dbbc97974a9e36e409d64300c828288f537c7e6c1110",
-    "bytes_per_launch": 275909760,    # 2.0 x 133,697.56 KiB FETCH_SIZE + 1.0 x 2,048 KiB WRITE_SIZE
+    "sources_sha256": "12172a5f2ef2a90359db65d4b5706061ef5ffcc90abb1cee13c29720fb7b8058",
+    "bytes_per_launch": 275921856,    # 2.0 x 133,703.47 KiB FETCH_SIZE + 1.0 x 2,048 KiB WRITE_SIZE
     "nodes_per_launch": 2070,         # attended nodes of the profiled (step-10) trie
     "qo_bytes_per_launch": 4194304,   # queries + outputs of the profiled launch
 }
