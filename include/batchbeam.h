@@ -53,7 +53,8 @@ typedef struct {
   int32_t n_layers;     /* L >= 1                                                          */
   int32_t n_q_heads;    /* Hq, a multiple of Hkv                                           */
   int32_t n_kv_heads;   /* Hkv >= 1                                                        */
-  int32_t head_dim;     /* d in {64, 96, 128}                                              */
+  int32_t head_dim;     /* d: a multiple of 32 in [32, 256] (the matrix-core kernel at 64, */
+                        /*   96 and 128 in bf16, else the vector-ALU kernel)              */
   int32_t window;       /* sliding window W (0 = dense): position p visible iff D - p < W */
   int32_t dtype;        /* td_dtype of the caches, q, out, k_new, v_new                    */
   int32_t attn_impl;    /* td_attn_impl                                                    */

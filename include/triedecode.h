@@ -70,8 +70,10 @@ typedef enum {
 
 typedef enum { TD_F32 = 0, TD_BF16 = 1 } td_dtype;
 
-/* Attention kernel choice: AUTO = bf16 -> matrix-core (MFMA) kernel, fp32 -> vector-ALU
- * kernel.  VALU / MFMA force one (MFMA requires bf16). */
+/* Attention kernel choice: AUTO = bf16 at head_dim 64, 96 or 128 -> matrix-core (MFMA)
+ * kernel, otherwise (fp32, or another head_dim) the vector-ALU kernel.  VALU / MFMA force
+ * one (MFMA requires bf16 and head_dim 64, 96 or 128, else td_create returns
+ * TD_EUNSUPPORTED). */
 typedef enum { TD_ATTN_AUTO = 0, TD_ATTN_VALU = 1, TD_ATTN_MFMA = 2 } td_attn_impl;
 
 typedef struct {
@@ -82,8 +84,9 @@ typedef struct {
   int32_t n_layers;     /* L >= 1                                                         */
   int32_t n_q_heads;    /* Hq, a multiple of Hkv                                          */
   int32_t n_kv_heads;   /* Hkv >= 1                                                       */
-  int32_t head_dim;     /* d: a multiple of 32 in [32, 256] (else TD_EINVAL); the kernels */
-                        /*   implement 64, 96 and 128 (others: TD_EUNSUPPORTED)          */
+  int32_t head_dim;     /* d: a multiple of 32 in [32, 256] (else TD_EINVAL); the matrix- */
+                        /*   core kernels implement 64, 96 and 128, the vector-ALU       */
+                        /*   kernel every d                                              */
   int32_t window;       /* sliding window W (0 = dense): key visible iff D - depth < W    */
   int32_t dtype;        /* td_dtype of pools, q, out, k_new, v_new                        */
   int32_t attn_impl;    /* td_attn_impl                                                   */
@@ -162,7 +165,8 @@ td_status trie_attn_decode(td_ctx* ctx, int32_t layer_begin, int32_t n_layers, c
  * (desc.dtype), layers [layer_begin, +n_layers).  A row with no query, or whose node lies
  * on no live leaf's path (a dead node awaiting collection), is written as zeros.  Every
  * node's K/V must be in the pools: TD_ESTATE while the leaves' rows are pending.  Needs the
- * matrix-core kernel (bf16, attn_impl != TD_ATTN_VALU), else TD_EUNSUPPORTED.  q_max >= 1
+ * matrix-core kernels (bf16, head_dim 64, 96 or 128, attn_impl != TD_ATTN_VALU), else
+ * TD_EUNSUPPORTED.  q_max >= 1
  * and q_max * (Hq/Hkv) <= 2^24, else TD_EINVAL.  Query sets of at least 128 rows
  * (q_max * Hq/Hkv) run on a prefill-shaped kernel (128 rows per workgroup, the key range
  * streamed once for all of them); smaller ones on the decode layout with node splits. */

@@ -10,8 +10,10 @@
 // per-row online softmax.  Groups, waves and (if the node axis is split over WGs) splits
 // are merged by the usual max/sum rescaling.
 //
-// Used for fp32 (cache-resident tiny shapes) and as the cross-check of the bf16
-// matrix-core kernel.
+// Used for fp32 (cache-resident tiny shapes), for the head dims the matrix-core kernel
+// does not implement (any multiple of 32 up to 256; blocks of 4 rows past d = 128, so that
+// the rows' query and output registers stay within the register file), and as the
+// cross-check of the bf16 matrix-core kernel.
 #include "attn_common.h"
 
 namespace td {
@@ -21,8 +23,8 @@ namespace {
 template <typename T> __device__ inline float to_f(T x) { return (float)x; }
 template <typename T> __device__ inline T from_f(float x) { return (T)x; }
 
-constexpr int kValuRows = 8;
 constexpr int kValuThreads = 256;
+constexpr int valu_rows(int d) { return d > 128 ? 4 : 8; }  // query rows per block
 constexpr float kNegBig = -1.0e30f;
 
 template <typename T, int EPL>
@@ -41,8 +43,8 @@ __device__ inline void merge_state(float& m, float& l, float m2, float l2, float
 
 template <typename T, int EPL>
 __global__ __launch_bounds__(kValuThreads) void k_attn_valu(DevState s, AttnArgs a) {
-  constexpr int R = kValuRows;
   constexpr int DD = 16 * EPL;
+  constexpr int R = valu_rows(DD);
   const AttnUnit u = attn_unit(s, a);
   const TrieHdr h = s.hdr[u.t];
   const int N = h.n_nodes, base = h.base, n_live = h.n_live, Dq = h.leaf_depth;
@@ -196,9 +198,10 @@ hipError_t launch_t(const DevState& s, const AttnArgs& a, dim3 grid, hipStream_t
                     hipEvent_t ev1) {
   const dim3 block(kValuThreads);
   switch (s.D) {
-    case 64: hipExtLaunchKernelGGL((k_attn_valu<T, 4>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
-    case 96: hipExtLaunchKernelGGL((k_attn_valu<T, 6>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
-    case 128: hipExtLaunchKernelGGL((k_attn_valu<T, 8>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
+#define VALU_CASE(DD) \
+    case DD: hipExtLaunchKernelGGL((k_attn_valu<T, DD / 16>), grid, block, 0, st, ev0, ev1, 0, s, a); break;
+    VALU_CASE(32) VALU_CASE(64) VALU_CASE(96) VALU_CASE(128) VALU_CASE(160) VALU_CASE(192) VALU_CASE(224) VALU_CASE(256)
+#undef VALU_CASE
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -206,7 +209,7 @@ hipError_t launch_t(const DevState& s, const AttnArgs& a, dim3 grid, hipStream_t
 
 }  // namespace
 
-int attn_valu_rows_per_block() { return kValuRows; }
+int attn_valu_rows_per_block(int d) { return valu_rows(d); }
 
 hipError_t launch_attn_valu(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
                             hipEvent_t ev1) {

@@ -90,8 +90,8 @@ td_status bbs_create(const bbs_desc* d, bbs_ctx** out) {
     return bfail(nullptr, TD_EUNSUPPORTED, "beam_width * ceil(vocab / 4096) must be <= %d", td::topb_max_chunk_lists());
   if (d->n_layers < 1 || d->n_kv_heads < 1 || d->n_q_heads < d->n_kv_heads || d->n_q_heads % d->n_kv_heads != 0)
     return bfail(nullptr, TD_EINVAL, "need n_layers >= 1, n_kv_heads >= 1, n_q_heads %% n_kv_heads == 0");
-  if (d->head_dim != 64 && d->head_dim != 96 && d->head_dim != 128)
-    return bfail(nullptr, TD_EUNSUPPORTED, "head_dim must be 64, 96 or 128");
+  if (d->head_dim < 32 || d->head_dim > 256 || d->head_dim % 32 != 0)
+    return bfail(nullptr, TD_EINVAL, "head_dim must be a multiple of 32 in [32, 256]");
   if (d->capacity < 2 || d->capacity > (1 << 30)) return bfail(nullptr, TD_EINVAL, "capacity must be in [2, 2^30]");
   if ((int64_t)d->n_requests * d->beam_width * d->capacity >= (int64_t(1) << 31))
     return bfail(nullptr, TD_EINVAL, "n_requests * beam_width * capacity must be < 2^31");
@@ -99,6 +99,8 @@ td_status bbs_create(const bbs_desc* d, bbs_ctx** out) {
   if (d->dtype != TD_F32 && d->dtype != TD_BF16) return bfail(nullptr, TD_EINVAL, "bad dtype");
   if (d->attn_impl < TD_ATTN_AUTO || d->attn_impl > TD_ATTN_MFMA) return bfail(nullptr, TD_EINVAL, "bad attn_impl");
   if (d->attn_impl == TD_ATTN_MFMA && d->dtype != TD_BF16) return bfail(nullptr, TD_EUNSUPPORTED, "the matrix-core kernel needs bf16");
+  if (d->attn_impl == TD_ATTN_MFMA && !td::mfma_head_dim(d->head_dim))
+    return bfail(nullptr, TD_EUNSUPPORTED, "the matrix-core kernel implements head_dim 64, 96 and 128");
   for (int i = 0; i < 2; ++i)
     if (!d->k_cache[i] || !d->v_cache[i] || !al16(d->k_cache[i]) || !al16(d->v_cache[i]))
       return bfail(nullptr, TD_EINVAL, "k_cache / v_cache buffers must be non-null and 16-byte aligned");
@@ -235,7 +237,7 @@ td_status batch_beam_attn_decode(bbs_ctx* c, int32_t layer_begin, int32_t n_laye
   if (!c->pending && (d_k_new || d_v_new)) return bfail(c, TD_EINVAL, "no K/V is pending (after init): pass NULL k_new / v_new");
   if (c->pending && (!al16(d_k_new) || !al16(d_v_new))) return bfail(c, TD_EINVAL, "k_new / v_new must be 16-byte aligned");
   if (!(scale > 0.0f) || !std::isfinite(scale)) return bfail(c, TD_EINVAL, "scale must be finite and > 0");
-  const bool mfma = s.dtype == TD_BF16 && c->desc.attn_impl != TD_ATTN_VALU;
+  const bool mfma = s.dtype == TD_BF16 && c->desc.attn_impl != TD_ATTN_VALU && td::mfma_head_dim(s.D);
   td::AttnArgs a{};
   a.q = d_q;
   a.k_new = d_k_new;
@@ -246,7 +248,7 @@ td_status batch_beam_attn_decode(bbs_ctx* c, int32_t layer_begin, int32_t n_laye
   a.scale_log2 = scale * 1.4426950408889634f;
   a.kv_pending = c->pending ? 1 : 0;
   a.moves = 0;
-  const int rpb = mfma ? td::attn_mfma_rows_per_block() : td::attn_valu_rows_per_block();
+  const int rpb = mfma ? td::attn_mfma_rows_per_block() : td::attn_valu_rows_per_block(s.D);
   a.row_blocks = (s.Hq / s.Hkv + rpb - 1) / rpb;
   a.row_blocks32 = a.row_blocks;
   a.splits = td::attn_choose_splits(s, n_layers, a.row_blocks);

@@ -112,8 +112,6 @@ td_status td_create(const td_desc* d, td_ctx** out) {
     return fail(nullptr, TD_EINVAL, "need n_layers >= 1, n_kv_heads >= 1, n_q_heads %% n_kv_heads == 0");
   if (d->head_dim < 32 || d->head_dim > 256 || d->head_dim % 32 != 0)
     return fail(nullptr, TD_EINVAL, "head_dim must be a multiple of 32 in [32, 256]");
-  if (d->head_dim != 64 && d->head_dim != 96 && d->head_dim != 128)
-    return fail(nullptr, TD_EUNSUPPORTED, "the kernels implement head_dim 64, 96 and 128");
   if (d->capacity < d->beam_width + 1 || d->capacity > (1 << 30))
     return fail(nullptr, TD_EINVAL, "capacity must be in [beam_width + 1, 2^30]");
   if (d->window < 0) return fail(nullptr, TD_EINVAL, "window must be >= 0");
@@ -129,6 +127,8 @@ td_status td_create(const td_desc* d, td_ctx** out) {
     return fail(nullptr, TD_EINVAL, "bad attn_impl");
   if (d->attn_impl == TD_ATTN_MFMA && d->dtype != TD_BF16)
     return fail(nullptr, TD_EUNSUPPORTED, "the matrix-core kernel needs bf16");
+  if (d->attn_impl == TD_ATTN_MFMA && !td::mfma_head_dim(d->head_dim))
+    return fail(nullptr, TD_EUNSUPPORTED, "the matrix-core kernel implements head_dim 64, 96 and 128");
   if (!d->k_pool || !d->v_pool || !aligned16(d->k_pool) || !aligned16(d->v_pool))
     return fail(nullptr, TD_EINVAL, "k_pool / v_pool must be non-null and 16-byte aligned");
 
@@ -241,7 +241,7 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   if (c->pending && (!aligned16(d_k_new) || !aligned16(d_v_new)))
     return fail(c, TD_EINVAL, "k_new / v_new must be 16-byte aligned");
   if (!(scale > 0.0f) || !std::isfinite(scale)) return fail(c, TD_EINVAL, "scale must be finite and > 0");
-  const bool mfma = s.dtype == TD_BF16 && c->desc.attn_impl != TD_ATTN_VALU;
+  const bool mfma = s.dtype == TD_BF16 && c->desc.attn_impl != TD_ATTN_VALU && td::mfma_head_dim(s.D);
   td::AttnArgs a{};
   a.q = d_q;
   a.k_new = d_k_new;
@@ -251,7 +251,7 @@ td_status trie_attn_decode(td_ctx* c, int32_t layer_begin, int32_t n_layers, con
   a.n_layers = n_layers;
   a.scale_log2 = scale * 1.4426950408889634f;
   a.kv_pending = c->pending ? 1 : 0;
-  const int rpb = mfma ? td::attn_mfma_rows_per_block() : td::attn_valu_rows_per_block();
+  const int rpb = mfma ? td::attn_mfma_rows_per_block() : td::attn_valu_rows_per_block(s.D);
   a.row_blocks = (s.b * (s.Hq / s.Hkv) + rpb - 1) / rpb;
   a.row_blocks32 = a.row_blocks;
   if (mfma && a.row_blocks == 2) {  // b G in (32, 64]: one WG over both row blocks
@@ -336,8 +336,8 @@ td_status trie_tree_attn(td_ctx* c, int32_t layer_begin, int32_t n_layers, int32
   if (!d_qslots || !d_q || !d_out || !aligned16(d_q) || !aligned16(d_out))
     return fail(c, TD_EINVAL, "qslots, q and out must be non-null (q, out 16-byte aligned)");
   if (!(scale > 0.0f) || !std::isfinite(scale)) return fail(c, TD_EINVAL, "scale must be finite and > 0");
-  if (s.dtype != TD_BF16 || c->desc.attn_impl == TD_ATTN_VALU)
-    return fail(c, TD_EUNSUPPORTED, "tree attention runs on the matrix-core kernel (bf16)");
+  if (s.dtype != TD_BF16 || c->desc.attn_impl == TD_ATTN_VALU || !td::mfma_head_dim(s.D))
+    return fail(c, TD_EUNSUPPORTED, "tree attention runs on the matrix-core kernels (bf16, head_dim 64, 96 or 128)");
   if (c->pending) return fail(c, TD_ESTATE, "the leaves' K/V are pending: run trie_attn_decode first");
   td::AttnArgs a{};
   a.q = d_q;

@@ -119,6 +119,9 @@ struct AttnArgs {
 
 hipError_t launch_init_prompt(const DevState& s, const int32_t* d_plen, const int32_t* d_tokens,
                               int stride, hipStream_t st);
+// Head dims the matrix-core kernels implement (the vector-ALU kernel takes any multiple of
+// 32 up to 256).
+inline bool mfma_head_dim(int d) { return d == 64 || d == 96 || d == 128; }
 // The launchers take optional kernel-timestamp events (hipExtLaunchKernel): ev0 records
 // the dispatch of the first launched kernel, ev1 the completion of the last (null = none).
 hipError_t launch_attn_mfma(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
@@ -131,7 +134,7 @@ int attn_mfma_rows_per_block();
 int attn_tree_rows_per_block();
 hipError_t launch_attn_tree(const DevState& s, const AttnArgs& a, hipStream_t st, hipEvent_t ev0,
                             hipEvent_t ev1);
-int attn_valu_rows_per_block();
+int attn_valu_rows_per_block(int d);  // query rows per block at head dim d
 int attn_choose_splits(const DevState& s, int n_layers, int row_blocks);
 hipError_t launch_logsoftmax_topk(const DevState& s, const float* logits, int32_t* sel_parent,
                                   int32_t* sel_token, float* sel_score, float* sel_logprob,

@@ -69,17 +69,18 @@ def test_create_rejects_bad_descriptors(kw, frag):
     assert frag in L.td_error_string(None).decode()
 
 
-@pytest.mark.parametrize("d,want", [(80, "TD_EINVAL"), (16, "TD_EINVAL"), (288, "TD_EINVAL"), (0, "TD_EINVAL"),
-                                    (32, "TD_EUNSUPPORTED"), (160, "TD_EUNSUPPORTED"),
-                                    (192, "TD_EUNSUPPORTED"), (224, "TD_EUNSUPPORTED"),
-                                    (256, "TD_EUNSUPPORTED")])
-def test_head_dim_outside_the_kernels(d, want):
-    """The boundary takes d as a multiple of 32 up to 256; other values are invalid, and the
-    kernels implement 64, 96 and 128 of the valid ones (the rest: unsupported).  Both are
-    rejected by td_create, before anything is allocated."""
+@pytest.mark.parametrize("d,impl,want", [(80, 0, "TD_EINVAL"), (16, 0, "TD_EINVAL"), (288, 0, "TD_EINVAL"),
+                                         (0, 0, "TD_EINVAL"), (32, 2, "TD_EUNSUPPORTED"),
+                                         (160, 2, "TD_EUNSUPPORTED"), (192, 2, "TD_EUNSUPPORTED"),
+                                         (224, 2, "TD_EUNSUPPORTED"), (256, 2, "TD_EUNSUPPORTED")])
+def test_head_dim_outside_the_kernels(d, impl, want):
+    """The boundary takes d as a multiple of 32 up to 256; other values are invalid.  The
+    matrix-core kernels implement 64, 96 and 128, so forcing them (attn_impl = MFMA) at
+    another valid d is unsupported; the vector-ALU kernel takes every valid d.  Both errors
+    come from td_create, before anything is allocated."""
     L = B.lib()
     ctx = ctypes.c_void_p()
-    st = L.td_create(ctypes.byref(_desc(head_dim=d)), ctypes.byref(ctx))
+    st = L.td_create(ctypes.byref(_desc(head_dim=d, attn_impl=impl)), ctypes.byref(ctx))
     assert st == getattr(B, want), (d, L.td_status_name(st))
     assert ctx.value is None
     assert "head_dim" in L.td_error_string(None).decode()

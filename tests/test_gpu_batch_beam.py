@@ -53,6 +53,13 @@ def test_several_requests_ragged_prompts():
     run_batch(small(n_tries=3, prompt_min=17, prompt_max=90, beam_width=4, steps=6), seed=4)
 
 
+@pytest.mark.parametrize("d", [32, 192])
+def test_head_dims_on_the_vector_alu_kernel(d):
+    # (bf16 outside the matrix-core kernels' head dims: the vector-ALU kernel)
+    run_batch(small(n_q_heads=8, n_kv_heads=2, head_dim=d, prompt_min=40, prompt_max=40, beam_width=4,
+                    steps=6, qkv_std=1.0 / np.sqrt(d)), seed=7 + d)
+
+
 def test_greedy_single_beam():
     run_batch(small(beam_width=1, steps=6), seed=5, mode="driven")
 

@@ -313,6 +313,26 @@ def test_one_row_block_half_wgs_window_deferred_collection_fused():
                    qkv_std=1.0 / np.sqrt(96.0), steps=12), seed=85, fused=True)
 
 
+# head dims outside the matrix-core kernels' 64, 96 and 128 run on the vector-ALU kernel
+# (bf16 storage, fp32 arithmetic; 4-row blocks past d = 128)
+@pytest.mark.parametrize("d", [32, 160, 192, 224, 256])
+def test_head_dims_on_the_vector_alu_kernel(d):
+    run_case(small(n_layers=2, n_q_heads=8, n_kv_heads=2, head_dim=d, beam_width=4, prompt_min=40,
+                   prompt_max=40, vocab=400, qkv_std=1.0 / np.sqrt(d), steps=6), seed=90 + d)
+
+
+def test_head_dim_256_fp32_window_splits_layer_calls():
+    layer_case(small(n_layers=3, n_q_heads=8, n_kv_heads=2, head_dim=256, dtype="f32", beam_width=6,
+                     prompt_min=60, prompt_max=60, vocab=500, window=30, gc_interval=2,
+                     qkv_std=1.0 / np.sqrt(256.0), steps=8), seed=97, calls=[0, 1, 3])
+
+
+def test_head_dim_32_several_tries_fused():
+    run_case(small(n_tries=3, n_layers=2, n_q_heads=4, n_kv_heads=4, head_dim=32, beam_width=8,
+                   prompt_min=10, prompt_max=50, vocab=300, alpha=0.0, qkv_std=1.0 / np.sqrt(32.0), steps=8),
+             seed=98, fused=True)
+
+
 @pytest.mark.parametrize("mode", ["driven", "scripted"])
 def test_smallest_vocabulary(mode):
     # V = b: at step 1 every candidate is selected; afterwards b of b * b

@@ -218,8 +218,14 @@ def test_tree_attn_rejects_bad_arguments():
     assert L.trie_tree_attn(*args(4, qs.data_ptr(), q.data_ptr(), out.data_ptr(), 1.0)) == B.TD_OK
     torch.cuda.synchronize()
     r.dec.close()
-    # the vector-ALU kernel and fp32 have no tree variant
+    # the vector-ALU kernel and fp32 have no tree variant, nor has a head dim outside the
+    # matrix-core kernels' 64, 96 and 128 (bf16 at d = 160 runs its decode on the vector ALU)
     r2 = Run(synth.WORKLOADS["tiny"], 0, oracle=False)
     assert L.trie_tree_attn(r2.dec.ctx, 0, 1, 4, qs.data_ptr(), q.data_ptr(), out.data_ptr(), 1.0,
                             None) == B.TD_EUNSUPPORTED
     r2.dec.close()
+    r3 = Run(small(steps=2, n_layers=1, head_dim=160), 0, oracle=False)
+    assert L.trie_tree_attn(r3.dec.ctx, 0, 1, 4, qs.data_ptr(), q.data_ptr(), out.data_ptr(), 1.0,
+                            None) == B.TD_EUNSUPPORTED
+    assert "head_dim" in B.td_error_string(r3.dec.ctx)
+    r3.dec.close()
