@@ -293,6 +293,7 @@ def gpu_bench(args, w, K):
     finished = [bench.dec.read_finished(t) for t in range(w.n_tries)] if args.eos >= 0 else None
     attn_graph_ms, attn_graph_nodes = attn_graph_time(bench, K, args.attn_reps)
     attn_cold_ms = attn_cold_time(bench, args.cold_reps)
+    step_cold_ms = None if args.eager else step_cold_time(bench, K)
     per_layer_ms = attn_per_layer_time(bench, max(4, args.attn_reps // 4))
     probe = read_probe_cold(bench.B, float(sum(attn_graph_nodes)) * w.node_bytes, args.cold_reps)
     copy_gbs = device_copy_gbs()
@@ -305,7 +306,8 @@ def gpu_bench(args, w, K):
     return dict(mode=mode, seconds=float(np.median(run_s)), run_seconds=run_s, eager_seconds=eager_s,
                 attn_ms=attn_ms, nodes=nodes,
                 attn_graph_ms=attn_graph_ms, attn_graph_nodes=attn_graph_nodes, phase_ms=phase_ms,
-                attn_cold_ms=attn_cold_ms, per_layer_ms=per_layer_ms, copy_gbs=copy_gbs, probe=probe,
+                attn_cold_ms=attn_cold_ms, step_cold_ms=step_cold_ms, per_layer_ms=per_layer_ms,
+                copy_gbs=copy_gbs, probe=probe,
                 collects=collects, stored=bench.stored, batch=batch, finished=finished, tree=tree,
                 qo_bytes=int(bench.q[0].numel() * bench.q[0].element_size() +
                              bench.out.numel() * bench.out.element_size()))
@@ -502,6 +504,44 @@ def attn_cold_time(bench, reps):
     ev.close()
     del flush
     return float(np.median(ms))
+
+
+def step_cold_time(bench, K):
+    """Whole decode steps with the last-level cache cleared: step i of the run is captured in
+    a graph of its own (the launches of the timed region's step i), and the run is replayed
+    one step at a time, each step after a 1 GiB read (four times the 256 MB cache) outside
+    its timed interval, then again without the read.  Each step is timed by events on the
+    replay stream around its graph launch (so one graph launch is inside every figure).
+    Returns (cold, warm) median ms per step over the K steps."""
+    import torch
+    cs = torch.cuda.Stream()
+    graphs = []
+    bench.init()
+    for i in range(K):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cs):
+            bench.step(i, torch.cuda.current_stream().cuda_stream)
+        graphs.append(g)
+    flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    med = {}
+    for cold in (True, False):
+        bench.init()
+        ms = []
+        for i in range(K):
+            if cold:
+                float(flush.sum())  # (waits for the read)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            with torch.cuda.stream(cs):
+                e0.record()
+                graphs[i].replay()
+                e1.record()
+            e1.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        med[cold] = float(np.median(ms))
+    if bench.dec.status() != 0:
+        raise RuntimeError("device status after the cold steps")
+    del flush, graphs
+    return med[True], med[False]
 
 
 def read_probe_cold(B, nbytes, reps):
@@ -774,6 +814,15 @@ def main():
                                     "step"},
         "hbm_gbps_unique_kv_whole_step": round(float(kv_bytes.mean() / (ms_per_step / 1e3) / 1e9), 1),
         "eager_ms_per_step": round(r["eager_seconds"] * 1e3 / K, 5),
+        **({} if r["step_cold_ms"] is None else {
+            "step_us_llc_cold": round(r["step_cold_ms"][0] * 1e3, 2),
+            "step_us_single_graph": round(r["step_cold_ms"][1] * 1e3, 2),
+            "step_us_cold_in_run": round(ms_per_step * 1e3 + (r["step_cold_ms"][0] - r["step_cold_ms"][1]) * 1e3, 2),
+            "step_cold": "each step of the run as a graph of its own, replayed one at a time after a 1 GiB "
+                         "read has cleared the last-level cache (median over the steps; one graph launch "
+                         "inside each figure); step_us_single_graph: the same replays without the read; "
+                         "step_us_cold_in_run: the timed run's step time plus that cold-minus-warm "
+                         "difference"}),
         "nodes_per_step_mean": round(float(r["nodes"].sum(axis=1).mean()), 1),
         "gc": gc_summary(w, r["phase_ms"], r["collects"]),
     }
