@@ -41,8 +41,8 @@ HBM_PEAK_GBS = 8000.0
 ATTN_TRAFFIC = {
     "workload": "llama8b",
     "profile": "profiles/k_attn_mfma_llama8b_hbm_traffic.md",
-    "sources_sha256": "12172a5f2ef2a90359db65d4b5706061ef5ffcc90abb1cee13c29720fb7b8058",
-    "bytes_per_launch": 275921856,    # 2.0 x 133,703.47 KiB FETCH_SIZE + 1.0 x 2,048 KiB WRITE_SIZE
+    "sources_sha256": "4d86f010c7daef700e6cd9f81802af3406a142bbe7ab1b8e5c48e919a2cc657b",
+    "bytes_per_launch": 275921664,    # 2.0 x 133,703.38 KiB FETCH_SIZE + 1.0 x 2,048 KiB WRITE_SIZE
     "nodes_per_launch": 2070,         # attended nodes of the profiled (step-10) trie
     "qo_bytes_per_launch": 4194304,   # queries + outputs of the profiled launch
 }
