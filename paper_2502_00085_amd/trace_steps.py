@@ -7,7 +7,9 @@ the timed graph replay of bench.py) into decode steps at each attention launch, 
 the decode pass (attention + top-b) against the garbage collection (the append kernel of a
 collecting step plus the row copy launched before the next attention), overall and per
 tenth of the run: the comparison of the paper's Figure 4 (Section 5.3).  A step collects
-when the position after its new leaves, P + step, is a multiple of g (Alg 2).
+when the position after its new leaves, P + step, is a multiple of g (Alg 2).  In a run of
+fused steps (the append inside the selection's merge kernel) the append has no launch of its
+own: the merge kernel's time on collecting steps is compared with the other steps instead.
 """
 from __future__ import annotations
 
@@ -38,7 +40,7 @@ def steps_of(path: str, run: int):
         if k == "k_move_rows":
             move += us
         elif k in ("k_attn_mfma", "k_attn_valu"):
-            cur = dict(attn=us, move=move, topb=0.0, append=0.0)
+            cur = dict(attn=us, move=move, topb=0.0, append=0.0, fused=0.0)
             move = 0.0
             steps.append(cur)
         elif cur is None:
@@ -47,6 +49,8 @@ def steps_of(path: str, run: int):
             cur["attn"] += us
         elif k in ("k_topb_chunk", "k_topb_final"):
             cur["topb"] += us
+            if k == "k_topb_final" and "true>" in r["Kernel_Name"]:
+                cur["fused"] += us
         elif k == "k_append_prune":
             cur["append"] += us
     return steps
@@ -71,12 +75,25 @@ def main():
     idx = np.nonzero(col)[0]
     print(f"steps {K}, collections {len(idx)}")
     print(f"decode pass (attention + top-b): {dec.mean():.2f} us (attention {att.mean():.2f}, top-b {tb.mean():.2f})")
-    if (~col).any():
+    fz = np.array([s["fused"] for s in st])
+    fused = bool(fz.any()) and not app.any()
+    if fused and len(idx) and (~col).any():
+        # the collection's share of a fused merge: its extra time on collecting steps
+        extra = max(0.0, float(fz[col].mean() - fz[~col].mean()))
+        gc = np.array([(extra if col[i] else 0.0) + mv[i + 1] for i in range(K)])
+        print(f"fused selection + append kernel: {fz[col].mean():.2f} us on collecting steps, "
+              f"{fz[~col].mean():.2f} us on the others")
+    elif (~col).any():
         print(f"append kernel, no collection: {app[~col].mean():.2f} us")
     if len(idx):
         copies = [mv[i + 1] for i in idx if i + 1 < K]
-        print(f"append kernel, collecting: {app[col].mean():.2f} us; row copy after it: {np.mean(copies):.2f} us")
-        print(f"collection (append + copy): {gc[col].mean():.2f} us = {gc[col].mean() / dec.mean() * 100:.1f} % "
+        what = ("append + copy" if not fused else "the fused merge's extra time + copy" if (~col).any()
+                else "the row copy only: every step collects, so the fused merge's share is not separable")
+        if not fused:
+            print(f"append kernel, collecting: {app[col].mean():.2f} us; row copy after it: {np.mean(copies):.2f} us")
+        else:
+            print(f"row copy after a collecting step: {np.mean(copies):.2f} us")
+        print(f"collection ({what}): {gc[col].mean():.2f} us = {gc[col].mean() / dec.mean() * 100:.1f} % "
               f"of a decode pass; {gc[col].sum() / K / dec.mean() * 100:.2f} % per step")
     print("| steps | decode pass (µs) | collection (µs) |")
     print("|---|---|---|")
